@@ -1,0 +1,464 @@
+"""Pins for the float64 oracle: each check ties it to something other than
+itself (a library routine, a closed form, an invariant the paper states, a
+hand-enumerated trace, or a scalar brute force on tiny inputs)."""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as Fn
+
+from oracle import reflex_oracle as O
+from paper_2607_14695_amd import workloads as WL
+from tests import brute_force
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- generator
+def test_round_bf16_matches_torch():
+    rng = np.random.default_rng(1)
+    x = (rng.standard_normal(100000) * 10 ** rng.uniform(-6, 6, 100000)).astype(np.float32)
+    ours = WL.round_bf16(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(ours, ref)
+
+
+def test_draws_are_keyed_not_ordered():
+    cfg = WL.CONFIGS["tiny_fp32"]
+    a = WL.make_noise(cfg.replace(batch=3), tick=2)
+    b = WL.make_noise(cfg, tick=2, envs=[0])
+    assert np.array_equal(a[0], b[0])
+    assert not np.array_equal(a[0], a[1])
+
+
+# ---------------------------------------------------------------- elementwise
+def test_rmsnorm_zero_modulation_matches_torch():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((7, 33)) * 3
+    eps = 1e-6
+    ours = O.ada_rms_norm(x, np.zeros(33), np.zeros(33), eps)
+    ref = Fn.rms_norm(torch.from_numpy(x), (33,), eps=eps).numpy()
+    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-13)
+
+
+def test_adarms_constant_vector_closed_form():
+    a, eps = 3.5, 1e-6
+    scale = np.linspace(-0.5, 0.5, 16)
+    shift = np.linspace(1.0, 2.0, 16)
+    y = O.ada_rms_norm(np.full(16, a), scale, shift, eps)
+    expect = a / math.sqrt(a * a + eps) * (1.0 + scale) + shift
+    np.testing.assert_allclose(y, expect, rtol=0, atol=1e-14)
+
+
+def test_adarms_scale_only_is_eq2_forward():
+    """mod_mode == scale_only reproduces the Appendix B.3 forward:
+    x * rsqrt(mean(x^2) + eps) * (1 + dense(cond)), dense = Linear-SiLU-Linear."""
+    rng = np.random.default_rng(3)
+    D, C, Hd = 12, 7, 9
+    x = rng.standard_normal((5, D))
+    c = rng.standard_normal(C)
+    w1 = rng.standard_normal((Hd, C)) * 0.3
+    w2 = rng.standard_normal((3 * D, Hd)) * 0.3
+    m = O.modulation(w1, w2, c, D, "scale_only")
+    ours = O.ada_rms_norm(x, m.scale, m.shift, 1e-6)
+    dense = torch.nn.Sequential(torch.nn.Linear(C, Hd, bias=False), torch.nn.SiLU(),
+                                torch.nn.Linear(Hd, D, bias=False)).double()
+    with torch.no_grad():
+        dense[0].weight.copy_(torch.from_numpy(w1))
+        dense[2].weight.copy_(torch.from_numpy(w2[:D]))
+        xt = torch.from_numpy(x)
+        r = xt.pow(2).mean(-1, keepdim=True)
+        ref = (xt * torch.rsqrt(r + 1e-6) * (1 + dense(torch.from_numpy(c)))).numpy()
+    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-13)
+
+
+def test_modulation_matches_torch_sequential():
+    rng = np.random.default_rng(4)
+    D, C, Hd = 6, 5, 11
+    c = rng.standard_normal(C)
+    w1 = rng.standard_normal((Hd, C))
+    w2 = rng.standard_normal((3 * D, Hd))
+    m = O.modulation(w1, w2, c, D, "full")
+    seq = torch.nn.Sequential(torch.nn.Linear(C, Hd, bias=False), torch.nn.SiLU(),
+                              torch.nn.Linear(Hd, 3 * D, bias=False)).double()
+    with torch.no_grad():
+        seq[0].weight.copy_(torch.from_numpy(w1))
+        seq[2].weight.copy_(torch.from_numpy(w2))
+        ref = seq(torch.from_numpy(c)).numpy()
+    np.testing.assert_allclose(np.concatenate([m.scale, m.shift, m.gate]), ref, rtol=0, atol=1e-12)
+
+
+def test_silu_gelu_match_torch():
+    u = np.linspace(-12, 12, 2001)
+    np.testing.assert_allclose(O.silu(u), Fn.silu(torch.from_numpy(u)).numpy(), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(O.gelu_tanh(u), Fn.gelu(torch.from_numpy(u), approximate="tanh").numpy(),
+                               rtol=0, atol=1e-13)
+
+
+def test_timestep_embedding_closed_forms():
+    d = 16
+    e0 = O.timestep_embedding(0.0, d, 4e-3, 4.0)
+    assert np.array_equal(e0, np.concatenate([np.zeros(8), np.ones(8)]))
+    e1 = O.timestep_embedding(1.0, d, 4e-3, 4.0)
+    # slowest frequency has period 4: angle pi/2 at tau = 1
+    assert abs(e1[7] - 1.0) < 1e-15 and abs(e1[15]) < 1e-15
+    # fastest has period 4e-3: angle 500*pi
+    assert abs(e1[0] - math.sin(2 * math.pi / 4e-3)) < 1e-15
+    # tau = 0.5, middle frequency: period = 4e-3 * 1000^(3/7)
+    p = 4e-3 * 1000 ** (3 / 7)
+    e = O.timestep_embedding(0.5, d, 4e-3, 4.0)
+    assert abs(e[3] - math.sin(math.pi / p)) < 1e-14 and abs(e[11] - math.cos(math.pi / p)) < 1e-14
+
+
+# ---------------------------------------------------------------- RoPE
+def test_rope_complex_form_and_hand_value():
+    rng = np.random.default_rng(5)
+    d, theta = 8, 10000.0
+    z = rng.standard_normal((6, 3, d))
+    pos = np.array([0, 1, 5, 1000, 123456, 381000])
+    ours = O.rope(z, pos, theta)
+    zc = z[..., : d // 2] + 1j * z[..., d // 2:]
+    freq = theta ** (-np.arange(d // 2) * 2.0 / d)
+    rot = zc * np.exp(1j * pos[:, None, None] * freq[None, None, :])
+    ref = np.concatenate([rot.real, rot.imag], axis=-1)
+    np.testing.assert_allclose(ours, ref, rtol=0, atol=1e-12)
+    # hand value, d = 4: theta_0 = 1, theta_1 = 0.01; p = 1
+    out = O.rope(np.array([[1.0, 2.0, 3.0, 4.0]]), np.array([1]), 10000.0)[0]
+    c0, s0, c1, s1 = math.cos(1), math.sin(1), math.cos(0.01), math.sin(0.01)
+    expect = [1 * c0 - 3 * s0, 2 * c1 - 4 * s1, 3 * c0 + 1 * s0, 4 * c1 + 2 * s1]
+    np.testing.assert_allclose(out, expect, rtol=0, atol=1e-15)
+
+
+def test_rope_identity_norm_and_relative_invariance():
+    rng = np.random.default_rng(6)
+    d = 64
+    q = rng.standard_normal((5, d))
+    k = rng.standard_normal((5, d))
+    assert np.array_equal(O.rope(q, np.zeros(5), 1e4), q)
+    p = np.array([3, 70, 500, 9000, 200000])
+    np.testing.assert_allclose(np.linalg.norm(O.rope(q, p, 1e4), axis=-1), np.linalg.norm(q, axis=-1),
+                               rtol=1e-13)
+    pk = np.array([1, 2, 3, 4, 5])
+    for delta in (7, 1000, 54321):
+        a = np.sum(O.rope(q, p, 1e4) * O.rope(k, pk, 1e4), axis=-1)
+        b = np.sum(O.rope(q, p + delta, 1e4) * O.rope(k, pk + delta, 1e4), axis=-1)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-9)
+
+
+# ---------------------------------------------------------------- attention
+def _sdpa(q, K, V, allowed):
+    T, Hq, dh = q.shape
+    Hkv = K.shape[1]
+    Kx = np.repeat(K, Hq // Hkv, axis=1)
+    Vx = np.repeat(V, Hq // Hkv, axis=1)
+    qt = torch.from_numpy(q.transpose(1, 0, 2).copy())
+    kt = torch.from_numpy(Kx.transpose(1, 0, 2).copy())
+    vt = torch.from_numpy(Vx.transpose(1, 0, 2).copy())
+    out = Fn.scaled_dot_product_attention(qt, kt, vt, attn_mask=torch.from_numpy(allowed))
+    return out.numpy().transpose(1, 0, 2)
+
+
+@pytest.mark.parametrize("hq,hkv", [(4, 1), (8, 1), (4, 2)])
+def test_masked_attention_matches_sdpa(hq, hkv):
+    rng = np.random.default_rng(7)
+    T, n_ctx, dh = 9, 23, 16
+    q = rng.standard_normal((T, hq, dh))
+    K = rng.standard_normal((n_ctx + T, hkv, dh))
+    V = rng.standard_normal((n_ctx + T, hkv, dh))
+    allowed = O.dyn_allowed(n_ctx, T)
+    np.testing.assert_allclose(O.masked_attention(q, K, V, allowed), _sdpa(q, K, V, allowed),
+                               rtol=0, atol=1e-12)
+
+
+def test_dyn_mask_shape():
+    a = O.dyn_allowed(5, 4)
+    assert a[:, :5].all()
+    assert a[0, 5] and not a[0, 6:].any()
+    assert a[1:, 5:].all()
+
+
+def test_partitioned_attention_equals_full():
+    """Proposition A.1 at the level of one attention call, random regions."""
+    rng = np.random.default_rng(8)
+    T, dh, hq = 7, 8, 4
+    sizes = [5, 3, 6, 6]
+    q = rng.standard_normal((T, hq, dh))
+    regs, Ks, Vs = [], [], []
+    for n in sizes:
+        K = rng.standard_normal((n, 1, dh)) * 3
+        V = rng.standard_normal((n, 1, dh))
+        regs.append((K, V, np.ones((T, n), dtype=bool)))
+        Ks.append(K)
+        Vs.append(V)
+    Kd = rng.standard_normal((T, 1, dh))
+    Vd = rng.standard_normal((T, 1, dh))
+    regs.append((Kd, Vd, O.dyn_allowed(0, T)))
+    full = O.masked_attention(q, np.concatenate(Ks + [Kd]), np.concatenate(Vs + [Vd]),
+                              O.dyn_allowed(sum(sizes), T))
+    np.testing.assert_allclose(O.partitioned_attention(q, regs), full, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------- ring
+def test_ring_trace_golden():
+    rows = []
+    with open(os.path.join(GOLDEN, "ring_trace_w2_f32_ls64.txt")) as fh:
+        for line in fh:
+            if line.strip() and not line.startswith("#"):
+                rows.append([int(t) for t in line.split()])
+    assert len(rows) == 5
+    for f, slot, p0, p1, nv, ev, dyn in rows:
+        st = O.ring_step(f, 2, 32, 64)
+        assert (st.frame_index, st.slot, st.pos0, st.pos0 + 31, st.n_valid, st.evicted, st.dyn_pos0) == \
+            (f, slot, p0, p1, nv, ev, dyn)
+    assert O.window_frames(5, 2) == [3, 4]
+    assert O.window_frames(1, 2) == [0]
+    assert O.window_frames(0, 2) == []
+
+
+# ---------------------------------------------------------------- Euler
+def test_euler_closed_forms():
+    x0 = np.array([[1.0, -2.0], [0.5, 3.0]])
+    c = np.array([[0.25, 1.0], [-1.0, 2.0]])
+    taus = [1.0, 0.75, 0.5, 0.25, 0.0]
+    np.testing.assert_allclose(O.euler_integrate(lambda x, t: c, x0, taus), x0 - c, rtol=0, atol=1e-15)
+    a = 0.3
+    xk = O.euler_integrate(lambda x, t: a * x, x0, taus)
+    np.testing.assert_allclose(xk, x0 * (1 - a * 0.25) ** 4, rtol=1e-15)
+    # field depending on tau only: v = tau -> x_K = x0 - sum_k tau_k * 0.25
+    xt = O.euler_integrate(lambda x, t: np.full_like(x, t), x0, taus)
+    np.testing.assert_allclose(xt, x0 - 0.25 * (1 + 0.75 + 0.5 + 0.25), rtol=0, atol=1e-15)
+    # non-uniform grid
+    taus2 = [1.0, 0.9, 0.4, 0.0]
+    xk2 = O.euler_integrate(lambda x, t: a * x, x0, taus2)
+    np.testing.assert_allclose(xk2, x0 * (1 - a * 0.1) * (1 - a * 0.5) * (1 - a * 0.4), rtol=1e-15)
+
+
+# ---------------------------------------------------------------- full expert
+def _inputs(cfg, ticks):
+    w = WL.make_weights(cfg)
+    sk, sv = WL.make_static_kv(cfg)
+    frames = {t: WL.make_frame(cfg, t) for t in range(ticks)}
+    return w, sk, sv, frames
+
+
+@pytest.mark.parametrize("frame_dim,mod_mode,hkv", [(5, "full", 1), (0, "full", 1), (5, "scale_only", 2)])
+def test_velocity_matches_scalar_brute_force(frame_dim, mod_mode, hkv):
+    cfg = WL.micro_config(frame_dim=frame_dim, mod_mode=mod_mode, n_kv_heads=hkv,
+                          embed_scale=1.5 if hkv == 2 else 1.0)
+    w, sk, sv, frames = _inputs(cfg, 3)
+    fw = 3  # ring has wrapped once
+    state = WL.make_state(cfg, 0)[0]
+    x = WL.make_noise(cfg, 0)[0]
+    pos = O.dyn_pos0(cfg, fw) + np.arange(cfg.action_horizon + 1)
+    attend = O.full_batch_attend(cfg, w, sk, sv, frames, fw, 0)
+    v = O.velocity(cfg, w, state, x, 0.6, pos, attend)
+    ctx = [O.context_kv(cfg, w, sk, sv, frames, fw, l, 0) for l in range(cfg.n_layers)]
+    ref = brute_force.velocity_loops(cfg, w, state, x, 0.6, [c[0] for c in ctx], [c[1] for c in ctx],
+                                     list(pos))
+    np.testing.assert_allclose(v, np.array(ref), rtol=0, atol=1e-12)
+
+
+def _torch_velocity(cfg, w, state, x, tau, ctx_k, ctx_v, pos):
+    """Composition of torch library routines (F.linear, F.rms_norm, F.gelu,
+    scaled_dot_product_attention), float64, for one env."""
+    t = lambda a: torch.as_tensor(np.asarray(a, dtype=np.float64))  # noqa: E731
+    D, L, Fm = cfg.width, cfg.n_layers, cfg.mlp_dim
+    Hq, Hkv, dh = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    half = D // 2
+    per = cfg.temb_min_period * (cfg.temb_max_period / cfg.temb_min_period) ** torch.linspace(
+        0, 1, half, dtype=torch.float64)
+    ang = 2 * math.pi * tau / per
+    cond = torch.cat([torch.sin(ang), torch.cos(ang), t(state)])
+    mods = []
+    for s in range(2 * L + 1):
+        m = Fn.linear(Fn.silu(Fn.linear(cond, t(w["w_mod1"][s]))), t(w["w_mod2"][s]))
+        mods.append((m[:D], m[D:2 * D], m[2 * D:]))
+    h = torch.cat([Fn.linear(t(state), t(w["w_state"]))[None], Fn.linear(t(x), t(w["w_ain"]))]) * cfg.embed_scale
+    T = h.shape[0]
+    inv = cfg.rope_theta ** (-torch.arange(0, dh, 2, dtype=torch.float64) / dh)
+    a = t(pos)[:, None] * inv[None]
+    cos, sin = torch.cat([torch.cos(a)] * 2, -1), torch.cat([torch.sin(a)] * 2, -1)
+
+    def rot(z):  # z [T, heads, dh]
+        z1, z2 = z[..., : dh // 2], z[..., dh // 2:]
+        return z * cos[:, None] + torch.cat([-z2, z1], -1) * sin[:, None]
+
+    n_ctx = ctx_k[0].shape[0]
+    mask = torch.from_numpy(O.dyn_allowed(n_ctx, T))
+    for l in range(L):
+        sc, sh, g = mods[2 * l]
+        y = Fn.rms_norm(h, (D,), eps=cfg.rms_eps) * (1 + sc) + sh
+        qkv = Fn.linear(y, t(w["w_qkv"][l]))
+        q = rot(qkv[:, :Hq * dh].reshape(T, Hq, dh))
+        k = rot(qkv[:, Hq * dh:(Hq + Hkv) * dh].reshape(T, Hkv, dh))
+        v = qkv[:, (Hq + Hkv) * dh:].reshape(T, Hkv, dh)
+        K = torch.cat([t(ctx_k[l]), k]).repeat_interleave(Hq // Hkv, dim=1)
+        V = torch.cat([t(ctx_v[l]), v]).repeat_interleave(Hq // Hkv, dim=1)
+        o = Fn.scaled_dot_product_attention(q.transpose(0, 1), K.transpose(0, 1), V.transpose(0, 1),
+                                            attn_mask=mask).transpose(0, 1).reshape(T, Hq * dh)
+        h = h + g * Fn.linear(o, t(w["w_o"][l]))
+        sc2, sh2, g2 = mods[2 * l + 1]
+        y2 = Fn.rms_norm(h, (D,), eps=cfg.rms_eps) * (1 + sc2) + sh2
+        u = Fn.linear(y2, t(w["w_gu"][l]))
+        z = Fn.gelu(u[:, :Fm], approximate="tanh") * u[:, Fm:]
+        h = h + g2 * Fn.linear(z, t(w["w_down"][l]))
+    scf, shf, _ = mods[2 * L]
+    yf = Fn.rms_norm(h[1:], (D,), eps=cfg.rms_eps) * (1 + scf) + shf
+    return Fn.linear(yf, t(w["w_aout"])).numpy()
+
+
+def test_velocity_matches_torch_composition_tiny():
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _inputs(cfg, 4)
+    fw = 4
+    state = WL.make_state(cfg, 3)[0]
+    x = WL.make_noise(cfg, 3)[0]
+    pos = O.dyn_pos0(cfg, fw) + np.arange(cfg.action_horizon + 1)
+    v = O.velocity(cfg, w, state, x, 0.75, pos, O.full_batch_attend(cfg, w, sk, sv, frames, fw, 0))
+    ctx = [O.context_kv(cfg, w, sk, sv, frames, fw, l, 0) for l in range(cfg.n_layers)]
+    ref = _torch_velocity(cfg, w, state, x, 0.75, [c[0] for c in ctx], [c[1] for c in ctx], pos)
+    np.testing.assert_allclose(v, ref, rtol=0, atol=1e-11)
+
+
+# ---------------------------------------------------------------- paper invariants
+def test_prop_a1_partitioned_equals_full_batch_tiny():
+    """Proposition A.1: the partitioned cache (built once, ring slots in
+    physical order, FIFO overwrite) gives the full-batch result, 1e-10 in fp64,
+    at every tick of a trace that wraps the ring twice."""
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _inputs(cfg, 5)
+    cache = O.PartitionedCache(cfg, w, sk, sv, env=0)
+    taus = cfg.taus()
+    for tick in range(5):
+        cache.write(frames[tick][0])
+        state = WL.make_state(cfg, tick)
+        noise = WL.make_noise(cfg, tick)
+        full = O.denoise_chunk(cfg, w, sk, sv, frames, tick + 1, state, noise, taus)[0]
+        part = O.denoise_chunk_partitioned(cfg, w, cache, state[0], noise[0], taus)
+        np.testing.assert_allclose(part, full, rtol=0, atol=1e-10)
+
+
+def test_prop_a1_with_empty_ring_and_direct_path():
+    cfg = WL.micro_config(frame_dim=0, window_frames=3)
+    w, sk, sv, frames = _inputs(cfg, 6)
+    cache = O.PartitionedCache(cfg, w, sk, sv, env=0)
+    taus = [1.0, 0.6, 0.1, 0.0]
+    for tick in range(-1, 6):
+        if tick >= 0:
+            cache.write(frames[tick][0])
+        state = WL.make_state(cfg, max(tick, 0))
+        noise = WL.make_noise(cfg, max(tick, 0))
+        full = O.denoise_chunk(cfg, w, sk, sv, frames, tick + 1, state, noise, taus)[0]
+        part = O.denoise_chunk_partitioned(cfg, w, cache, state[0], noise[0], taus)
+        np.testing.assert_allclose(part, full, rtol=0, atol=1e-10)
+
+
+def test_timestep_invariance_of_cached_regions():
+    """The perception K/V do not depend on the flow time (Section 3.1): the
+    cached regions read at different Euler steps are bit-identical."""
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _inputs(cfg, 3)
+    seen = {}
+    base = O.full_batch_attend(cfg, w, sk, sv, frames, 3, 0)
+    calls = {"n": 0}
+
+    def spy(layer, q, k, v):
+        Kc, Vc = O.context_kv(cfg, w, sk, sv, frames, 3, layer, 0)
+        key = layer
+        if key in seen:
+            assert np.array_equal(seen[key][0], Kc) and np.array_equal(seen[key][1], Vc)
+        else:
+            seen[key] = (Kc, Vc)
+        calls["n"] += 1
+        return base(layer, q, k, v)
+
+    state = WL.make_state(cfg, 0)[0]
+    noise = WL.make_noise(cfg, 0)[0]
+    pos = O.dyn_pos0(cfg, 3) + np.arange(cfg.action_horizon + 1)
+    O.euler_integrate(lambda x, t: O.velocity(cfg, w, state, x, t, pos, spy), noise, cfg.taus())
+    assert calls["n"] == cfg.num_steps * cfg.n_layers
+
+
+def test_naive_cache_negative_control():
+    """Reusing the dynamic K/V across timesteps (a cache that ignores t, the
+    "Naive Cache" of Section 4.6) must move x_K by more than the fp32 parity
+    tolerance (1e-4) with the stock synthetic weights, and by far more than the
+    bf16 tolerance once the attention branch is made stronger (q/k/v and
+    output projections x5)."""
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _inputs(cfg, 2)
+    state, noise = WL.make_state(cfg, 1)[0], WL.make_noise(cfg, 1)[0]
+    for factor, bound in ((1.0, 2e-4), (5.0, 0.1)):
+        w2 = dict(w)
+        w2["w_qkv"] = w["w_qkv"] * factor
+        w2["w_o"] = w["w_o"] * factor
+        cache = O.PartitionedCache(cfg, w2, sk, sv, env=0)
+        cache.write(frames[0][0])
+        cache.write(frames[1][0])
+        good = O.denoise_chunk_partitioned(cfg, w2, cache, state, noise, cfg.taus())
+        bad = O.denoise_chunk_partitioned(cfg, w2, cache, state, noise, cfg.taus(), naive_cache=True)
+        assert np.max(np.abs(good - bad)) > bound
+
+
+def test_state_row_ignores_action_tokens():
+    """Mask reading: the state token attends to the cache and itself only, so
+    its attention output at every layer is independent of the action noise."""
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _inputs(cfg, 2)
+    state = WL.make_state(cfg, 0)[0]
+    pos = O.dyn_pos0(cfg, 2) + np.arange(cfg.action_horizon + 1)
+    attend = O.full_batch_attend(cfg, w, sk, sv, frames, 2, 0)
+    d1, d2 = {}, {}
+    O.velocity(cfg, w, state, WL.make_noise(cfg, 0)[0], 0.5, pos, attend, diag=d1)
+    O.velocity(cfg, w, state, WL.make_noise(cfg, 1)[0], 0.5, pos, attend, diag=d2)
+    for a, b in zip(d1["attn"], d2["attn"]):
+        np.testing.assert_allclose(a[0], b[0], rtol=0, atol=1e-13)
+        assert np.max(np.abs(a[1:] - b[1:])) > 1e-6
+
+
+def test_window_excludes_evicted_frames():
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _inputs(cfg, 4)
+    state, noise = WL.make_state(cfg, 0), WL.make_noise(cfg, 0)
+    taus = [1.0, 0.5, 0.0]
+    a = O.denoise_chunk(cfg, w, sk, sv, frames, 4, state, noise, taus)
+    fr2 = dict(frames)
+    fr2[1] = frames[1] * 0 + 7.0  # frame 1 was evicted by frames 2, 3
+    b = O.denoise_chunk(cfg, w, sk, sv, fr2, 4, state, noise, taus)
+    assert np.array_equal(a, b)
+    fr3 = dict(frames)
+    fr3[2] = frames[2] * 0 + 7.0  # frame 2 is inside the window
+    c = O.denoise_chunk(cfg, w, sk, sv, fr3, 4, state, noise, taus)
+    assert np.max(np.abs(a - c)) > 1e-6
+
+
+def test_single_step_closed_form():
+    """K = 1: x_1 = x_0 - v(x_0, 1)."""
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _inputs(cfg, 1)
+    state, noise = WL.make_state(cfg, 0), WL.make_noise(cfg, 0)
+    x1 = O.denoise_chunk(cfg, w, sk, sv, frames, 1, state, noise, [1.0, 0.0])[0]
+    pos = O.dyn_pos0(cfg, 1) + np.arange(cfg.action_horizon + 1)
+    v = O.velocity(cfg, w, state[0], noise[0], 1.0, pos, O.full_batch_attend(cfg, w, sk, sv, frames, 1, 0))
+    np.testing.assert_allclose(x1, noise[0] - v, rtol=0, atol=1e-14)
+
+
+def test_position_shift_leaves_attention_unchanged():
+    """Absolute-position RoPE: shifting every position (cache and dynamic) by
+    the same amount leaves the attention output unchanged."""
+    rng = np.random.default_rng(9)
+    T, n, dh, hq = 5, 12, 16, 4
+    q0 = rng.standard_normal((T, hq, dh))
+    k0 = rng.standard_normal((n + T, 1, dh))
+    V = rng.standard_normal((n + T, 1, dh))
+    pk = np.concatenate([np.arange(n), 300 + np.arange(T)])
+    pq = 300 + np.arange(T)
+    outs = []
+    for delta in (0, 17, 380000):
+        q = O.rope(q0, pq + delta, 1e4)
+        K = O.rope(k0, pk + delta, 1e4)
+        outs.append(O.masked_attention(q, K, V, O.dyn_allowed(n, T)))
+    np.testing.assert_allclose(outs[1], outs[0], rtol=0, atol=1e-10)
+    np.testing.assert_allclose(outs[2], outs[0], rtol=0, atol=1e-9)
