@@ -1,0 +1,246 @@
+#!/usr/bin/env python3
+"""Benchmark of the Reflex denoise hot path on one MI355X.
+
+A "step" is one control tick of the pi0-scale single-chunk workload: write one
+observation frame into the ring (768 tokens x 18 layers of K/V, RoPE at the
+absolute position) and denoise one 50 x 32 action chunk with 10 Euler steps of
+the 18-layer width-1024 action expert over 48 static + 768 window + 51 dynamic
+tokens, batch 1, bf16 operands with fp32 statistics and accumulation.  Inputs
+are resident in HBM before the timed region.
+
+Prints one JSON line.  Besides the headline (chunks/s at batch 1), it reports
+the denoise-step latency, a batch-32 tick (frames through the per-layer K/V
+projection), per-kernel-class device times from the library's event profile,
+the roofline of the dominant kernel and the float64 CPU oracle timed on this
+host's cores as a reference baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "denoise-step latency (us) + action chunks/s at batch 1/32; attn HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def _device_inputs(cfg, torch, seed=0):
+    """Synthetic weights / cache / inputs drawn on the device (values do not
+    affect timing; parity is covered by the tests with the seeded generator)."""
+    from paper_2607_14695_amd import workloads as WL
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    dt = torch.bfloat16 if cfg.bf16 else torch.float32
+    w = {}
+    for name, shape in WL.weight_shapes(cfg).items():
+        w[name] = (torch.randn(shape, generator=g, device="cuda") * WL.WEIGHT_STD).to(dt)
+    shp = (cfg.batch, cfg.n_layers, cfg.static_len, cfg.head_dim)
+    sk = torch.randn(shp, generator=g, device="cuda").to(dt)
+    sv = torch.randn(shp, generator=g, device="cuda").to(dt)
+    frames = [torch.randn((cfg.batch,) + WL.frame_shape(cfg), generator=g, device="cuda").to(dt) for _ in range(3)]
+    state = torch.randn((cfg.batch, cfg.state_dim), generator=g, device="cuda")
+    noise = torch.randn((cfg.batch, cfg.action_horizon, cfg.action_dim), generator=g, device="cuda")
+    return w, sk, sv, frames, state, noise
+
+
+def _class_bytes_flops(cfg):
+    """Algorithmic HBM bytes and flops of ONE launch of each kernel class.
+
+    GEMMs: weight bytes + activation bytes in + one output copy (fp32 for the
+    split-K residual/QKV outputs, operand type for gate/up).  Attention: the
+    visible cached K and V rows + q/k/v in (fp32) + o out."""
+    T = cfg.action_horizon + 1
+    M = cfg.batch * T
+    D, Fm, Hq, dh = cfg.width, cfg.mlp_dim, cfg.n_q_heads, cfg.head_dim
+    eb = 2 if cfg.bf16 else 4
+    nqkv = (Hq + 2) * dh
+    Lc = cfg.static_len + cfg.window_frames * cfg.frame_tokens
+    out = {
+        "gemm_qkv": (nqkv * D * eb + M * D * eb + M * nqkv * 4, 2.0 * M * nqkv * D),
+        "gemm_o": (D * Hq * dh * eb + M * Hq * dh * eb + M * D * 4, 2.0 * M * D * Hq * dh),
+        "gemm_gate_up": (2 * Fm * D * eb + M * D * eb + M * Fm * eb, 2.0 * M * 2 * Fm * D),
+        "gemm_down": (D * Fm * eb + M * Fm * eb + M * D * 4, 2.0 * M * D * Fm),
+    }
+    vis = Lc * T + (1 + (T - 1) * T)  # visible keys summed over dynamic rows
+    out["attention"] = (cfg.batch * (2 * Lc * dh * eb + M * nqkv * 4 + M * Hq * dh * eb),
+                        cfg.batch * 4.0 * Hq * dh * vis)
+    return out
+
+
+def _time_ticks(eng, frames, state, noise, steps, warmup, torch, denoise_only=False):
+    for i in range(warmup):
+        if not denoise_only:
+            eng.write_frame(frames[i % len(frames)])
+        eng.denoise(state, noise)
+    eng.synchronize()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        if not denoise_only:
+            eng.write_frame(frames[i % len(frames)])
+        eng.denoise(state, noise)
+    eng.synchronize()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def cpu_baseline(cfg, log):
+    """The float64 oracle timed on this host's cores: one full chunk (1 env,
+    10 Euler steps, one frame in the window), median of two runs."""
+    import numpy as np
+
+    from oracle import reflex_oracle as O
+    from paper_2607_14695_amd import workloads as WL
+
+    cores = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
+    except Exception:  # threadpoolctl missing: BLAS uses its default pool
+        limiter = None
+    rng = np.random.default_rng(0)
+    w = {}
+    for name, shape in WL.weight_shapes(cfg).items():
+        w[name] = rng.standard_normal(size=shape) * WL.WEIGHT_STD
+    shp = (1, cfg.n_layers, cfg.static_len, cfg.head_dim)
+    sk, sv = rng.standard_normal(size=shp), rng.standard_normal(size=shp)
+    frames = {0: rng.standard_normal(size=(1,) + WL.frame_shape(cfg))}
+    state = rng.standard_normal(size=(1, cfg.state_dim))
+    noise = rng.standard_normal(size=(1, cfg.action_horizon, cfg.action_dim))
+    times = []
+    for _ in range(2):
+        t0 = time.perf_counter()
+        O.denoise_chunk(cfg, w, sk, sv, frames, 1, state, noise, cfg.taus())
+        times.append(time.perf_counter() - t0)
+        log(f"cpu oracle chunk: {times[-1]:.2f} s")
+    sec = float(np.median(times))
+    if limiter is not None:
+        limiter.unregister()
+    return {"value": 1.0 / sec, "unit": "chunks/s", "cores": cores, "kind": "oracle",
+            "sample": "one full pi0_chunk_bf16 chunk (env 0, 10 Euler steps, 48 static + 768 frame "
+                      f"+ 51 dynamic tokens), float64 numpy, median of 2 runs = {sec:.2f} s/chunk"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-b32", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(environments would shard over GPUs with replicated weights and no collective)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_14695_amd import workloads as WL
+    from paper_2607_14695_amd.reflex import ReflexEngine
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    cfg = WL.CONFIGS["pi0_chunk_bf16"]
+    w, sk, sv, frames, state, noise = _device_inputs(cfg, torch)
+    eng = ReflexEngine(cfg, w, sk, sv)
+    log("engine ready (pi0_chunk_bf16)")
+    tick_s = _time_ticks(eng, frames, state, noise, args.steps, args.warmup, torch)
+    log(f"tick {tick_s * 1e3:.3f} ms")
+    chunk_s = _time_ticks(eng, frames, state, noise, args.steps, args.warmup, torch, denoise_only=True)
+    log(f"chunk {chunk_s * 1e3:.3f} ms")
+    prof = eng.profile(state, noise)
+    log("profile: " + ", ".join(f"{k}={v[0]:.3f}ms/{v[1]}" for k, v in prof.items() if v[1]))
+    bf = _class_bytes_flops(cfg)
+    dominant = max((k for k in bf if prof.get(k, (0, 0))[1] > 0), key=lambda k: prof[k][0])
+    ms, n = prof[dominant]
+    avg_s = ms / n / 1e3
+    achieved = bf[dominant][0] / avg_s / 1e9
+    attn_ms, attn_n = prof["attention"]
+    attn_gbs = bf["attention"][0] / (attn_ms / attn_n / 1e3) / 1e9
+    kernel_avg_us = {k: round(v[0] / v[1] * 1e3, 3) for k, v in prof.items() if v[1]}
+    eng.close()
+    del eng, w
+
+    b32 = None
+    if not args.no_b32:
+        c32 = WL.CONFIGS["pi0_batch32_bf16"]
+        w32, sk32, sv32, fr32, st32, nz32 = _device_inputs(c32, torch, seed=1)
+        e32 = ReflexEngine(c32, w32, sk32, sv32)
+        steps32 = max(3, args.steps // 3)
+        t32 = _time_ticks(e32, fr32, st32, nz32, steps32, 2, torch)
+        c32s = _time_ticks(e32, fr32, st32, nz32, steps32, 1, torch, denoise_only=True)
+        p32 = e32.profile(st32, nz32)
+        bf32 = _class_bytes_flops(c32)
+        a_ms, a_n = p32["attention"]
+        b32 = {
+            "workload": "pi0_batch32_bf16 tick: 32 envs, frame write through per-layer Wk/Wv 2048->256 "
+                        "(embedding path) + 10-step denoise over 48 static + 2x768 ring + 51 dynamic tokens",
+            "chunks_per_s": round(c32.batch / t32, 2),
+            "tick_ms": round(t32 * 1e3, 3),
+            "chunk_ms": round(c32s * 1e3, 3),
+            "denoise_step_us": round(c32s / c32.num_steps * 1e6, 1),
+            "attn_hbm_gbs": round(bf32["attention"][0] / (a_ms / a_n / 1e3) / 1e9, 1),
+            "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in p32.items() if v[1]},
+        }
+        for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
+            ms_k, n_k = p32[k]
+            b32[f"{k}_mfma_tflops"] = round(bf32[k][1] / (ms_k / n_k / 1e3) / 1e12, 1)
+        e32.close()
+        log(f"b32 tick {t32 * 1e3:.3f} ms, chunk {c32s * 1e3:.3f} ms")
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, log)
+
+    result = {
+        "metric": METRIC,
+        "value": round(cfg.batch / tick_s, 3),
+        "unit": "chunks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(tick_s * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "pi0_chunk_bf16 tick: 18-layer width-1024 action expert (MLP 4096, 8 q heads / 1 kv "
+                        "head of 256), one 768-token frame written to a 1-frame ring (direct K/V path) + "
+                        "10-step Euler denoise of a 50x32 action chunk over 48 static + 768 frame + 51 "
+                        "dynamic tokens",
+            "batch": cfg.batch,
+            "euler_steps": cfg.num_steps,
+            "cached_tokens": cfg.static_len + cfg.window_frames * cfg.frame_tokens,
+        },
+        "denoise_step_us": round(chunk_s / cfg.num_steps * 1e6, 2),
+        "chunk_ms": round(chunk_s * 1e3, 4),
+        "attn_hbm_gbs": round(attn_gbs, 1),
+        "kernel_avg_us": kernel_avg_us,
+        "roofline": {
+            "kernel": dominant,
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+        },
+        "b32": b32,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,262 @@
+/*
+ * reflex.h -- C ABI of the MI355X (gfx950) Reflex denoise hot path.
+ *
+ * The library computes the per-denoising-step forward of a flow-matching
+ * action expert over a three-region KV cache, following the paper "Reflex:
+ * Real-Time Vision-Language-Action Control through Streaming Inference":
+ *
+ *   - a pinned static prefix (language tokens), written once (Section 3.1);
+ *   - a sliding FIFO window of the last W observation frames, held in a
+ *     pre-allocated ring and overwritten in O(1) per frame (Section 3.1,
+ *     Section 3.4 "Ring Buffer Architecture", Appendix B.1-B.2);
+ *   - a dynamic suffix (one state token + H action tokens) recomputed at every
+ *     Euler step; attention over [static; window; dynamic] is Eq. 1 and equals
+ *     full-batch attention (Appendix A, Proposition A.1).
+ *
+ * Every layer uses AdaRMSNorm with fp32 statistics (Eq. 2, Section 3.2),
+ * packed QKV and gate|up projections (Section 3.4 "Operator Fusion"), and the
+ * chunk is integrated with explicit Euler from noise at tau = 1 to actions at
+ * tau = 0.
+ *
+ * Memory ownership: the caller allocates and owns every device buffer
+ * (weights, cache, workspace, inputs, outputs).  The library never allocates
+ * or frees device memory; it owns only the host-side context.  All device
+ * work is enqueued on the stream given to reflex_cache_init and is
+ * asynchronous unless stated otherwise.  A context is bound to one stream and
+ * is not thread-safe.
+ *
+ * Status codes: 0 on success, a negative REFLEX_E* value on failure;
+ * reflex_strerror() describes a code (and the last HIP error for
+ * REFLEX_EHIP).  On failure no context state changes.
+ */
+#ifndef REFLEX_H
+#define REFLEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define REFLEX_OK 0
+#define REFLEX_EINVAL (-1)   /* null pointer, bad shape or unsupported size */
+#define REFLEX_EDTYPE (-2)   /* weight dtype differs from the config's dtype */
+#define REFLEX_EHIP (-3)     /* a HIP call or kernel launch failed */
+#define REFLEX_ESTATE (-4)   /* context not initialised or already destroyed */
+
+#define REFLEX_DTYPE_F32 0
+#define REFLEX_DTYPE_BF16 1
+
+#define REFLEX_MOD_FULL 0        /* y = n(x)(1+scale)+shift; h += gate * f(y) */
+#define REFLEX_MOD_SCALE_ONLY 1  /* shift = 0, gate = 1: Eq. 2 exactly */
+
+#define REFLEX_MAX_STEPS 64
+
+/*
+ * Shape of the action expert and of the cache.
+ *
+ * Model: n_layers transformer layers of width `width`; a gated-GELU MLP of
+ * width mlp_dim; n_q_heads query heads sharing n_kv_heads K/V heads of size
+ * head_dim; one state token (state_dim) and action_horizon action tokens
+ * (action_dim each) form the dynamic region (T = 1 + action_horizon rows).
+ * The conditioning MLP of each AdaRMSNorm site maps c = [sinusoidal(tau) (width
+ * values); state] through cond_hidden SiLU units to 3*width outputs
+ * (scale, shift, gate).  Sites: 2*l (attention norm of layer l), 2*l+1 (MLP norm
+ * of layer l), 2*n_layers (final norm before the action head).
+ *
+ * Cache: static_len prefix tokens; window_frames ring slots of frame_tokens
+ * tokens.  frame_dim > 0: frames arrive as [frame_tokens, frame_dim]
+ * embeddings and K/V come from the per-layer frame projection w_kv;
+ * frame_dim == 0: frames arrive as pre-RoPE per-layer K/V.  batch independent
+ * environments advance in lockstep and share the weights.
+ *
+ * Numerics: dtype is the storage/compute type of weights, cache and GEMM
+ * operands (accumulation, statistics, residual stream and actions are fp32).
+ * RoPE: rotate-half, base rope_theta; positions are absolute: static
+ * 0..static_len-1, frame f token j at static_len + f*frame_tokens + j, dynamic
+ * token i at static_len + frames_written*frame_tokens + i.  The token embeddings
+ * are multiplied by embed_scale.
+ *
+ * Supported by this build: n_kv_heads == 1; head_dim in {64, 128, 256};
+ * width, mlp_dim, cond_hidden multiples of 64; state_dim, action_dim, frame_dim
+ * multiples of 8; dynamic rows T <= 64 per env.
+ */
+typedef struct reflex_config {
+  int32_t n_layers;
+  int32_t width;
+  int32_t mlp_dim;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t state_dim;
+  int32_t action_dim;
+  int32_t action_horizon;
+  int32_t cond_hidden;
+  int32_t static_len;
+  int32_t frame_tokens;
+  int32_t window_frames;
+  int32_t frame_dim;
+  int32_t batch;
+  int32_t dtype;       /* REFLEX_DTYPE_* */
+  int32_t mod_mode;    /* REFLEX_MOD_* */
+  int32_t max_steps;   /* largest num_steps a denoise call may use (<= 64) */
+  float rms_eps;
+  float embed_scale;
+  double rope_theta;
+  double temb_min_period;
+  double temb_max_period;
+} reflex_config;
+
+/*
+ * Device pointers to the weights, row-major, rows are output features
+ * (y = x W^T), element type `dtype`.  The library reads them in place; they
+ * must stay valid and unchanged for the life of the context.
+ *
+ *   w_qkv  [n_layers][(Hq + 2) * head_dim][width]  rows: q heads, k, v
+ *   w_o    [n_layers][width][Hq * head_dim]
+ *   w_gu   [n_layers][2 * mlp_dim][width]           rows: gate, then up
+ *   w_down [n_layers][width][mlp_dim]
+ *   w_state[width][state_dim]
+ *   w_ain  [width][action_dim]
+ *   w_aout [action_dim][width]
+ *   w_mod1 [2*n_layers+1][cond_hidden][width + state_dim]
+ *   w_mod2 [2*n_layers+1][3 * width][cond_hidden]  rows: scale, shift, gate
+ *   w_kv   [n_layers][2 * head_dim][frame_dim]     rows: k, then v; NULL when
+ *                                                   frame_dim == 0
+ *
+ * dtype: the element type the caller's framework reports for the output
+ * projection w_o (the dtype probe of Section 3.2 "Robust Dtype Inference").
+ */
+typedef struct reflex_weights {
+  const void* w_qkv;
+  const void* w_o;
+  const void* w_gu;
+  const void* w_down;
+  const void* w_state;
+  const void* w_ain;
+  const void* w_aout;
+  const void* w_mod1;
+  const void* w_mod2;
+  const void* w_kv;
+  int32_t dtype;
+} reflex_weights;
+
+/* Host-side bookkeeping of one FIFO write (Section 3.1; Appendix B.1). */
+typedef struct reflex_ring_step {
+  int64_t frame_index; /* f: index of the frame being written (0-based)      */
+  int32_t slot;        /* ring slot f mod W                                   */
+  int32_t n_valid;     /* frames visible after the write: min(f + 1, W)       */
+  int64_t pos0;        /* absolute position of the frame's first token        */
+  int64_t dyn_pos0;    /* absolute position of dynamic token 0 afterwards     */
+  int32_t evicted;     /* tokens evicted by the write: frame_tokens if f >= W */
+  int32_t reserved;
+} reflex_ring_step;
+
+typedef struct reflex_ctx reflex_ctx;
+
+/*
+ * Bytes the caller must allocate for the cache and the workspace.  Pure host
+ * function (no device calls).  Both buffers need 256-byte alignment.
+ *
+ * Cache layout (element type `dtype`), R = static_len + window_frames*frame_tokens:
+ *   K at offset 0:           [batch][n_layers][R][head_dim]   RoPE applied
+ *   V at offset K bytes:     [batch][n_layers][head_dim][R]   stored transposed
+ * Rows [0, static_len) hold the static prefix; ring slot s holds rows
+ * [static_len + s*frame_tokens, static_len + (s+1)*frame_tokens).
+ * The first 24 bytes of the workspace hold the device tick state as three
+ * int64 values {frames_written, n_valid, dyn_pos0} (read-only for callers);
+ * the rest of the workspace is private scratch of the library.
+ * Returns REFLEX_EINVAL for an unsupported config.
+ */
+int reflex_query_sizes(const reflex_config* cfg, size_t* cache_bytes, size_t* workspace_bytes);
+
+/*
+ * Validate the config, check the weights' dtype against cfg->dtype (dtype
+ * probe, Section 3.2), bind the caller's buffers and write the pinned static
+ * prefix: K rows get RoPE at positions 0..static_len-1, V rows are copied.
+ *
+ * static_k, static_v: device, [batch][n_layers][static_len][head_dim], pre-RoPE,
+ * element type dtype; read during this call's stream work only.
+ * cache_mem / workspace_mem: device buffers of the sizes reflex_query_sizes
+ * returned.  stream: a hipStream_t (NULL = the null stream).
+ * On success *out receives a new context with frames_written = 0.
+ * Errors: REFLEX_EINVAL, REFLEX_EDTYPE, REFLEX_EHIP; *out untouched on error.
+ */
+int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* cache_mem,
+                      void* workspace_mem, const void* static_k, const void* static_v,
+                      void* stream, reflex_ctx** out);
+
+/*
+ * Write one new frame for all envs (FIFO, incremental prefill of the newest
+ * frame only, Section 3.1): slot f mod W is overwritten; K gets RoPE at
+ * positions static_len + f*frame_tokens + j.
+ *
+ * frame: device, element type dtype;
+ *   frame_dim > 0:  [batch][frame_tokens][frame_dim] embeddings;
+ *   frame_dim == 0: [batch][n_layers][2][frame_tokens][head_dim] pre-RoPE K, V.
+ * frame_index_out / evicted_tokens_out (nullable host pointers) receive f and
+ * the evicted token count (the eviction count of add_new_prefix, Appendix B.1).
+ * The host metadata is returned synchronously; the device work is async.
+ * Errors: REFLEX_EINVAL, REFLEX_ESTATE, REFLEX_EHIP; on error f is not advanced.
+ */
+int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_index_out,
+                             int32_t* evicted_tokens_out);
+
+/*
+ * Denoise one action chunk per env over the current cache (static prefix +
+ * the n_valid written frames + the dynamic region), num_steps Euler steps.
+ *
+ * state:  device fp32 [batch][state_dim]
+ * noise:  device fp32 [batch][action_horizon][action_dim], x at tau_0
+ * actions_out: device fp32 [batch][action_horizon][action_dim], x at tau_K;
+ *         may alias noise.
+ * tau_schedule: host fp32 array of num_steps + 1 values, tau_0 = 1 > ... >
+ *         tau_K = 0, or NULL for tau_k = 1 - k/num_steps.
+ * The cache is only read (timestep invariance, Section 3.1).  An empty ring
+ * is allowed.  Launches are captured once into a HIP graph per distinct
+ * (pointers, num_steps, schedule) and replayed.
+ * Errors: REFLEX_EINVAL (null pointer, num_steps outside [1, max_steps]),
+ * REFLEX_ESTATE, REFLEX_EHIP.
+ */
+int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                         const float* tau_schedule, float* actions_out);
+
+/* Release the host context and its captured graphs; never frees caller
+ * memory.  NULL is a no-op.  Returns 0. */
+int reflex_destroy(reflex_ctx* ctx);
+
+/* Text for a status code (for REFLEX_EHIP, the last HIP error string). */
+const char* reflex_strerror(int status);
+
+/*
+ * Bookkeeping of writing frame number frames_written into a ring of
+ * window_frames slots (pure host function, Section 3.1 FIFO; Appendix B.2).
+ * Errors: REFLEX_EINVAL for a null out, a negative frames_written or
+ * non-positive sizes.
+ */
+int reflex_ring_plan(int64_t frames_written, int32_t window_frames, int32_t frame_tokens,
+                     int32_t static_len, reflex_ring_step* out);
+
+/* Frames written so far into the context (host mirror).  Returns a negative
+ * status for a NULL context. */
+int64_t reflex_frames_written(const reflex_ctx* ctx);
+
+/*
+ * Per-kernel-class device timing of the next denoise call (diagnostics).
+ * When enabled, the next reflex_denoise_chunk runs its launches eagerly (no
+ * graph) with hipEvents around each launch; reflex_profile_read then returns
+ * the summed milliseconds and launch counts per class (the class names are
+ * "embed_norm", "gemm_qkv", "attention", "attn_merge", "gemm_o", "resid_norm",
+ * "gemm_gate_up", "gemm_down", "final_euler", "modulation", "rope_table").
+ * n_classes in/out: capacity of the arrays in, number written out.
+ */
+int reflex_profile_enable(reflex_ctx* ctx, int enable);
+int reflex_profile_read(reflex_ctx* ctx, const char** names, double* ms, int32_t* launches,
+                        int32_t* n_classes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REFLEX_H */

@@ -1,0 +1,147 @@
+// Internal launch interface between the C-ABI layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace reflex {
+
+// Start/stop events attached to the next launch (profiling only).  With both
+// null the launch is a plain dispatch; otherwise the runtime stamps the
+// events from the kernel's own dispatch packet, so the elapsed time is the
+// kernel's execution time without host-side launch overhead.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+extern thread_local LaunchEvents g_launch_events;
+
+#define RFX_LAUNCH(kernel, grid, block, shm, stream, ...)                                            \
+  hipExtLaunchKernelGGL(kernel, grid, block, shm, stream, ::reflex::g_launch_events.start,          \
+                        ::reflex::g_launch_events.stop, 0, __VA_ARGS__)
+
+enum Epi : int {
+  EPI_F32 = 0,   // out_f32[z][split][row][col] = acc (split-K partial sums)
+  EPI_SILU = 1,  // out_t[z][row][col] = silu(acc)
+  EPI_GELU = 2,  // dual B: out_t[row][col] = gelu_tanh(acc_gate) * acc_up
+  EPI_MOD = 3,   // like EPI_F32 (one split); with mod_width > 0 the shift/gate
+                 // columns are replaced by 0/1 (scale-only modulation)
+};
+
+// C[M][N] = A[M][K] * B[N][K]^T (+ epilogue).  For EPI_GELU the B rows
+// [0, N) are the gate projection and [N, 2N) the up projection.
+struct GemmArgs {
+  const void* A;
+  const void* B;
+  void* out;
+  int64_t lda, ldb, ldo;              // row strides in elements
+  int64_t a_bstride, b_bstride;       // per blockIdx.z strides (elements)
+  int64_t o_bstride, o_split_stride;  // output strides (elements)
+  int M, N, K;
+  int splits;        // K split across blockIdx.y (EPI_F32 only)
+  int k_per_split;   // multiple of the k-step
+  int mod_width;     // EPI_MOD: width D, 0 = full modulation
+  int batch;         // blockIdx.z extent
+};
+
+template <typename T> hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
+// Heuristic: number of K splits for an EPI_F32 GEMM.
+int gemm_pick_splits(int M, int N, int K, int elem_bytes);
+
+// Partitioned-region attention (Eq. 1) for the dynamic rows of every env.
+struct AttnArgs {
+  const float* qkv;       // [qkv_splits][B*T][(Hq+2)*dh] fp32 partial sums, pre-RoPE
+  int64_t qkv_split_stride;
+  int qkv_splits;
+  const float2* rope;     // [T][dh/2] (cos, sin) at the dynamic positions
+  const void* cache_k;    // layer base: [B] stride ck_bstride, rows [R][dh]
+  const void* cache_vt;   // layer base: [B] stride ck_bstride, [dh][R]
+  int64_t ck_bstride;     // elements between envs (= L*R*dh)
+  const int32_t* n_valid; // device: frames visible in the ring
+  int static_len, frame_tokens, R;
+  int B, T, Hq;
+  int nsplit;             // key splits (blockIdx.x)
+  float* part_o;          // [B][nsplit][rows_pad][dh]
+  float* part_ml;         // [B][nsplit][rows_pad][2]
+  int rows_pad;
+  void* out;              // [B*T][Hq*dh] (written directly when nsplit == 1)
+};
+template <typename T> hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
+template <typename T> hipError_t launch_attn_merge(const AttnArgs& a, int head_dim, hipStream_t s);
+int attention_pick_splits(int B, int rows, int max_keys, int head_dim);
+
+// Token embedding + first AdaRMSNorm: h = embed_scale*[s W_s^T ; x W_ain^T], y = ada(h).
+struct EmbedArgs {
+  const float* x;        // [B][H][da]
+  const float* state;    // [B][ds]
+  const void* w_state;   // [D][ds]
+  const void* w_ain;     // [D][da]
+  const float* mod;      // site block for this step: [B][3D]
+  float* h;              // [B*T][D]
+  void* y;               // [B*T][D]
+  int B, T, D, ds, da;
+  float embed_scale, eps;
+};
+template <typename T> hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s);
+
+// h += gate (.) sum_s parts[s]; y = ada(h) with the next site's scale/shift.
+struct ResidArgs {
+  float* h;               // [M][D]
+  const float* parts;     // [nparts][M][D]
+  int64_t part_stride;
+  int nparts;
+  const float* gate_mod;  // [B][3D] block of the residual's site (gate at +2D)
+  const float* norm_mod;  // [B][3D] block of the next norm site
+  void* y;                // [M][D]
+  int M, T, D;
+  float eps;
+};
+template <typename T> hipError_t launch_resid_norm(const ResidArgs& a, hipStream_t s);
+
+// Last residual + final AdaRMSNorm + action head + Euler update.
+struct FinalArgs {
+  const float* h;         // [B*T][D]
+  const float* parts;
+  int64_t part_stride;
+  int nparts;
+  const float* gate_mod;  // [B][3D]
+  const float* final_mod; // [B][3D]
+  const void* w_aout;     // [da][D]
+  const float* x_in;      // [B][H][da]
+  float* x_out;           // [B][H][da]
+  int B, T, D, da;
+  float dt, eps;
+};
+template <typename T> hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s);
+
+// RoPE (cos, sin) table for positions pos0 + i, i < n; pos0 from *pos0_dev
+// when non-null.  Angles formed in double.
+hipError_t launch_rope_table(float2* out, const int64_t* pos0_dev, int64_t pos0, int n, int head_dim,
+                             double theta, hipStream_t s);
+
+// Conditioning rows c[k*B + b] = [sinusoidal(tau_k) ; state_b].
+struct TauTable { float tau[65]; };
+template <typename T> hipError_t launch_cond(void* cond, const float* state, const TauTable& taus, int K,
+                                             int B, int D, int ds, double min_p, double max_p,
+                                             hipStream_t s);
+
+// Ring/static write: K rows get RoPE from the table, V is stored transposed.
+struct RingWriteArgs {
+  const void* src_k;     // element (b, l, j, d) at b*sb + l*sl + j*sj + d
+  const void* src_v;
+  int64_t sb, sl, sj;
+  const float2* rope;    // [n_tok][dh/2]
+  void* cache_k;         // cache base, [B][L][R][dh]
+  void* cache_vt;        // cache base, [B][L][dh][R]
+  int row0;              // first cache row written
+  int n_tok, L, B, R;
+  // tick state update (written by block 0 when tick != nullptr)
+  int64_t* tick;
+  int64_t frames_written, dyn_pos0;
+  int32_t n_valid;
+};
+template <typename T, typename S> hipError_t launch_ring_write(const RingWriteArgs& a, int head_dim,
+                                                               hipStream_t s);
+
+}  // namespace reflex

@@ -1,0 +1,264 @@
+// Row kernels of the denoise step and the cache writers:
+//  * token embedding fused with the first AdaRMSNorm,
+//  * residual update fused with the next AdaRMSNorm (it also sums the split-K
+//    partials of the producing projection, so those GEMMs need no reduction),
+//  * the last residual + final AdaRMSNorm + action head + Euler update,
+//  * RoPE (cos, sin) tables with angles formed in double,
+//  * conditioning rows [sinusoidal(tau_k); state] for the modulation MLPs,
+//  * the ring / static-prefix writer (RoPE on K, V stored transposed).
+//
+// AdaRMSNorm (Eq. 2, Section 3.2): y = x * rsqrt(mean(x^2) + eps) * (1 + scale)
+// + shift with the mean of squares accumulated in fp32 (the paper's mixed-
+// precision guardrail); h stays fp32, y is rounded once to the GEMM operand
+// type.  One workgroup per row: one read of h, one write of h and y.
+#include "common.h"
+#include "kernels.h"
+
+namespace reflex {
+
+// ---------------------------------------------------------------------------
+// embedding + first norm: row m = b*T + t; t = 0 is the state token
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void embed_norm_kernel(EmbedArgs p) {
+  __shared__ float red[4];
+  __shared__ float in[64];
+  __shared__ float hs[16 * 256];
+  const int m = blockIdx.x, b = m / p.T, t = m % p.T;
+  const int n_in = (t == 0) ? p.ds : p.da;
+  const float* src = (t == 0) ? p.state + (int64_t)b * p.ds : p.x + ((int64_t)b * (p.T - 1) + (t - 1)) * p.da;
+  const T* W = reinterpret_cast<const T*>(t == 0 ? p.w_state : p.w_ain);
+  if (threadIdx.x < n_in) in[threadIdx.x] = src[threadIdx.x];
+  __syncthreads();
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < p.D; c += 256) {
+    const T* w = W + (int64_t)c * n_in;
+    float acc = 0.f;
+    for (int e = 0; e < n_in; ++e) acc += to_f(w[e]) * in[e];
+    acc *= p.embed_scale;
+    hs[c] = acc;
+    ss += acc * acc;
+  }
+  const float tot = block_sum_256(ss, red);
+  const float r = rsqrtf(tot / (float)p.D + p.eps);
+  const float* mod = p.mod + (int64_t)b * 3 * p.D;
+  for (int c = threadIdx.x; c < p.D; c += 256) {
+    p.h[(int64_t)m * p.D + c] = hs[c];
+    const float y = hs[c] * r * (1.f + mod[c]) + mod[p.D + c];
+    reinterpret_cast<T*>(p.y)[(int64_t)m * p.D + c] = from_f<T>(y);
+  }
+}
+
+template <typename T>
+hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s) {
+  if (a.D > 16 * 256 || a.ds > 64 || a.da > 64) return hipErrorInvalidValue;
+  RFX_LAUNCH((embed_norm_kernel<T>), dim3(a.B * a.T), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// residual + norm
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void resid_norm_kernel(ResidArgs p) {
+  __shared__ float red[4];
+  __shared__ float hs[16 * 256];
+  const int m = blockIdx.x, b = m / p.T;
+  const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
+  const float* nmod = p.norm_mod + (int64_t)b * 3 * p.D;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < p.D; c += 256) {
+    float acc = 0.f;
+    for (int s = 0; s < p.nparts; ++s) acc += p.parts[s * p.part_stride + (int64_t)m * p.D + c];
+    const float v = p.h[(int64_t)m * p.D + c] + gmod[c] * acc;
+    hs[c] = v;
+    ss += v * v;
+  }
+  const float tot = block_sum_256(ss, red);
+  const float r = rsqrtf(tot / (float)p.D + p.eps);
+  for (int c = threadIdx.x; c < p.D; c += 256) {
+    p.h[(int64_t)m * p.D + c] = hs[c];
+    const float y = hs[c] * r * (1.f + nmod[c]) + nmod[p.D + c];
+    reinterpret_cast<T*>(p.y)[(int64_t)m * p.D + c] = from_f<T>(y);
+  }
+}
+
+template <typename T>
+hipError_t launch_resid_norm(const ResidArgs& a, hipStream_t s) {
+  if (a.D > 16 * 256) return hipErrorInvalidValue;
+  RFX_LAUNCH((resid_norm_kernel<T>), dim3(a.M), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// last residual + final norm + action head + Euler: one block per action row
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
+  __shared__ float red[4];
+  __shared__ float ys[16 * 256];
+  const int H = p.T - 1;
+  const int b = blockIdx.x / H, i = blockIdx.x % H;
+  const int64_t m = (int64_t)b * p.T + 1 + i;
+  const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
+  const float* fmod = p.final_mod + (int64_t)b * 3 * p.D;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < p.D; c += 256) {
+    float acc = 0.f;
+    for (int s = 0; s < p.nparts; ++s) acc += p.parts[s * p.part_stride + m * p.D + c];
+    const float v = p.h[m * p.D + c] + gmod[c] * acc;
+    ys[c] = v;
+    ss += v * v;
+  }
+  const float tot = block_sum_256(ss, red);
+  const float r = rsqrtf(tot / (float)p.D + p.eps);
+  for (int c = threadIdx.x; c < p.D; c += 256) ys[c] = ys[c] * r * (1.f + fmod[c]) + fmod[p.D + c];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const T* W = reinterpret_cast<const T*>(p.w_aout);
+  const int64_t xo = ((int64_t)b * H + i) * p.da;
+  for (int a = wave; a < p.da; a += 4) {
+    float acc = 0.f;
+    for (int c = lane; c < p.D; c += 64) acc += ys[c] * to_f(W[(int64_t)a * p.D + c]);
+    acc = warp_sum(acc);
+    if (lane == 0) p.x_out[xo + a] = p.x_in[xo + a] + p.dt * acc;
+  }
+}
+
+template <typename T>
+hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s) {
+  if (a.D > 16 * 256) return hipErrorInvalidValue;
+  RFX_LAUNCH((final_euler_kernel<T>), dim3(a.B * (a.T - 1)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// RoPE table: out[i][f] = (cos, sin)((pos0 + i) * theta^(-2f/d)), double angles
+// ---------------------------------------------------------------------------
+__global__ void rope_table_kernel(float2* out, const int64_t* pos0_dev, int64_t pos0, int n, int half,
+                                  double theta) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n * half) return;
+  const int i = idx / half, f = idx % half;
+  const int64_t base = pos0_dev ? *pos0_dev : pos0;
+  const double inv = pow(theta, -2.0 * (double)f / (double)(2 * half));
+  const double ang = (double)(base + i) * inv;
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  out[idx] = make_float2((float)cs, (float)sn);
+}
+
+hipError_t launch_rope_table(float2* out, const int64_t* pos0_dev, int64_t pos0, int n, int head_dim,
+                             double theta, hipStream_t s) {
+  const int half = head_dim / 2;
+  const int tot = n * half;
+  if (tot <= 0) return hipSuccess;
+  RFX_LAUNCH(rope_table_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, out, pos0_dev, pos0, n, half,
+                     theta);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// conditioning rows
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void cond_kernel(T* cond, const float* state, TauTable taus, int B, int D, int ds, double min_p,
+                            double max_p) {
+  const int row = blockIdx.x;  // k*B + b
+  const int k = row / B, b = row % B;
+  const int half = D / 2;
+  const int C = D + ds;
+  const double tau = (double)taus.tau[k];
+  for (int c = threadIdx.x; c < C; c += blockDim.x) {
+    float v;
+    if (c < D) {
+      const int i = c < half ? c : c - half;
+      const double frac = half > 1 ? (double)i / (double)(half - 1) : 0.0;
+      const double period = min_p * pow(max_p / min_p, frac);
+      const double ang = 6.283185307179586 * tau / period;
+      v = (float)(c < half ? sin(ang) : cos(ang));
+    } else {
+      v = state[(int64_t)b * ds + (c - D)];
+    }
+    cond[(int64_t)row * C + c] = from_f<T>(v);
+  }
+}
+
+template <typename T>
+hipError_t launch_cond(void* cond, const float* state, const TauTable& taus, int K, int B, int D, int ds,
+                       double min_p, double max_p, hipStream_t s) {
+  RFX_LAUNCH((cond_kernel<T>), dim3(K * B), dim3(256), 0, s, reinterpret_cast<T*>(cond), state, taus,
+                     B, D, ds, min_p, max_p);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// ring / static writer.  Block = (64-token tile, layer, env).
+// K: cache_k[b][l][row0 + j][d] = rope(k_j)[d]
+// V: cache_vt[b][l][d][row0 + j] = v_j[d]   (transposed through LDS)
+// ---------------------------------------------------------------------------
+template <typename T, typename S, int DH>
+__global__ __launch_bounds__(256) void ring_write_kernel(RingWriteArgs p) {
+  constexpr int TJ = 32;  // tokens per block
+  __shared__ float vt[TJ][DH + 1];
+  const int j0 = blockIdx.x * TJ, l = blockIdx.y, b = blockIdx.z;
+  if (p.tick && blockIdx.x == 0 && l == 0 && b == 0 && threadIdx.x == 0) {
+    p.tick[0] = p.frames_written;
+    p.tick[1] = (int64_t)p.n_valid;
+    p.tick[2] = p.dyn_pos0;
+  }
+  const S* sk = reinterpret_cast<const S*>(p.src_k) + (int64_t)b * p.sb + (int64_t)l * p.sl;
+  const S* sv = reinterpret_cast<const S*>(p.src_v) + (int64_t)b * p.sb + (int64_t)l * p.sl;
+  T* ck = reinterpret_cast<T*>(p.cache_k) + ((int64_t)b * p.L + l) * (int64_t)p.R * DH;
+  T* cv = reinterpret_cast<T*>(p.cache_vt) + ((int64_t)b * p.L + l) * (int64_t)p.R * DH;
+  const int ntok = min(TJ, p.n_tok - j0);
+  // K with RoPE: pairs (f, f + DH/2)
+  for (int e = threadIdx.x; e < ntok * (DH / 2); e += 256) {
+    const int jj = e / (DH / 2), f = e % (DH / 2);
+    const int j = j0 + jj;
+    const S* src = sk + (int64_t)j * p.sj;
+    const float lo = to_f(src[f]), hi = to_f(src[f + DH / 2]);
+    const float2 cs = p.rope[(int64_t)j * (DH / 2) + f];
+    T* dst = ck + (int64_t)(p.row0 + j) * DH;
+    dst[f] = from_f<T>(lo * cs.x - hi * cs.y);
+    dst[f + DH / 2] = from_f<T>(hi * cs.x + lo * cs.y);
+  }
+  // V transposed
+  for (int e = threadIdx.x; e < ntok * DH; e += 256) {
+    const int jj = e / DH, d = e % DH;
+    vt[jj][d] = to_f(sv[(int64_t)(j0 + jj) * p.sj + d]);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < ntok * DH; e += 256) {
+    const int d = e / ntok, jj = e % ntok;
+    cv[(int64_t)d * p.R + p.row0 + j0 + jj] = from_f<T>(vt[jj][d]);
+  }
+}
+
+template <typename T, typename S>
+hipError_t launch_ring_write(const RingWriteArgs& a, int head_dim, hipStream_t s) {
+  dim3 grid((a.n_tok + 31) / 32, a.L, a.B);
+  switch (head_dim) {
+    case 64: RFX_LAUNCH((ring_write_kernel<T, S, 64>), grid, dim3(256), 0, s, a); break;
+    case 128: RFX_LAUNCH((ring_write_kernel<T, S, 128>), grid, dim3(256), 0, s, a); break;
+    case 256: RFX_LAUNCH((ring_write_kernel<T, S, 256>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template hipError_t launch_embed_norm<float>(const EmbedArgs&, hipStream_t);
+template hipError_t launch_embed_norm<bf16_t>(const EmbedArgs&, hipStream_t);
+template hipError_t launch_resid_norm<float>(const ResidArgs&, hipStream_t);
+template hipError_t launch_resid_norm<bf16_t>(const ResidArgs&, hipStream_t);
+template hipError_t launch_final_euler<float>(const FinalArgs&, hipStream_t);
+template hipError_t launch_final_euler<bf16_t>(const FinalArgs&, hipStream_t);
+template hipError_t launch_cond<float>(void*, const float*, const TauTable&, int, int, int, int, double, double,
+                                       hipStream_t);
+template hipError_t launch_cond<bf16_t>(void*, const float*, const TauTable&, int, int, int, int, double, double,
+                                        hipStream_t);
+template hipError_t launch_ring_write<float, float>(const RingWriteArgs&, int, hipStream_t);
+template hipError_t launch_ring_write<bf16_t, bf16_t>(const RingWriteArgs&, int, hipStream_t);
+template hipError_t launch_ring_write<bf16_t, float>(const RingWriteArgs&, int, hipStream_t);
+
+}  // namespace reflex

@@ -1,0 +1,641 @@
+// C ABI of the Reflex denoise hot path (declared in include/reflex.h).
+//
+// The context holds only host integers and the caller's device pointers; the
+// ring bookkeeping (frame index, slot, positions, eviction count) follows the
+// FIFO window of Section 3.1 and the circular pointer arithmetic of Section 3.4
+// / Appendix B.2, and is mirrored into a small device "tick state" so the
+// captured denoise graph reads the current window length and dynamic positions
+// from memory and never needs re-capture when a frame arrives.
+#include <string.h>
+
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "../../include/reflex.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace reflex;
+
+namespace reflex {
+thread_local LaunchEvents g_launch_events;
+}
+
+namespace {
+
+thread_local char g_hip_err[256] = "";
+
+enum ProfClass {
+  PC_EMBED = 0, PC_QKV, PC_ATTN, PC_MERGE, PC_O, PC_RESID, PC_GU, PC_DOWN, PC_FINAL, PC_MOD, PC_ROPE, PC_N
+};
+const char* const kProfNames[PC_N] = {"embed_norm", "gemm_qkv",     "attention", "attn_merge",
+                                      "gemm_o",     "resid_norm",   "gemm_gate_up", "gemm_down",
+                                      "final_euler", "modulation",  "rope_table"};
+
+struct SplitK {
+  int splits = 1;
+  int kps = 0;
+};
+
+struct GraphEntry {
+  const float* state;
+  const float* noise;
+  float* out;
+  int steps;
+  float taus[REFLEX_MAX_STEPS + 1];
+  hipGraphExec_t exec;
+};
+
+struct Workspace {
+  int64_t* tick;
+  float2* rope_dyn;
+  float2* rope_frame;
+  void* cond;
+  void* hid;
+  float* mod;
+  float* h;
+  void* y;
+  float* qkv;
+  void* o;
+  float* part_o;
+  float* part_ml;
+  void* z;
+  float* rparts;
+  float* frame_scratch;
+};
+
+struct Plan {
+  int T, M, S, Nqkv, C, R, rows_pad, eb;
+  SplitK qkv, o, down, kv;
+  int attn_splits;
+  int max_parts;
+  size_t cache_bytes, ws_bytes;
+  size_t off[15];
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+SplitK make_split(int M, int K, int splits, int eb) {
+  // skinny kernels step K in 64-byte k-steps, tiled kernels in 128-byte stages
+  const int gran = (M <= 64 ? 64 : 128) / eb;
+  SplitK s;
+  if (splits < 1) splits = 1;
+  int kps = (K + splits - 1) / splits;
+  kps = (kps + gran - 1) / gran * gran;
+  s.kps = kps;
+  s.splits = (K + kps - 1) / kps;
+  return s;
+}
+
+int validate(const reflex_config* c) {
+  if (!c) return REFLEX_EINVAL;
+  if (c->dtype != REFLEX_DTYPE_F32 && c->dtype != REFLEX_DTYPE_BF16) return REFLEX_EINVAL;
+  if (c->mod_mode != REFLEX_MOD_FULL && c->mod_mode != REFLEX_MOD_SCALE_ONLY) return REFLEX_EINVAL;
+  if (c->n_layers < 1 || c->n_layers > 1024) return REFLEX_EINVAL;
+  if (c->width < 64 || c->width > 4096 || c->width % 64) return REFLEX_EINVAL;
+  if (c->mlp_dim < 64 || c->mlp_dim % 64) return REFLEX_EINVAL;
+  if (c->cond_hidden < 64 || c->cond_hidden % 64) return REFLEX_EINVAL;
+  if (c->n_q_heads < 1 || c->n_q_heads > 64) return REFLEX_EINVAL;
+  if (c->n_kv_heads != 1) return REFLEX_EINVAL;
+  if (c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256) return REFLEX_EINVAL;
+  if (c->dtype == REFLEX_DTYPE_F32 && c->head_dim > 128) return REFLEX_EINVAL;
+  if (c->state_dim < 8 || c->state_dim > 64 || c->state_dim % 8) return REFLEX_EINVAL;
+  if (c->action_dim < 1 || c->action_dim > 64) return REFLEX_EINVAL;
+  if (c->action_horizon < 1 || c->action_horizon + 1 > 64) return REFLEX_EINVAL;
+  if (c->static_len < 0 || c->static_len % 8) return REFLEX_EINVAL;
+  if (c->frame_tokens < 8 || c->frame_tokens % 8) return REFLEX_EINVAL;
+  if (c->window_frames < 1) return REFLEX_EINVAL;
+  if (c->frame_dim < 0 || c->frame_dim % 8) return REFLEX_EINVAL;
+  if (c->batch < 1 || c->batch > 4096) return REFLEX_EINVAL;
+  if (c->max_steps < 1 || c->max_steps > REFLEX_MAX_STEPS) return REFLEX_EINVAL;
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.0) || !(c->temb_min_period > 0.0) ||
+      !(c->temb_max_period > 0.0))
+    return REFLEX_EINVAL;
+  const int64_t R = (int64_t)c->static_len + (int64_t)c->window_frames * c->frame_tokens;
+  if (R > (1 << 24)) return REFLEX_EINVAL;
+  return REFLEX_OK;
+}
+
+Plan make_plan(const reflex_config* c) {
+  Plan p;
+  const int eb = c->dtype == REFLEX_DTYPE_BF16 ? 2 : 4;
+  p.eb = eb;
+  p.T = 1 + c->action_horizon;
+  p.M = c->batch * p.T;
+  p.S = 2 * c->n_layers + 1;
+  p.Nqkv = (c->n_q_heads + 2) * c->head_dim;
+  p.C = c->width + c->state_dim;
+  p.R = c->static_len + c->window_frames * c->frame_tokens;
+  const int rows = p.T * c->n_q_heads;
+  p.rows_pad = (rows + 63) / 64 * 64;
+  p.qkv = make_split(p.M, c->width, gemm_pick_splits(p.M, p.Nqkv, c->width, eb), eb);
+  p.o = make_split(p.M, c->n_q_heads * c->head_dim,
+                   gemm_pick_splits(p.M, c->width, c->n_q_heads * c->head_dim, eb), eb);
+  p.down = make_split(p.M, c->mlp_dim, gemm_pick_splits(p.M, c->width, c->mlp_dim, eb), eb);
+  p.kv = make_split(c->batch * c->frame_tokens, c->frame_dim > 0 ? c->frame_dim : 8, 1, eb);
+  p.attn_splits = attention_pick_splits(c->batch, rows, p.R, c->head_dim);
+  p.max_parts = p.o.splits > p.down.splits ? p.o.splits : p.down.splits;
+
+  const size_t B = c->batch, L = c->n_layers, dh = c->head_dim, D = c->width, K = c->max_steps;
+  p.cache_bytes = align256(B * L * p.R * dh * eb) * 2;
+  size_t sz[15];
+  sz[0] = 64;                                                             // tick
+  sz[1] = (size_t)p.T * (dh / 2) * sizeof(float2);                        // rope_dyn
+  sz[2] = (size_t)(c->static_len > c->frame_tokens ? c->static_len : c->frame_tokens) * (dh / 2) *
+          sizeof(float2);                                                 // rope_frame
+  sz[3] = K * B * p.C * eb;                                               // cond
+  sz[4] = K * B * (size_t)p.S * c->cond_hidden * eb;                      // hid
+  sz[5] = (size_t)p.S * K * B * 3 * D * sizeof(float);                    // mod
+  sz[6] = (size_t)p.M * D * sizeof(float);                                // h
+  sz[7] = (size_t)p.M * D * eb;                                           // y
+  sz[8] = (size_t)p.qkv.splits * p.M * p.Nqkv * sizeof(float);            // qkv
+  sz[9] = (size_t)p.M * c->n_q_heads * dh * eb;                           // o
+  sz[10] = B * p.attn_splits * (size_t)p.rows_pad * dh * sizeof(float);   // part_o
+  sz[11] = B * p.attn_splits * (size_t)p.rows_pad * 2 * sizeof(float);    // part_ml
+  sz[12] = (size_t)p.M * c->mlp_dim * eb;                                 // z
+  sz[13] = (size_t)p.max_parts * p.M * D * sizeof(float);                 // rparts
+  sz[14] = c->frame_dim > 0 ? B * c->frame_tokens * L * 2 * dh * sizeof(float) : 0;  // frame scratch
+  size_t off = 0;
+  for (int i = 0; i < 15; ++i) {
+    p.off[i] = off;
+    off += align256(sz[i]);
+  }
+  p.ws_bytes = off;
+  return p;
+}
+
+}  // namespace
+
+struct reflex_ctx {
+  reflex_config cfg;
+  reflex_weights w;
+  Plan plan;
+  Workspace ws;
+  void* cache_k;
+  void* cache_vt;
+  hipStream_t stream;
+  int64_t frames_written;
+  int alive;
+  std::vector<GraphEntry> graphs;
+  // profiling
+  int prof_enabled;
+  double prof_ms[PC_N];
+  int32_t prof_launches[PC_N];
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> ev_pending;
+};
+
+namespace {
+
+int hip_fail(hipError_t e) {
+  snprintf(g_hip_err, sizeof(g_hip_err), "HIP error %d: %s", (int)e, hipGetErrorString(e));
+  return REFLEX_EHIP;
+}
+
+struct Launcher {
+  reflex_ctx* ctx;
+  bool prof;
+  size_t ev_next = 0;
+  hipEvent_t take() {
+    if (ev_next == ctx->ev_pool.size()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      ctx->ev_pool.push_back(e);
+    }
+    return ctx->ev_pool[ev_next++];
+  }
+  template <typename F>
+  int run(int cls, F&& f) {
+    hipEvent_t a = nullptr, b = nullptr;
+    if (prof) {
+      a = take();
+      b = take();
+      if (!a || !b) return hip_fail(hipErrorOutOfMemory);
+      g_launch_events.start = a;
+      g_launch_events.stop = b;
+    }
+    hipError_t e = f();
+    g_launch_events = LaunchEvents{};
+    if (e != hipSuccess) return hip_fail(e);
+    if (prof) ctx->ev_pending.push_back({cls, {a, b}});
+    return REFLEX_OK;
+  }
+};
+
+#define RFX_TRY(expr)           \
+  do {                          \
+    const int _rc = (expr);     \
+    if (_rc != REFLEX_OK) return _rc; \
+  } while (0)
+
+template <typename T>
+int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
+                  float* out, bool prof) {
+  const reflex_config& c = ctx->cfg;
+  const Plan& P = ctx->plan;
+  const Workspace& W = ctx->ws;
+  hipStream_t st = ctx->stream;
+  Launcher L{ctx, prof};
+  const int B = c.batch, Tn = P.T, M = P.M, D = c.width, dh = c.head_dim, Hq = c.n_q_heads;
+  const int Kmax = c.max_steps;
+  const int64_t site_stride = (int64_t)Kmax * B * 3 * D;
+  auto mod_at = [&](int site, int k) { return W.mod + site * site_stride + (int64_t)k * B * 3 * D; };
+
+  RFX_TRY(L.run(PC_ROPE, [&] { return launch_rope_table(W.rope_dyn, W.tick + 2, 0, Tn, dh, c.rope_theta, st); }));
+
+  // conditioning MLPs for every step and site (hoisted: c depends on tau_k and s only)
+  TauTable tt;
+  memset(&tt, 0, sizeof(tt));
+  for (int k = 0; k <= steps; ++k) tt.tau[k] = taus[k];
+  RFX_TRY(L.run(PC_MOD, [&] {
+    return launch_cond<T>(W.cond, state, tt, steps, B, D, c.state_dim, c.temb_min_period, c.temb_max_period, st);
+  }));
+  {
+    GemmArgs g{};
+    g.A = W.cond; g.lda = P.C;
+    g.B = ctx->w.w_mod1; g.ldb = P.C;
+    g.out = W.hid; g.ldo = (int64_t)P.S * c.cond_hidden;
+    g.M = steps * B; g.N = P.S * c.cond_hidden; g.K = P.C;
+    g.splits = 1; g.k_per_split = P.C + 64; g.batch = 1;
+    RFX_TRY(L.run(PC_MOD, [&] { return launch_gemm<T>(g, EPI_SILU, st); }));
+    GemmArgs h{};
+    h.A = W.hid; h.lda = (int64_t)P.S * c.cond_hidden; h.a_bstride = c.cond_hidden;
+    h.B = ctx->w.w_mod2; h.ldb = c.cond_hidden; h.b_bstride = (int64_t)3 * D * c.cond_hidden;
+    h.out = W.mod; h.ldo = 3 * D; h.o_bstride = site_stride;
+    h.M = steps * B; h.N = 3 * D; h.K = c.cond_hidden;
+    h.splits = 1; h.k_per_split = c.cond_hidden + 64; h.batch = P.S;
+    h.mod_width = c.mod_mode == REFLEX_MOD_SCALE_ONLY ? D : 0;
+    RFX_TRY(L.run(PC_MOD, [&] { return launch_gemm<T>(h, EPI_MOD, st); }));
+  }
+
+  const size_t eb = sizeof(T);
+  const char* wqkv = (const char*)ctx->w.w_qkv;
+  const char* wo = (const char*)ctx->w.w_o;
+  const char* wgu = (const char*)ctx->w.w_gu;
+  const char* wdown = (const char*)ctx->w.w_down;
+  const int64_t rpart_stride = (int64_t)M * D;
+
+  for (int k = 0; k < steps; ++k) {
+    const float* x_in = (k == 0) ? noise : out;
+    EmbedArgs ea{x_in, state, ctx->w.w_state, ctx->w.w_ain, mod_at(0, k), W.h, W.y,
+                 B, Tn, D, c.state_dim, c.action_dim, c.embed_scale, c.rms_eps};
+    RFX_TRY(L.run(PC_EMBED, [&] { return launch_embed_norm<T>(ea, st); }));
+    for (int l = 0; l < c.n_layers; ++l) {
+      GemmArgs q{};
+      q.A = W.y; q.lda = D;
+      q.B = wqkv + (size_t)l * P.Nqkv * D * eb; q.ldb = D;
+      q.out = W.qkv; q.ldo = P.Nqkv; q.o_split_stride = (int64_t)M * P.Nqkv;
+      q.M = M; q.N = P.Nqkv; q.K = D; q.splits = P.qkv.splits; q.k_per_split = P.qkv.kps; q.batch = 1;
+      RFX_TRY(L.run(PC_QKV, [&] { return launch_gemm<T>(q, EPI_F32, st); }));
+
+      AttnArgs aa{};
+      aa.qkv = W.qkv; aa.qkv_split_stride = (int64_t)M * P.Nqkv; aa.qkv_splits = P.qkv.splits;
+      aa.rope = W.rope_dyn;
+      aa.cache_k = (const char*)ctx->cache_k + (size_t)l * P.R * dh * eb;
+      aa.cache_vt = (const char*)ctx->cache_vt + (size_t)l * P.R * dh * eb;
+      aa.ck_bstride = (int64_t)c.n_layers * P.R * dh;
+      aa.n_valid = reinterpret_cast<const int32_t*>(W.tick + 1);
+      aa.static_len = c.static_len; aa.frame_tokens = c.frame_tokens; aa.R = P.R;
+      aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits;
+      aa.part_o = W.part_o; aa.part_ml = W.part_ml; aa.rows_pad = P.rows_pad; aa.out = W.o;
+      RFX_TRY(L.run(PC_ATTN, [&] { return launch_attention<T>(aa, dh, st); }));
+      if (P.attn_splits > 1) RFX_TRY(L.run(PC_MERGE, [&] { return launch_attn_merge<T>(aa, dh, st); }));
+
+      GemmArgs og{};
+      og.A = W.o; og.lda = (int64_t)Hq * dh;
+      og.B = wo + (size_t)l * D * Hq * dh * eb; og.ldb = (int64_t)Hq * dh;
+      og.out = W.rparts; og.ldo = D; og.o_split_stride = rpart_stride;
+      og.M = M; og.N = D; og.K = Hq * dh; og.splits = P.o.splits; og.k_per_split = P.o.kps; og.batch = 1;
+      RFX_TRY(L.run(PC_O, [&] { return launch_gemm<T>(og, EPI_F32, st); }));
+
+      ResidArgs r1{W.h, W.rparts, rpart_stride, P.o.splits, mod_at(2 * l, k), mod_at(2 * l + 1, k), W.y,
+                   M, Tn, D, c.rms_eps};
+      RFX_TRY(L.run(PC_RESID, [&] { return launch_resid_norm<T>(r1, st); }));
+
+      GemmArgs gu{};
+      gu.A = W.y; gu.lda = D;
+      gu.B = wgu + (size_t)l * 2 * c.mlp_dim * D * eb; gu.ldb = D;
+      gu.out = W.z; gu.ldo = c.mlp_dim;
+      gu.M = M; gu.N = c.mlp_dim; gu.K = D; gu.splits = 1; gu.k_per_split = D + 128; gu.batch = 1;
+      RFX_TRY(L.run(PC_GU, [&] { return launch_gemm<T>(gu, EPI_GELU, st); }));
+
+      GemmArgs dg{};
+      dg.A = W.z; dg.lda = c.mlp_dim;
+      dg.B = wdown + (size_t)l * D * c.mlp_dim * eb; dg.ldb = c.mlp_dim;
+      dg.out = W.rparts; dg.ldo = D; dg.o_split_stride = rpart_stride;
+      dg.M = M; dg.N = D; dg.K = c.mlp_dim; dg.splits = P.down.splits; dg.k_per_split = P.down.kps; dg.batch = 1;
+      RFX_TRY(L.run(PC_DOWN, [&] { return launch_gemm<T>(dg, EPI_F32, st); }));
+
+      if (l + 1 < c.n_layers) {
+        ResidArgs r2{W.h, W.rparts, rpart_stride, P.down.splits, mod_at(2 * l + 1, k), mod_at(2 * l + 2, k),
+                     W.y, M, Tn, D, c.rms_eps};
+        RFX_TRY(L.run(PC_RESID, [&] { return launch_resid_norm<T>(r2, st); }));
+      }
+    }
+    const float dt = (float)((double)taus[k + 1] - (double)taus[k]);
+    FinalArgs fa{W.h, W.rparts, rpart_stride, P.down.splits, mod_at(2 * c.n_layers - 1, k),
+                 mod_at(2 * c.n_layers, k), ctx->w.w_aout, x_in, out, B, Tn, D, c.action_dim, dt, c.rms_eps};
+    RFX_TRY(L.run(PC_FINAL, [&] { return launch_final_euler<T>(fa, st); }));
+  }
+  return REFLEX_OK;
+}
+
+int enqueue_chunk_dispatch(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
+                           float* out, bool prof) {
+  if (ctx->cfg.dtype == REFLEX_DTYPE_BF16)
+    return enqueue_chunk<bf16_t>(ctx, state, noise, steps, taus, out, prof);
+  return enqueue_chunk<float>(ctx, state, noise, steps, taus, out, prof);
+}
+
+template <typename T>
+int write_static(reflex_ctx* ctx, const void* sk, const void* sv) {
+  const reflex_config& c = ctx->cfg;
+  const Plan& P = ctx->plan;
+  hipError_t e;
+  if (c.static_len > 0) {
+    e = launch_rope_table(ctx->ws.rope_frame, nullptr, 0, c.static_len, c.head_dim, c.rope_theta, ctx->stream);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  RingWriteArgs a{};
+  a.src_k = sk; a.src_v = sv;
+  a.sb = (int64_t)c.n_layers * c.static_len * c.head_dim;
+  a.sl = (int64_t)c.static_len * c.head_dim;
+  a.sj = c.head_dim;
+  a.rope = ctx->ws.rope_frame;
+  a.cache_k = ctx->cache_k; a.cache_vt = ctx->cache_vt;
+  a.row0 = 0; a.n_tok = c.static_len; a.L = c.n_layers; a.B = c.batch; a.R = P.R;
+  a.tick = ctx->ws.tick; a.frames_written = 0; a.n_valid = 0; a.dyn_pos0 = c.static_len;
+  if (c.static_len == 0) {
+    // still publish the tick state; a one-token dummy write is not needed, so
+    // set it with a tiny copy instead
+    int64_t host_tick[3] = {0, 0, (int64_t)c.static_len};
+    e = hipMemcpyAsync(ctx->ws.tick, host_tick, sizeof(host_tick), hipMemcpyHostToDevice, ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    return e == hipSuccess ? REFLEX_OK : hip_fail(e);
+  }
+  e = launch_ring_write<T, T>(a, c.head_dim, ctx->stream);
+  return e == hipSuccess ? REFLEX_OK : hip_fail(e);
+}
+
+template <typename T>
+int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp) {
+  const reflex_config& c = ctx->cfg;
+  const Plan& P = ctx->plan;
+  hipError_t e = launch_rope_table(ctx->ws.rope_frame, nullptr, stp.pos0, c.frame_tokens, c.head_dim,
+                                   c.rope_theta, ctx->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  RingWriteArgs a{};
+  const int dh = c.head_dim;
+  a.rope = ctx->ws.rope_frame;
+  a.cache_k = ctx->cache_k; a.cache_vt = ctx->cache_vt;
+  a.row0 = c.static_len + stp.slot * c.frame_tokens;
+  a.n_tok = c.frame_tokens; a.L = c.n_layers; a.B = c.batch; a.R = P.R;
+  a.tick = ctx->ws.tick; a.frames_written = stp.frame_index + 1; a.n_valid = stp.n_valid;
+  a.dyn_pos0 = stp.dyn_pos0;
+  if (c.frame_dim > 0) {
+    const int N = c.n_layers * 2 * dh;
+    GemmArgs g{};
+    g.A = frame; g.lda = c.frame_dim;
+    g.B = ctx->w.w_kv; g.ldb = c.frame_dim;
+    g.out = ctx->ws.frame_scratch; g.ldo = N;
+    g.M = c.batch * c.frame_tokens; g.N = N; g.K = c.frame_dim;
+    g.splits = 1; g.k_per_split = c.frame_dim + 128; g.batch = 1;
+    e = launch_gemm<T>(g, EPI_F32, ctx->stream);
+    if (e != hipSuccess) return hip_fail(e);
+    a.src_k = ctx->ws.frame_scratch;
+    a.src_v = ctx->ws.frame_scratch + dh;
+    a.sb = (int64_t)c.frame_tokens * N;
+    a.sl = 2 * dh;
+    a.sj = N;
+    e = launch_ring_write<T, float>(a, dh, ctx->stream);
+  } else {
+    a.src_k = frame;
+    a.src_v = (const char*)frame + (size_t)c.frame_tokens * dh * sizeof(T);
+    a.sb = (int64_t)c.n_layers * 2 * c.frame_tokens * dh;
+    a.sl = (int64_t)2 * c.frame_tokens * dh;
+    a.sj = dh;
+    e = launch_ring_write<T, T>(a, dh, ctx->stream);
+  }
+  return e == hipSuccess ? REFLEX_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int reflex_ring_plan(int64_t frames_written, int32_t window_frames, int32_t frame_tokens, int32_t static_len,
+                     reflex_ring_step* out) {
+  if (!out || frames_written < 0 || window_frames < 1 || frame_tokens < 1 || static_len < 0) return REFLEX_EINVAL;
+  const int64_t f = frames_written;
+  out->frame_index = f;
+  out->slot = (int32_t)(f % window_frames);
+  out->n_valid = (int32_t)(f + 1 < window_frames ? f + 1 : window_frames);
+  out->pos0 = (int64_t)static_len + f * frame_tokens;
+  out->dyn_pos0 = (int64_t)static_len + (f + 1) * frame_tokens;
+  out->evicted = f >= window_frames ? frame_tokens : 0;
+  out->reserved = 0;
+  return REFLEX_OK;
+}
+
+int reflex_query_sizes(const reflex_config* cfg, size_t* cache_bytes, size_t* workspace_bytes) {
+  const int rc = validate(cfg);
+  if (rc != REFLEX_OK) return rc;
+  if (!cache_bytes || !workspace_bytes) return REFLEX_EINVAL;
+  const Plan p = make_plan(cfg);
+  *cache_bytes = p.cache_bytes;
+  *workspace_bytes = p.ws_bytes;
+  return REFLEX_OK;
+}
+
+int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* cache_mem, void* workspace_mem,
+                      const void* static_k, const void* static_v, void* stream, reflex_ctx** out) {
+  int rc = validate(cfg);
+  if (rc != REFLEX_OK) return rc;
+  if (!w || !cache_mem || !workspace_mem || !out) return REFLEX_EINVAL;
+  if (cfg->static_len > 0 && (!static_k || !static_v)) return REFLEX_EINVAL;
+  if (!w->w_qkv || !w->w_o || !w->w_gu || !w->w_down || !w->w_state || !w->w_ain || !w->w_aout || !w->w_mod1 ||
+      !w->w_mod2)
+    return REFLEX_EINVAL;
+  if (cfg->frame_dim > 0 && !w->w_kv) return REFLEX_EINVAL;
+  if (((uintptr_t)cache_mem & 255) || ((uintptr_t)workspace_mem & 255)) return REFLEX_EINVAL;
+  if (w->dtype != cfg->dtype) return REFLEX_EDTYPE;
+
+  reflex_ctx* ctx = new (std::nothrow) reflex_ctx();
+  if (!ctx) return REFLEX_EINVAL;
+  ctx->cfg = *cfg;
+  ctx->w = *w;
+  ctx->plan = make_plan(cfg);
+  ctx->stream = reinterpret_cast<hipStream_t>(stream);
+  ctx->frames_written = 0;
+  ctx->alive = 1;
+  ctx->prof_enabled = 0;
+  const Plan& P = ctx->plan;
+  char* base = reinterpret_cast<char*>(workspace_mem);
+  Workspace& W = ctx->ws;
+  W.tick = reinterpret_cast<int64_t*>(base + P.off[0]);
+  W.rope_dyn = reinterpret_cast<float2*>(base + P.off[1]);
+  W.rope_frame = reinterpret_cast<float2*>(base + P.off[2]);
+  W.cond = base + P.off[3];
+  W.hid = base + P.off[4];
+  W.mod = reinterpret_cast<float*>(base + P.off[5]);
+  W.h = reinterpret_cast<float*>(base + P.off[6]);
+  W.y = base + P.off[7];
+  W.qkv = reinterpret_cast<float*>(base + P.off[8]);
+  W.o = base + P.off[9];
+  W.part_o = reinterpret_cast<float*>(base + P.off[10]);
+  W.part_ml = reinterpret_cast<float*>(base + P.off[11]);
+  W.z = base + P.off[12];
+  W.rparts = reinterpret_cast<float*>(base + P.off[13]);
+  W.frame_scratch = reinterpret_cast<float*>(base + P.off[14]);
+  ctx->cache_k = cache_mem;
+  ctx->cache_vt = reinterpret_cast<char*>(cache_mem) + P.cache_bytes / 2;
+
+  // zeroed cache, as the paper's pre-allocated ring buffer (Appendix B.2)
+  hipError_t e = hipMemsetAsync(cache_mem, 0, P.cache_bytes, ctx->stream);
+  if (e == hipSuccess) e = hipMemsetAsync(W.tick, 0, 64, ctx->stream);
+  if (e != hipSuccess) {
+    delete ctx;
+    return hip_fail(e);
+  }
+  rc = cfg->dtype == REFLEX_DTYPE_BF16 ? write_static<bf16_t>(ctx, static_k, static_v)
+                                        : write_static<float>(ctx, static_k, static_v);
+  if (rc != REFLEX_OK) {
+    delete ctx;
+    return rc;
+  }
+  *out = ctx;
+  return REFLEX_OK;
+}
+
+int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_index_out,
+                             int32_t* evicted_tokens_out) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  if (!frame) return REFLEX_EINVAL;
+  const reflex_config& c = ctx->cfg;
+  reflex_ring_step stp;
+  int rc = reflex_ring_plan(ctx->frames_written, c.window_frames, c.frame_tokens, c.static_len, &stp);
+  if (rc != REFLEX_OK) return rc;
+  rc = c.dtype == REFLEX_DTYPE_BF16 ? write_frame<bf16_t>(ctx, frame, stp) : write_frame<float>(ctx, frame, stp);
+  if (rc != REFLEX_OK) return rc;
+  ctx->frames_written += 1;
+  if (frame_index_out) *frame_index_out = stp.frame_index;
+  if (evicted_tokens_out) *evicted_tokens_out = stp.evicted;
+  return REFLEX_OK;
+}
+
+int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                         const float* tau_schedule, float* actions_out) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  if (!state || !noise || !actions_out) return REFLEX_EINVAL;
+  if (num_steps < 1 || num_steps > ctx->cfg.max_steps) return REFLEX_EINVAL;
+  float taus[REFLEX_MAX_STEPS + 1];
+  for (int k = 0; k <= num_steps; ++k)
+    taus[k] = tau_schedule ? tau_schedule[k] : (float)(1.0 - (double)k / (double)num_steps);
+
+  if (ctx->prof_enabled) {
+    ctx->ev_pending.clear();
+    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, true);
+    if (rc != REFLEX_OK) return rc;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(e);
+    for (int i = 0; i < PC_N; ++i) {
+      ctx->prof_ms[i] = 0.0;
+      ctx->prof_launches[i] = 0;
+    }
+    for (auto& pe : ctx->ev_pending) {
+      float ms = 0.f;
+      (void)hipEventElapsedTime(&ms, pe.second.first, pe.second.second);
+      ctx->prof_ms[pe.first] += ms;
+      ctx->prof_launches[pe.first] += 1;
+    }
+    ctx->ev_pending.clear();
+    return REFLEX_OK;
+  }
+
+  GraphEntry* hit = nullptr;
+  for (auto& g : ctx->graphs) {
+    if (g.state == state && g.noise == noise && g.out == actions_out && g.steps == num_steps &&
+        memcmp(g.taus, taus, sizeof(float) * (num_steps + 1)) == 0) {
+      hit = &g;
+      break;
+    }
+  }
+  if (!hit) {
+    hipGraph_t graph;
+    hipError_t e = hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) return hip_fail(e);
+    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, false);
+    e = hipStreamEndCapture(ctx->stream, &graph);
+    if (rc != REFLEX_OK) {
+      if (e == hipSuccess) (void)hipGraphDestroy(graph);
+      return rc;
+    }
+    if (e != hipSuccess) return hip_fail(e);
+    hipGraphExec_t exec;
+    e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (e != hipSuccess) return hip_fail(e);
+    if (ctx->graphs.size() >= 8) {
+      (void)hipGraphExecDestroy(ctx->graphs.front().exec);
+      ctx->graphs.erase(ctx->graphs.begin());
+    }
+    GraphEntry ge;
+    ge.state = state; ge.noise = noise; ge.out = actions_out; ge.steps = num_steps;
+    memset(ge.taus, 0, sizeof(ge.taus));
+    memcpy(ge.taus, taus, sizeof(float) * (num_steps + 1));
+    ge.exec = exec;
+    ctx->graphs.push_back(ge);
+    hit = &ctx->graphs.back();
+  }
+  hipError_t e = hipGraphLaunch(hit->exec, ctx->stream);
+  return e == hipSuccess ? REFLEX_OK : hip_fail(e);
+}
+
+int reflex_destroy(reflex_ctx* ctx) {
+  if (!ctx) return REFLEX_OK;
+  ctx->alive = 0;
+  for (auto& g : ctx->graphs) (void)hipGraphExecDestroy(g.exec);
+  ctx->graphs.clear();
+  for (auto e : ctx->ev_pool) (void)hipEventDestroy(e);
+  ctx->ev_pool.clear();
+  delete ctx;
+  return REFLEX_OK;
+}
+
+const char* reflex_strerror(int status) {
+  switch (status) {
+    case REFLEX_OK: return "ok";
+    case REFLEX_EINVAL: return "invalid argument or unsupported configuration";
+    case REFLEX_EDTYPE: return "weight dtype does not match the configured compute dtype";
+    case REFLEX_EHIP: return g_hip_err[0] ? g_hip_err : "HIP error";
+    case REFLEX_ESTATE: return "context not initialised or destroyed";
+    default: return "unknown status";
+  }
+}
+
+int64_t reflex_frames_written(const reflex_ctx* ctx) {
+  if (!ctx) return REFLEX_ESTATE;
+  return ctx->frames_written;
+}
+
+int reflex_profile_enable(reflex_ctx* ctx, int enable) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  ctx->prof_enabled = enable ? 1 : 0;
+  return REFLEX_OK;
+}
+
+int reflex_profile_read(reflex_ctx* ctx, const char** names, double* ms, int32_t* launches, int32_t* n_classes) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  if (!names || !ms || !launches || !n_classes) return REFLEX_EINVAL;
+  const int n = *n_classes < PC_N ? *n_classes : PC_N;
+  for (int i = 0; i < n; ++i) {
+    names[i] = kProfNames[i];
+    ms[i] = ctx->prof_ms[i];
+    launches[i] = ctx->prof_launches[i];
+  }
+  *n_classes = n;
+  return REFLEX_OK;
+}
+
+}  // extern "C"

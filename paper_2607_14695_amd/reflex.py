@@ -1,0 +1,330 @@
+"""Python binding of libreflex.so (ctypes).
+
+Argument marshalling only: device memory and the stream come from PyTorch,
+every step of the denoise path runs in the library's HIP kernels.  There is no
+fallback: if the shared library is missing or a call fails, an exception is
+raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Dict, Optional, Sequence, Tuple
+
+import numpy as np
+
+from .workloads import ReflexConfig
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libreflex.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "reflex.h")
+
+REFLEX_OK = 0
+REFLEX_EINVAL = -1
+REFLEX_EDTYPE = -2
+REFLEX_EHIP = -3
+REFLEX_ESTATE = -4
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+MOD_FULL = 0
+MOD_SCALE_ONLY = 1
+MAX_STEPS = 64
+
+c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
+
+
+class ConfigC(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", c_i32), ("width", c_i32), ("mlp_dim", c_i32), ("n_q_heads", c_i32),
+        ("n_kv_heads", c_i32), ("head_dim", c_i32), ("state_dim", c_i32), ("action_dim", c_i32),
+        ("action_horizon", c_i32), ("cond_hidden", c_i32), ("static_len", c_i32),
+        ("frame_tokens", c_i32), ("window_frames", c_i32), ("frame_dim", c_i32), ("batch", c_i32),
+        ("dtype", c_i32), ("mod_mode", c_i32), ("max_steps", c_i32), ("rms_eps", c_f32),
+        ("embed_scale", c_f32), ("rope_theta", c_f64), ("temb_min_period", c_f64),
+        ("temb_max_period", c_f64),
+    ]
+
+
+class WeightsC(ctypes.Structure):
+    _fields_ = [
+        ("w_qkv", c_vp), ("w_o", c_vp), ("w_gu", c_vp), ("w_down", c_vp), ("w_state", c_vp),
+        ("w_ain", c_vp), ("w_aout", c_vp), ("w_mod1", c_vp), ("w_mod2", c_vp), ("w_kv", c_vp),
+        ("dtype", c_i32),
+    ]
+
+
+class RingStepC(ctypes.Structure):
+    _fields_ = [
+        ("frame_index", c_i64), ("slot", c_i32), ("n_valid", c_i32), ("pos0", c_i64),
+        ("dyn_pos0", c_i64), ("evicted", c_i32), ("reserved", c_i32),
+    ]
+
+
+class ReflexError(RuntimeError):
+    def __init__(self, status: int, what: str, text: str):
+        super().__init__(f"{what} failed with status {status}: {text}")
+        self.status = status
+
+
+_LIB = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load libreflex.so (built in-tree by build.py); raise if it is absent."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} not found: build it with __graft_entry__.build() "
+                          "(hipcc --offload-arch=gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    sig = {
+        "reflex_query_sizes": (c_i32, [P(ConfigC), P(ctypes.c_size_t), P(ctypes.c_size_t)]),
+        "reflex_cache_init": (c_i32, [P(ConfigC), P(WeightsC), c_vp, c_vp, c_vp, c_vp, c_vp, P(c_vp)]),
+        "reflex_cache_write_frame": (c_i32, [c_vp, c_vp, P(c_i64), P(c_i32)]),
+        "reflex_denoise_chunk": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp]),
+        "reflex_destroy": (c_i32, [c_vp]),
+        "reflex_strerror": (ctypes.c_char_p, [c_i32]),
+        "reflex_ring_plan": (c_i32, [c_i64, c_i32, c_i32, c_i32, P(RingStepC)]),
+        "reflex_frames_written": (c_i64, [c_vp]),
+        "reflex_profile_enable": (c_i32, [c_vp, c_i32]),
+        "reflex_profile_read": (c_i32, [c_vp, P(ctypes.c_char_p), P(c_f64), P(c_i32), P(c_i32)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def header_functions() -> Sequence[str]:
+    """Names of the functions declared in include/reflex.h."""
+    with open(HEADER_PATH) as fh:
+        text = fh.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z0-9_]+\s*\*?\s*(reflex_[a-z_]+)\s*\(", text, re.M)))
+
+
+def strerror(status: int) -> str:
+    return load_library().reflex_strerror(status).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != REFLEX_OK:
+        raise ReflexError(status, what, strerror(status))
+
+
+def config_to_c(cfg: ReflexConfig, max_steps: Optional[int] = None) -> ConfigC:
+    ms = max_steps if max_steps is not None else max(cfg.num_steps, 1)
+    return ConfigC(
+        n_layers=cfg.n_layers, width=cfg.width, mlp_dim=cfg.mlp_dim, n_q_heads=cfg.n_q_heads,
+        n_kv_heads=cfg.n_kv_heads, head_dim=cfg.head_dim, state_dim=cfg.state_dim,
+        action_dim=cfg.action_dim, action_horizon=cfg.action_horizon, cond_hidden=cfg.cond_hidden,
+        static_len=cfg.static_len, frame_tokens=cfg.frame_tokens, window_frames=cfg.window_frames,
+        frame_dim=cfg.frame_dim, batch=cfg.batch, dtype=DTYPE_BF16 if cfg.bf16 else DTYPE_F32,
+        mod_mode=MOD_SCALE_ONLY if cfg.mod_mode == "scale_only" else MOD_FULL, max_steps=ms,
+        rms_eps=cfg.rms_eps, embed_scale=cfg.embed_scale, rope_theta=cfg.rope_theta,
+        temb_min_period=cfg.temb_min_period, temb_max_period=cfg.temb_max_period)
+
+
+def query_sizes(cfg: ReflexConfig, max_steps: Optional[int] = None) -> Tuple[int, int]:
+    lib = load_library()
+    c = config_to_c(cfg, max_steps)
+    cb, wb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(lib.reflex_query_sizes(ctypes.byref(c), ctypes.byref(cb), ctypes.byref(wb)), "reflex_query_sizes")
+    return cb.value, wb.value
+
+
+def query_sizes_status(c: ConfigC) -> int:
+    lib = load_library()
+    cb, wb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    return lib.reflex_query_sizes(ctypes.byref(c), ctypes.byref(cb), ctypes.byref(wb))
+
+
+def ring_plan(frames_written: int, window: int, frame_tokens: int, static_len: int) -> Dict[str, int]:
+    lib = load_library()
+    out = RingStepC()
+    _check(lib.reflex_ring_plan(frames_written, window, frame_tokens, static_len, ctypes.byref(out)),
+           "reflex_ring_plan")
+    return {k: getattr(out, k) for k, _ in RingStepC._fields_ if k != "reserved"}
+
+
+class ReflexEngine:
+    """One library context: caller-owned device buffers + the host context.
+
+    weights: numpy float32 arrays (bf16-representable for bf16 workloads) or
+    torch tensors already on the device with the config's dtype.
+    """
+
+    WEIGHT_ORDER = ("w_qkv", "w_o", "w_gu", "w_down", "w_state", "w_ain", "w_aout", "w_mod1", "w_mod2", "w_kv")
+
+    def __init__(self, cfg: ReflexConfig, weights, static_k, static_v, device: str = "cuda:0",
+                 max_steps: Optional[int] = None, weight_dtype_override=None):
+        import torch
+
+        self.torch = torch
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.lib = load_library()
+        self.dtype = torch.bfloat16 if cfg.bf16 else torch.float32
+        self.max_steps = max_steps if max_steps is not None else max(cfg.num_steps, 1)
+        self.stream = torch.cuda.Stream(device=self.device)
+        self.ctx = c_vp(None)
+        self._bufs = {}
+        with torch.cuda.stream(self.stream):
+            self.w = {}
+            for name in self.WEIGHT_ORDER:
+                if name not in weights:
+                    continue
+                self.w[name] = self._dev(weights[name], weight_dtype_override)
+            sk = self._dev(static_k)
+            sv = self._dev(static_v)
+            self.cache_bytes, self.ws_bytes = query_sizes(cfg, self.max_steps)
+            self.cache = torch.empty(self.cache_bytes, dtype=torch.uint8, device=self.device)
+            self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+            wc = WeightsC(**{n: (self.w[n].data_ptr() if n in self.w else None) for n in self.WEIGHT_ORDER})
+            probe = self.w["w_o"].dtype  # dtype probe of the output projection
+            wc.dtype = DTYPE_BF16 if probe == torch.bfloat16 else (DTYPE_F32 if probe == torch.float32 else 99)
+            cc = config_to_c(cfg, self.max_steps)
+            st = self.lib.reflex_cache_init(ctypes.byref(cc), ctypes.byref(wc), self.cache.data_ptr(),
+                                            self.ws.data_ptr(), sk.data_ptr() if sk.numel() else None,
+                                            sv.data_ptr() if sv.numel() else None,
+                                            self.stream.cuda_stream, ctypes.byref(self.ctx))
+            _check(st, "reflex_cache_init")
+        self.stream.synchronize()
+
+    # -- helpers -------------------------------------------------------------
+    def _dev(self, a, dtype=None):
+        torch = self.torch
+        dt = dtype if dtype is not None else self.dtype
+        if isinstance(a, torch.Tensor):
+            return a.to(device=self.device, dtype=dt).contiguous()
+        return torch.from_numpy(np.ascontiguousarray(a)).to(device=self.device).to(dt).contiguous()
+
+    def _f32(self, a):
+        torch = self.torch
+        if isinstance(a, torch.Tensor):
+            return a.to(device=self.device, dtype=torch.float32).contiguous()
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(self.device)
+
+    # -- API -----------------------------------------------------------------
+    def _enter(self):
+        """Order the engine stream after the caller's current stream."""
+        caller = self.torch.cuda.current_stream(self.device)
+        self.stream.wait_stream(caller)
+        return caller
+
+    def write_frame(self, frame) -> Tuple[int, int]:
+        """Write one frame for all envs; returns (frame_index, evicted_tokens).
+
+        Device work runs on the engine's stream; the caller's current stream
+        is ordered after it, so later work there sees the written cache."""
+        caller = self._enter()
+        with self.torch.cuda.stream(self.stream):
+            f = self._dev(frame)
+            fi, ev = c_i64(0), c_i32(0)
+            _check(self.lib.reflex_cache_write_frame(self.ctx, f.data_ptr(), ctypes.byref(fi), ctypes.byref(ev)),
+                   "reflex_cache_write_frame")
+            self._keep_frame = f  # alive until the stream has consumed it
+        caller.wait_stream(self.stream)
+        return fi.value, ev.value
+
+    def _staged(self, key, a):
+        """Device fp32 view of an input; numpy inputs are copied into a
+        persistent buffer so repeated calls keep the same device pointers (and
+        so replay the same captured graph)."""
+        torch = self.torch
+        if isinstance(a, torch.Tensor) and a.device == self.device and a.dtype == torch.float32 \
+                and a.is_contiguous():
+            return a
+        src = a if isinstance(a, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+        buf = self._bufs.get(key)
+        if buf is None or tuple(buf.shape) != tuple(src.shape):
+            buf = torch.empty(tuple(src.shape), dtype=torch.float32, device=self.device)
+            self._bufs[key] = buf
+        buf.copy_(src.to(torch.float32), non_blocking=False)
+        return buf
+
+    def denoise(self, state, noise, num_steps: Optional[int] = None, taus: Optional[Sequence[float]] = None,
+                out=None):
+        """Denoise one chunk per env; returns the fp32 action tensor (device).
+
+        Without ``out`` the result lands in a buffer owned by the engine that
+        the next call overwrites.  The caller's current stream is ordered
+        after the denoise, so reading the result there is safe."""
+        torch = self.torch
+        k = num_steps if num_steps is not None else self.cfg.num_steps
+        caller = self._enter()
+        with torch.cuda.stream(self.stream):
+            s = self._staged("state", state)
+            n = self._staged("noise", noise)
+            if out is None:
+                out = self._bufs.get("out")
+                if out is None or tuple(out.shape) != tuple(n.shape):
+                    out = torch.empty(tuple(n.shape), dtype=torch.float32, device=self.device)
+                    self._bufs["out"] = out
+            tau_arr = None
+            if taus is not None:
+                tau_np = np.ascontiguousarray(np.asarray(taus, dtype=np.float32))
+                if tau_np.shape[0] != k + 1:
+                    raise ValueError("tau schedule needs num_steps + 1 entries")
+                self._keep_taus = tau_np
+                tau_arr = tau_np.ctypes.data
+            _check(self.lib.reflex_denoise_chunk(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr, out.data_ptr()),
+                   "reflex_denoise_chunk")
+            self._keep_io = (s, n, out)
+        caller.wait_stream(self.stream)
+        return out
+
+    def synchronize(self):
+        self.stream.synchronize()
+
+    def frames_written(self) -> int:
+        return int(self.lib.reflex_frames_written(self.ctx))
+
+    def tick_state(self) -> Tuple[int, int, int]:
+        """Device tick state (frames_written, n_valid, dyn_pos0), first 24 workspace bytes."""
+        self.synchronize()
+        t = self.ws[:24].view(self.torch.int64).cpu().tolist()
+        return int(t[0]), int(t[1]), int(t[2])
+
+    def cache_views(self):
+        """(K [B, L, R, dh], V^T [B, L, dh, R]) views of the cache, config dtype."""
+        c = self.cfg
+        R = c.cache_rows
+        n = c.batch * c.n_layers * R * c.head_dim
+        half = self.cache_bytes // 2
+        esz = 2 if c.bf16 else 4
+        k = self.cache[: n * esz].view(self.dtype).view(c.batch, c.n_layers, R, c.head_dim)
+        v = self.cache[half: half + n * esz].view(self.dtype).view(c.batch, c.n_layers, c.head_dim, R)
+        return k, v
+
+    def profile(self, state, noise, num_steps: Optional[int] = None) -> Dict[str, Tuple[float, int]]:
+        """Run one denoise eagerly with per-launch events; {class: (ms, launches)}."""
+        _check(self.lib.reflex_profile_enable(self.ctx, 1), "reflex_profile_enable")
+        try:
+            self.denoise(state, noise, num_steps)
+            self.synchronize()
+            n = 16
+            names = (ctypes.c_char_p * n)()
+            ms = (c_f64 * n)()
+            cnt = (c_i32 * n)()
+            nc = c_i32(n)
+            _check(self.lib.reflex_profile_read(self.ctx, names, ms, cnt, ctypes.byref(nc)), "reflex_profile_read")
+            return {names[i].decode(): (ms[i], cnt[i]) for i in range(nc.value)}
+        finally:
+            self.lib.reflex_profile_enable(self.ctx, 0)
+
+    def close(self):
+        if self.ctx:
+            self.synchronize()
+            self.lib.reflex_destroy(self.ctx)
+            self.ctx = c_vp(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,195 @@
+"""GPU parity of the HIP path against the float64 oracle on small shapes the
+oracle finishes in seconds: the tiny fp32 workload (max-abs 1e-4 on the action
+chunk) and ragged variants that leave partial key tiles, partial query blocks,
+several envs and an empty ring.  Integer bookkeeping is compared bit-exactly."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import reflex_oracle as O
+from paper_2607_14695_amd import reflex as R
+from paper_2607_14695_amd import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = 1e-4
+
+
+def _setup(cfg, ticks):
+    w = WL.make_weights(cfg)
+    sk, sv = WL.make_static_kv(cfg)
+    frames = {t: WL.make_frame(cfg, t) for t in range(ticks)}
+    return w, sk, sv, frames
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    cfg = WL.CONFIGS["tiny_fp32"]
+    return (cfg,) + _setup(cfg, cfg.ticks)
+
+
+RAGGED = WL.CONFIGS["tiny_fp32"].replace(
+    name="ragged_fp32", batch=3, static_len=40, frame_tokens=24, window_frames=3, action_horizon=5,
+    n_q_heads=3, head_dim=128, width=128, mlp_dim=192, cond_hidden=64, state_dim=8, action_dim=5,
+    frame_dim=72, n_layers=2, num_steps=3)
+
+
+def test_tiny_static_prefix_and_tick_state(tiny):
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    assert eng.tick_state() == (0, 0, cfg.static_len)
+    K, Vt = eng.cache_views()
+    K, Vt = K.cpu().numpy(), Vt.cpu().numpy()
+    for l in range(cfg.n_layers):
+        ks, vs = O.static_kv(cfg, sk, sv, l, 0)
+        np.testing.assert_allclose(K[0, l, :cfg.static_len], ks[:, 0], rtol=1e-5, atol=1e-5)
+        np.testing.assert_allclose(Vt[0, l, :, :cfg.static_len], vs[:, 0].T, rtol=0, atol=0)
+    eng.close()
+
+
+def test_tiny_ring_writes_match_oracle_and_trace(tiny):
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(cfg.ticks):
+        f, ev = eng.write_frame(frames[t])
+        st = O.ring_step(t, cfg.window_frames, cfg.frame_tokens, cfg.static_len)
+        assert (f, ev) == (st.frame_index, st.evicted)
+        assert eng.tick_state() == (t + 1, st.n_valid, st.dyn_pos0)
+        assert eng.frames_written() == t + 1
+        K, Vt = eng.cache_views()
+        K, Vt = K.cpu().numpy(), Vt.cpu().numpy()
+        r0 = cfg.static_len + st.slot * cfg.frame_tokens
+        for l in range(cfg.n_layers):
+            kf, vf = O.frame_kv(cfg, w, frames[t][0], t, l)
+            np.testing.assert_allclose(K[0, l, r0:r0 + cfg.frame_tokens], kf[:, 0], rtol=1e-4, atol=1e-4)
+            np.testing.assert_allclose(Vt[0, l, :, r0:r0 + cfg.frame_tokens], vf[:, 0].T, rtol=1e-4, atol=1e-4)
+    eng.close()
+
+
+def test_tiny_denoise_every_tick(tiny):
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(cfg.ticks):
+        eng.write_frame(frames[t])
+        state, noise = WL.make_state(cfg, t), WL.make_noise(cfg, t)
+        got = eng.denoise(state, noise)
+        eng.synchronize()
+        ref = O.denoise_chunk(cfg, w, sk, sv, frames, t + 1, state, noise, cfg.taus())
+        err = np.max(np.abs(got.cpu().numpy() - ref))
+        assert err <= FP32_TOL, (t, err)
+    eng.close()
+
+
+def test_tiny_empty_ring(tiny):
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    state, noise = WL.make_state(cfg, 0), WL.make_noise(cfg, 0)
+    got = eng.denoise(state, noise)
+    eng.synchronize()
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 0, state, noise, cfg.taus())
+    assert np.max(np.abs(got.cpu().numpy() - ref)) <= FP32_TOL
+    eng.close()
+
+
+def test_tiny_cache_bytes_unchanged_by_denoise(tiny):
+    """Timestep invariance (Section 3.1): the denoise only reads the cache."""
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(3):
+        eng.write_frame(frames[t])
+    eng.synchronize()
+    before = eng.cache.clone()
+    for k in range(3):
+        eng.denoise(WL.make_state(cfg, k), WL.make_noise(cfg, k))
+        eng.synchronize()
+        assert torch.equal(before, eng.cache)
+    eng.close()
+
+
+def test_tiny_per_step_velocity(tiny):
+    """Each Euler step on its own: v_k = (x_{k+1} - x_k) / dt from a 1-step call
+    started at the oracle's x_k (a check that x_K alone could hide)."""
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(2):
+        eng.write_frame(frames[t])
+    state, noise = WL.make_state(cfg, 1), WL.make_noise(cfg, 1)
+    taus = cfg.taus()
+    diag = {}
+    O.denoise_chunk(cfg, w, sk, sv, frames, 2, state, noise, taus, diag=diag)
+    x = noise[0].astype(np.float64)
+    for k in range(cfg.num_steps):
+        xk32 = x.astype(np.float32)
+        got = eng.denoise(state, xk32[None], num_steps=1, taus=[taus[k], taus[k + 1]])
+        eng.synchronize()
+        dt = float(taus[k + 1]) - float(taus[k])
+        v_gpu = (got.cpu().numpy()[0].astype(np.float64) - xk32) / dt
+        v_ref = diag["v"][0][k]
+        assert np.max(np.abs(v_gpu - v_ref)) <= 1e-3, k
+        x = x + dt * v_ref
+    eng.close()
+
+
+def test_tiny_graph_replay_is_deterministic(tiny):
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    eng.write_frame(frames[0])
+    state = torch.from_numpy(WL.make_state(cfg, 0)).cuda()
+    noise = torch.from_numpy(WL.make_noise(cfg, 0)).cuda()
+    outs = []
+    for _ in range(4):
+        outs.append(eng.denoise(state, noise).clone())
+        eng.synchronize()
+        torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o, outs[0])
+    eng.close()
+
+
+def test_tiny_scale_only_and_custom_schedule():
+    cfg = WL.CONFIGS["tiny_fp32"].replace(mod_mode="scale_only", num_steps=5,
+                                          tau_schedule=(1.0, 0.97, 0.6, 0.3, 0.02, 0.0))
+    w, sk, sv, frames = _setup(cfg, 3)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(3):
+        eng.write_frame(frames[t])
+    state, noise = WL.make_state(cfg, 2), WL.make_noise(cfg, 2)
+    got = eng.denoise(state, noise, taus=cfg.taus())
+    eng.synchronize()
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 3, state, noise, cfg.taus())
+    assert np.max(np.abs(got.cpu().numpy() - ref)) <= FP32_TOL
+    eng.close()
+
+
+@pytest.mark.parametrize("frame_dim", [72, 0])
+def test_ragged_multi_env(frame_dim):
+    """Partial key tiles (Ls = 40, F = 24), partial query blocks (T*Hq = 18),
+    three independent envs, a 3-slot ring wrapped twice, both frame paths."""
+    cfg = RAGGED.replace(frame_dim=frame_dim)
+    w, sk, sv, frames = _setup(cfg, 7)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(7):
+        eng.write_frame(frames[t])
+        if t in (0, 2, 6):
+            state, noise = WL.make_state(cfg, t), WL.make_noise(cfg, t)
+            got = eng.denoise(state, noise)
+            eng.synchronize()
+            ref = O.denoise_chunk(cfg, w, sk, sv, frames, t + 1, state, noise, cfg.taus())
+            assert np.max(np.abs(got.cpu().numpy() - ref)) <= FP32_TOL, t
+    eng.close()
+
+
+def test_dtype_probe_rejects_mismatch(tiny):
+    cfg, w, sk, sv, frames = tiny
+    with pytest.raises(R.ReflexError) as ei:
+        R.ReflexEngine(cfg, w, sk, sv, weight_dtype_override=torch.bfloat16)
+    assert ei.value.status == R.REFLEX_EDTYPE
+
+
+def test_denoise_rejects_bad_steps(tiny):
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    with pytest.raises(R.ReflexError) as ei:
+        eng.denoise(WL.make_state(cfg, 0), WL.make_noise(cfg, 0), num_steps=cfg.num_steps + 1)
+    assert ei.value.status == R.REFLEX_EINVAL
+    eng.close()
