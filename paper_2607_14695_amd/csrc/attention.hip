@@ -8,21 +8,30 @@
 // read in physical order; the result equals one softmax over the concatenated
 // context (Appendix A, Proposition A.1).
 //
-// Decomposition: blockIdx = (key split, 64-row query block, env).  A split
-// owns a contiguous range of 64-key tiles; the dynamic tile comes last.  Each
-// tile's K rows and V^T columns are staged in LDS once and reused by all 64
-// query rows of the block (4 waves x 16 rows).
+// Inputs come ready from the QKV projection's epilogue: RoPE-rotated q rows
+// and dynamic keys, and transposed dynamic values zero-padded to 64 columns,
+// so the dynamic tile is staged exactly like a cached tile.
 //
-// Per wave the scores are computed transposed, S^T = K Q^T, with MFMA (A = K
-// rows, B = the wave's 16 query rows held in registers).  In that layout each
+// Decomposition and placement.  A workgroup owns one 64-row query block of one
+// env and a contiguous range of 64-key tiles (a key split); the dynamic tile
+// comes last.  All query blocks of one (env, split) group share the same K/V
+// tiles, so the 1-D grid is laid out such that a group's blocks are
+// dispatched to the same XCD (workgroups go round-robin over the 8 XCDs): the
+// tiles then come from HBM once and from that XCD's L2 for the other blocks.
+// Each tile's K rows and V^T columns are staged in LDS and reused by the
+// block's 64 rows (4 waves x 16 rows); the next tile's global loads are issued
+// into registers before the current tile's MFMAs.
+//
+// Per wave the scores are computed transposed, S^T = K Q^T (A = K rows from
+// LDS, B = the wave's 16 query rows held in registers).  In that layout each
 // lane holds, for its query row, 4 consecutive keys of every 16-key block, so
 // exp(S^T - m) is already the B operand of O^T = V^T P^T: the probabilities
-// never leave registers.  V is stored transposed (d-major) in the cache so the
-// A operand V^T[d][keys] is a contiguous LDS read.  Online softmax in base 2;
-// row max / sum cross the 4 lane groups with two xor shuffles.
+// never leave registers.  V is stored transposed (d-major) so V^T[d][keys] is
+// a contiguous LDS read.  Online softmax in base 2; the row max / sum cross
+// the 4 lane groups with two xor shuffles.
 //
-// With more than one split each block writes (O unnormalised, m, l) and a
-// merge kernel combines the splits with log-sum-exp weights.
+// With more than one key split each block writes (O unnormalised, m, l) and a
+// merge kernel combines the splits with log-sum-exp weights in a fixed order.
 #include "common.h"
 #include "kernels.h"
 
@@ -30,63 +39,53 @@ namespace reflex {
 
 constexpr int AKT = 64;  // keys per tile
 
+// (group, query block) of a workgroup in the XCD-aware 1-D grid; false if
+// the workgroup is padding.
+RFX_DEV bool attn_decode(int bid, int groups, int nrb, int& group, int& rb) {
+  const int xcd = bid & 7, slot = bid >> 3;
+  const int gx = slot / nrb;
+  rb = slot - gx * nrb;
+  group = gx * 8 + xcd;
+  return group < groups;
+}
+
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
   constexpr int ES = (int)sizeof(T);
   constexpr int KPF = ElemT<T>::kPerFrag;
-  constexpr int KSD = 4 * KPF;       // head-dim elements per k-step
-  constexpr int NKS = DH / KSD;      // k-steps over the head dim
-  constexpr int NKB = AKT / 16;      // 16-key blocks per tile
-  constexpr int NDB = DH / 16;       // 16-wide d blocks of the output
-  constexpr int KROW = DH * ES + 16; // LDS bytes per K row
-  constexpr int VROW = AKT * ES + 16;// LDS bytes per V^T row
+  constexpr int KSD = 4 * KPF;        // head-dim elements per k-step
+  constexpr int NKS = DH / KSD;       // k-steps over the head dim
+  constexpr int NKB = AKT / 16;       // 16-key blocks per tile
+  constexpr int NDB = DH / 16;        // 16-wide d blocks of the output
+  constexpr int KROW = DH * ES + 16;  // LDS bytes per K row
+  constexpr int VROW = AKT * ES + 16; // LDS bytes per V^T row
+  constexpr int KCH = DH * ES / 16;   // 16-byte chunks per K row
+  constexpr int VCH = AKT * ES / 16;  // 16-byte chunks per V^T row (one tile)
+  constexpr int NKL = AKT * KCH / 256;  // K chunks per thread
+  constexpr int NVL = DH * VCH / 256;   // V^T chunks per thread
   __shared__ __attribute__((aligned(16))) unsigned char Ks[AKT * KROW];
   __shared__ __attribute__((aligned(16))) unsigned char Vts[DH * VROW];
 
+  int group, rb;
+  if (!attn_decode(blockIdx.x, p.B * p.nsplit, p.rows_pad / 64, group, rb)) return;
+  const int b = group / p.nsplit, split = group - b * p.nsplit;
+
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int split = blockIdx.x, rb = blockIdx.y, b = blockIdx.z;
   const int T_ = p.T, Hq = p.Hq;
   const int nrows = T_ * Hq;
   const int rq = rb * 64 + wave * 16 + r16;
   const bool qvalid = rq < nrows;
   const int iq = qvalid ? rq / Hq : 0;
   const int jq = qvalid ? rq % Hq : 0;
-  const int64_t ldq = (int64_t)(Hq + 2) * DH;
   const int64_t mrow0 = (int64_t)b * T_;
 
-  // ---- query fragments with RoPE at the dynamic position --------------------
+  // ---- query fragments (RoPE applied by the projection epilogue) -----------
   uint4 qf[NKS];
   {
-    float q[NKS][KPF];
+    const T* qrow = reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + rq) * DH + g * KPF;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-      for (int e = 0; e < KPF; ++e) q[ks][e] = 0.f;
-    if (qvalid) {
-      for (int sp = 0; sp < p.qkv_splits; ++sp) {
-        const float* src = p.qkv + sp * p.qkv_split_stride + (mrow0 + iq) * ldq + jq * DH + g * KPF;
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-          for (int e = 0; e < KPF; e += 4) {
-            const float4 v = *reinterpret_cast<const float4*>(src + ks * KSD + e);
-            q[ks][e] += v.x; q[ks][e + 1] += v.y; q[ks][e + 2] += v.z; q[ks][e + 3] += v.w;
-          }
-      }
-      const float2* rope = p.rope + (int64_t)iq * (DH / 2);
-#pragma unroll
-      for (int ks = 0; ks < NKS / 2; ++ks)
-#pragma unroll
-        for (int e = 0; e < KPF; ++e) {
-          const float2 cs = rope[ks * KSD + g * KPF + e];
-          const float lo = q[ks][e], hi = q[ks + NKS / 2][e];
-          q[ks][e] = lo * cs.x - hi * cs.y;
-          q[ks + NKS / 2][e] = hi * cs.x + lo * cs.y;
-        }
-    }
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[ks] = f_to_frag(q[ks], T());
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = qvalid ? ld16(qrow + ks * KSD) : zero16();
   }
 
   // ---- key range of this split ---------------------------------------------
@@ -100,73 +99,70 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
 
   const T* ck = reinterpret_cast<const T*>(p.cache_k) + (int64_t)b * p.ck_bstride;
   const T* cvt = reinterpret_cast<const T*>(p.cache_vt) + (int64_t)b * p.ck_bstride;
+  const T* kdb = reinterpret_cast<const T*>(p.kd) + (int64_t)b * T_ * DH;
+  const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
   const float scale = rsqrtf((float)DH) * 1.4426950408889634f;  // 1/sqrt(d) * log2(e)
+
+  // global -> register staging of one tile (zero rows / columns past the end)
+  uint4 rk[NKL], rv[NVL];
+  auto gload = [&](int t) {
+    const bool dyn = t >= n_ct;
+    const int base = dyn ? (t - n_ct) * AKT : t * AKT;
+    const int lim = dyn ? T_ : Lc;
+    const T* ksrc = dyn ? kdb : ck;
+#pragma unroll
+    for (int i = 0; i < NKL; ++i) {
+      const int c = tid + 256 * i;
+      const int kr = c / KCH, cc = c % KCH;
+      const int r = base + kr;
+      rk[i] = r < lim ? ld16(reinterpret_cast<const unsigned char*>(ksrc + (int64_t)r * DH) + cc * 16) : zero16();
+    }
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int c = tid + 256 * i;
+      const int d = c / VCH, cc = c % VCH;
+      const int key = base + cc * (16 / ES);
+      if (dyn) {  // padded to tpad columns, zero beyond T
+        rv[i] = ld16(reinterpret_cast<const unsigned char*>(vdb + (int64_t)d * p.tpad + key));
+      } else {
+        rv[i] = key < lim ? ld16(reinterpret_cast<const unsigned char*>(cvt + (int64_t)d * p.R + key)) : zero16();
+      }
+    }
+  };
 
   f32x4_v o[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) o[db] = f32x4_v{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
+  if (t_beg < t_end) gload(t_beg);
   for (int t = t_beg; t < t_end; ++t) {
     const bool dyn = t >= n_ct;
     __syncthreads();  // previous tile fully consumed
-    if (!dyn) {
-      const int r0 = t * AKT;
-      constexpr int KCH = DH * ES / 16;  // 16-byte chunks per K row
-      for (int c = tid; c < AKT * KCH; c += 256) {
-        const int kr = c / KCH, cc = c % KCH;
-        const int r = r0 + kr;
-        uint4 v = zero16();
-        if (r < Lc) v = ld16(reinterpret_cast<const unsigned char*>(ck + (int64_t)r * DH) + cc * 16);
-        st16(&Ks[kr * KROW + cc * 16], v);
-      }
-      constexpr int VCH = AKT * ES / 16;  // 16-byte chunks per V^T row
-      for (int c = tid; c < DH * VCH; c += 256) {
-        const int d = c / VCH, cc = c % VCH;
-        const int key = r0 + cc * (16 / ES);
-        uint4 v = zero16();
-        if (key < Lc) v = ld16(reinterpret_cast<const unsigned char*>(cvt + (int64_t)d * p.R + key));
-        st16(&Vts[d * VROW + cc * 16], v);
-      }
-    } else {
-      const int kd0 = (t - n_ct) * AKT;
-      for (int c = tid; c < AKT * (DH / 2); c += 256) {
-        const int kr = c / (DH / 2), f = c % (DH / 2);
-        const int kd = kd0 + kr;
-        float klo = 0.f, khi = 0.f, vlo = 0.f, vhi = 0.f;
-        if (kd < T_) {
-          for (int sp = 0; sp < p.qkv_splits; ++sp) {
-            const float* src = p.qkv + sp * p.qkv_split_stride + (mrow0 + kd) * ldq + (int64_t)Hq * DH;
-            klo += src[f];
-            khi += src[f + DH / 2];
-            vlo += src[DH + f];
-            vhi += src[DH + f + DH / 2];
-          }
-          const float2 cs = p.rope[(int64_t)kd * (DH / 2) + f];
-          const float a = klo * cs.x - khi * cs.y;
-          khi = khi * cs.x + klo * cs.y;
-          klo = a;
-        }
-        T* krow = reinterpret_cast<T*>(&Ks[kr * KROW]);
-        krow[f] = from_f<T>(klo);
-        krow[f + DH / 2] = from_f<T>(khi);
-        reinterpret_cast<T*>(&Vts[f * VROW])[kr] = from_f<T>(vlo);
-        reinterpret_cast<T*>(&Vts[(f + DH / 2) * VROW])[kr] = from_f<T>(vhi);
-      }
+#pragma unroll
+    for (int i = 0; i < NKL; ++i) {
+      const int c = tid + 256 * i;
+      st16(&Ks[(c / KCH) * KROW + (c % KCH) * 16], rk[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int c = tid + 256 * i;
+      st16(&Vts[(c / VCH) * VROW + (c % VCH) * 16], rv[i]);
     }
     __syncthreads();
+    if (t + 1 < t_end) gload(t + 1);  // in flight during this tile's math
 
     // S^T = K Q^T for this tile: s[kb][i] = score(key kb*16 + 4g + i, query r16)
     f32x4_v s[NKB];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-      s[kb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+    for (int kb = 0; kb < NKB; ++kb) s[kb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
         const uint4 a = *reinterpret_cast<const uint4*>(&Ks[(kb * 16 + r16) * KROW + ks * 64 + g * 16]);
         mfma_step(s[kb], a, qf[ks], T());
       }
-    }
     // scale + mask, tile max
     float mt = -INFINITY;
 #pragma unroll
@@ -245,42 +241,61 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int i = 0; i < 4; ++i) dst[db * 16 + 4 * g + i] = from_f<T>(o[db][i] * inv);
-  } else {
-    const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq;
-    float* dst = p.part_o + prow * DH;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      *reinterpret_cast<float4*>(dst + db * 16 + 4 * g) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
-    if (g == 0) {
-      p.part_ml[prow * 2] = m_run;
-      p.part_ml[prow * 2 + 1] = l_run;
-    }
+    return;
   }
+  const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq;
+  float* dst = p.part_o + prow * DH;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+    *reinterpret_cast<float4*>(dst + db * 16 + 4 * g) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+  if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
 }
 
-// Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+// Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
+// splits combined in index order.  One thread per (query row, d).
+constexpr int kMaxSplits = 32;
+
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   constexpr int RPB = 256 / DH;  // rows per block
+  __shared__ float wts[RPB][kMaxSplits];
+  __shared__ float inv_l[RPB];
   const int b = blockIdx.y;
-  const int rq = blockIdx.x * RPB + threadIdx.x / DH;
-  const int d = threadIdx.x % DH;
+  const int rsub = threadIdx.x / DH, d = threadIdx.x % DH;
+  const int rq = blockIdx.x * RPB + rsub;
   const int nrows = p.T * p.Hq;
-  if (rq >= nrows) return;
-  float M = -INFINITY;
-  for (int s = 0; s < p.nsplit; ++s)
-    M = fmaxf(M, p.part_ml[(((int64_t)b * p.nsplit + s) * p.rows_pad + rq) * 2]);
-  const float Mu = (M == -INFINITY) ? 0.f : M;
-  float L = 0.f, acc = 0.f;
-  for (int s = 0; s < p.nsplit; ++s) {
-    const int64_t prow = ((int64_t)b * p.nsplit + s) * p.rows_pad + rq;
-    const float w = exp2f(p.part_ml[prow * 2] - Mu);
-    L += w * p.part_ml[prow * 2 + 1];
-    acc += w * p.part_o[prow * DH + d];
+  const int64_t base = (int64_t)b * p.nsplit * p.rows_pad;
+  if (d == 0 && rq < nrows) {
+    float m[kMaxSplits], M = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < kMaxSplits; ++s) {
+      m[s] = -INFINITY;
+      if (s < p.nsplit) {
+        const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + (base + (int64_t)s * p.rows_pad + rq) * 2);
+        m[s] = ml.x;
+        wts[rsub][s] = ml.y;
+        M = fmaxf(M, ml.x);
+      }
+    }
+    const float Mu = (M == -INFINITY) ? 0.f : M;
+    float L = 0.f;
+#pragma unroll
+    for (int s = 0; s < kMaxSplits; ++s)
+      if (s < p.nsplit) {
+        const float w = exp2f(m[s] - Mu);
+        L += w * wts[rsub][s];
+        wts[rsub][s] = w;
+      }
+    inv_l[rsub] = L > 0.f ? 1.f / L : 0.f;
   }
+  __syncthreads();
+  if (rq >= nrows) return;
+  float acc = 0.f;
+#pragma unroll 8
+  for (int s = 0; s < p.nsplit; ++s) acc += wts[rsub][s] * p.part_o[(base + (int64_t)s * p.rows_pad + rq) * DH + d];
   const int i = rq / p.Hq, j = rq % p.Hq;
   T* dst = reinterpret_cast<T*>(p.out) + ((int64_t)b * p.T + i) * (int64_t)(p.Hq * DH) + j * DH + d;
-  *dst = from_f<T>(L > 0.f ? acc / L : 0.f);
+  *dst = from_f<T>(acc * inv_l[rsub]);
 }
 
 int attention_pick_splits(int B, int rows, int max_keys, int head_dim) {
@@ -288,27 +303,20 @@ int attention_pick_splits(int B, int rows, int max_keys, int head_dim) {
   const int rbs = (rows + 63) / 64;
   const int base = B * rbs;
   const int tiles = (max_keys + AKT - 1) / AKT + 1;
-  int s = (256 + base - 1) / base;
+  // one workgroup per CU is resident (register bound): aim for ~1 wave of
+  // workgroups over 256 CUs, at least two tiles per split
+  int s = 256 / base;
   const int cap = (tiles + 1) / 2;
   if (s > cap) s = cap;
+  if (s > kMaxSplits) s = kMaxSplits;
   return s < 1 ? 1 : s;
 }
 
 template <typename T, int DH>
 static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
-  dim3 grid(a.nsplit, (a.T * a.Hq + 63) / 64, a.B);
-  RFX_LAUNCH((attn_kernel<T, DH>), grid, dim3(256), 0, s, a);
-}
-
-template <typename T>
-hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
-  switch (head_dim) {
-    case 64: launch_attn_dh<T, 64>(a, s); break;
-    case 128: launch_attn_dh<T, 128>(a, s); break;
-    case 256: launch_attn_dh<T, 256>(a, s); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  const int groups = a.B * a.nsplit, nrb = a.rows_pad / 64;
+  const int nwg = ((groups + 7) / 8) * 8 * nrb;
+  RFX_LAUNCH((attn_kernel<T, DH>), dim3(nwg), dim3(256), 0, s, a);
 }
 
 template <typename T, int DH>
@@ -319,7 +327,20 @@ static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
 }
 
 template <typename T>
+hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
+  if (a.nsplit < 1 || a.nsplit > kMaxSplits || a.rows_pad % 64) return hipErrorInvalidValue;
+  switch (head_dim) {
+    case 64: launch_attn_dh<T, 64>(a, s); break;
+    case 128: launch_attn_dh<T, 128>(a, s); break;
+    case 256: launch_attn_dh<T, 256>(a, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
 hipError_t launch_attn_merge(const AttnArgs& a, int head_dim, hipStream_t s) {
+  if (a.nsplit <= 1) return hipSuccess;
   switch (head_dim) {
     case 64: launch_merge_dh<T, 64>(a, s); break;
     case 128: launch_merge_dh<T, 128>(a, s); break;

@@ -1,22 +1,30 @@
-// MFMA GEMMs for the dense projections of the action expert: packed QKV,
-// output projection, packed gate|up with the gated-GELU epilogue, down
-// projection, the conditioning MLPs and the frame K/V projection
-// (Section 3.4 "Operator Fusion": packed W_QKV and packed gate/up).
+// MFMA GEMMs for the dense projections of the action expert: packed QKV with
+// the RoPE epilogue, output projection, packed gate|up with the gated-GELU
+// epilogue, down projection, the conditioning MLPs and the frame K/V
+// projection (Section 3.4 "Operator Fusion": packed W_QKV and packed gate/up).
 //
 // C[M][N] = A[M][K] * B[N][K]^T, both operands K-contiguous, fp32 accumulate.
+//
+// Paired strips.  Two epilogues combine two output columns that are far apart
+// in N: the gated GELU needs gate column c and up column N + c, rotate-half
+// RoPE needs columns d and d + head_dim/2 of the same head.  A workgroup
+// therefore owns a strip of "first" columns together with the strip they pair
+// with, so both values of every pair end up in the same lane of the same wave
+// and the epilogue works in registers.  For QKV this lets the projection write
+// RoPE-rotated bf16 q rows, dynamic keys and transposed dynamic values straight
+// into the layouts the attention kernel reads.
 //
 // Two regimes:
 //  * gemm_skinny (M <= 64): weight streaming.  At one environment the
 //    activations are 51 rows while every weight byte is read once per Euler
 //    step, so the kernel is bound by HBM bandwidth on the weights.  A workgroup
-//    owns a 16- or 32-column strip and a K range; its four waves interleave
-//    k-steps so that, per weight row, the wave group reads 256 contiguous
-//    bytes per round; fragments go straight from global memory into MFMA
-//    operands (no LDS staging: every weight byte is used by all rows in the
-//    same instruction).  The four waves' partial tiles are summed through LDS.
-//    K may be split across workgroups; the split partials are summed by the
-//    consumer kernel (attention for QKV, the residual/norm kernel for the
-//    output and down projections), so no atomics and no extra launch.
+//    owns a 32-column strip (or a 16 + 16 paired strip) and a K range; its four
+//    waves interleave k-steps so that, per weight row, the wave group reads 256
+//    contiguous bytes per round; fragments go straight from global memory into
+//    MFMA operands (every weight byte is used by all rows in one instruction).
+//    The waves' partial tiles are summed through LDS.  K may be split across
+//    workgroups for the plain fp32 epilogue; the consumer (the residual/norm
+//    kernel) sums the split partials, so no atomics and no extra launch.
 //  * gemm_tiled (M > 64): 128x128 workgroup tiles, 2x2 waves of 64x64, two
 //    k-steps (128 bytes of K per row) per LDS stage, double-buffered LDS with
 //    the next stage's global loads in flight during the MFMAs.
@@ -25,39 +33,79 @@
 
 namespace reflex {
 
+enum Pair : int { PAIR_NONE = 0, PAIR_N = 1, PAIR_HEAD = 2 };
+
+template <int EPI>
+struct EpiPair {
+  static constexpr int value = EPI == EPI_GELU ? PAIR_N : (EPI == EPI_ROPE ? PAIR_HEAD : PAIR_NONE);
+};
+
+// Store one output (plain epilogues) or one column pair (paired epilogues).
+// For paired epilogues `col` is the first column, v its value, u the value of
+// the paired column.
 template <int EPI, typename T>
 RFX_DEV void epilogue_store(const GemmArgs& p, int z, int split, int row, int col, float v, float u) {
-  if (EPI == EPI_F32 || EPI == EPI_MOD) {
+  if constexpr (EPI == EPI_F32 || EPI == EPI_MOD) {
     if (EPI == EPI_MOD && p.mod_width > 0 && col >= p.mod_width) v = (col < 2 * p.mod_width) ? 0.f : 1.f;
     float* o = reinterpret_cast<float*>(p.out) + (int64_t)z * p.o_bstride +
                (int64_t)split * p.o_split_stride + (int64_t)row * p.ldo + col;
     *o = v;
-  } else {
+  } else if constexpr (EPI == EPI_SILU) {
     T* o = reinterpret_cast<T*>(p.out) + (int64_t)z * p.o_bstride + (int64_t)row * p.ldo + col;
-    if (EPI == EPI_SILU)
-      *o = from_f<T>(silu(v));
-    else
-      *o = from_f<T>(gelu_tanh(v) * u);
+    *o = from_f<T>(silu(v));
+  } else if constexpr (EPI == EPI_GELU) {
+    T* o = reinterpret_cast<T*>(p.out) + (int64_t)z * p.o_bstride + (int64_t)row * p.ldo + col;
+    *o = from_f<T>(gelu_tanh(v) * u);
+  } else {  // EPI_ROPE
+    const QkvOut& q = p.qkv;
+    const int dh = q.head_dim, half = dh >> 1;
+    const int head = col / dh, d = col - head * dh;  // d < half
+    const int b = row / q.T, i = row - b * q.T;
+    if (head <= q.Hq) {
+      const float2 cs = q.rope[i * half + d];
+      const float lo = v * cs.x - u * cs.y;
+      const float hi = u * cs.x + v * cs.y;
+      T* dst = head < q.Hq
+                   ? reinterpret_cast<T*>(q.q) + ((int64_t)b * q.rows_pad + i * q.Hq + head) * dh
+                   : reinterpret_cast<T*>(q.k) + ((int64_t)b * q.T + i) * dh;
+      dst[d] = from_f<T>(lo);
+      dst[d + half] = from_f<T>(hi);
+    } else {
+      T* dst = reinterpret_cast<T*>(q.vt) + (int64_t)b * dh * q.tpad;
+      dst[(int64_t)d * q.tpad + i] = from_f<T>(v);
+      dst[(int64_t)(d + half) * q.tpad + i] = from_f<T>(u);
+    }
   }
 }
 
 // --------------------------------------------------------------------------
-// skinny: M <= 16*MB rows per workgroup chunk, NB 16-col blocks per strip
+// skinny: 16*MB rows per workgroup chunk, NB 16-col blocks per strip
 // --------------------------------------------------------------------------
-template <typename T, int MB, int NB, bool DUAL, int EPI>
+template <typename T, int MB, int NB, int EPI>
 __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
+  constexpr int PAIR = EpiPair<EPI>::value;
   constexpr int KPF = ElemT<T>::kPerFrag;
-  constexpr int KS = 4 * KPF;             // elements per k-step
-  constexpr int NBT = DUAL ? 2 * NB : NB; // B fragments per k-step
-  constexpr int COLS = 16 * NB;           // output columns per workgroup
-  constexpr int RCOLS = 16 * NBT + 1;     // LDS reduction row (padded)
+  constexpr int KS = 4 * KPF;                      // elements per k-step
+  constexpr int NBT = PAIR ? 2 * NB : NB;          // B fragments per k-step
+  constexpr int COLS = 16 * NB;                    // first columns per workgroup
+  constexpr int RCOLS = 16 * NBT + 1;              // LDS reduction row (padded)
   __shared__ float red[4][MB * 16][RCOLS];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int z = blockIdx.z;
   const int mchunk = blockIdx.y / p.splits, split = blockIdx.y % p.splits;
-  const int m0 = mchunk * (16 * MB), n0 = blockIdx.x * COLS;
+  const int m0 = mchunk * (16 * MB);
+  int n0, pair_off;
+  if constexpr (PAIR == PAIR_HEAD) {
+    const int half = p.qkv.head_dim >> 1, per_head = half / COLS;
+    const int h = blockIdx.x / per_head;
+    n0 = h * p.qkv.head_dim + (blockIdx.x - h * per_head) * COLS;
+    pair_off = half;
+  } else {
+    n0 = blockIdx.x * COLS;
+    pair_off = p.N;  // PAIR_N: up rows follow the gate rows
+  }
   const int kbeg = split * p.k_per_split;
   const int kend = min(p.K, kbeg + p.k_per_split);
 
@@ -72,8 +120,13 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
   const T* brow[NBT];
 #pragma unroll
   for (int nb = 0; nb < NBT; ++nb) {
-    const int c = min(n0 + (nb % NB) * 16 + r16, p.N - 1);
-    const int brw = (DUAL && nb >= NB) ? p.N + c : c;
+    int brw;
+    if (PAIR == PAIR_NONE) {
+      brw = min(n0 + nb * 16 + r16, p.N - 1);
+    } else {
+      const int c = n0 + (nb % NB) * 16 + r16;
+      brw = nb >= NB ? c + pair_off : c;
+    }
     brow[nb] = B + (int64_t)brw * p.ldb + g * KPF;
   }
 
@@ -84,7 +137,7 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
     for (int nb = 0; nb < NBT; ++nb) acc[mb][nb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
 
   const int nsteps = (kend - kbeg + KS - 1) / KS;
-  constexpr int U = 2;
+  constexpr int U = 4;
   for (int s0 = wave; s0 < nsteps; s0 += 4 * U) {
     uint4 bf[U][NBT], af[U][MB];
 #pragma unroll
@@ -114,23 +167,25 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
 
   for (int e = threadIdx.x; e < MB * 16 * COLS; e += 256) {
     const int row = e / COLS, col = e % COLS;
-    const int grow = m0 + row, gcol = n0 + col;
-    if (grow >= p.M || gcol >= p.N) continue;
-    float v = red[0][row][col] + red[1][row][col] + red[2][row][col] + red[3][row][col];
+    const int grow = m0 + row;
+    const int gcol = PAIR == PAIR_NONE ? n0 + col : n0 + col;
+    if (grow >= p.M || (PAIR == PAIR_NONE && gcol >= p.N)) continue;
+    const float v = red[0][row][col] + red[1][row][col] + red[2][row][col] + red[3][row][col];
     float u = 0.f;
-    if (DUAL) u = red[0][row][col + COLS] + red[1][row][col + COLS] + red[2][row][col + COLS] +
+    if (PAIR) u = red[0][row][col + COLS] + red[1][row][col + COLS] + red[2][row][col + COLS] +
                   red[3][row][col + COLS];
     epilogue_store<EPI, T>(p, z, split, grow, gcol, v, u);
   }
 }
 
 // --------------------------------------------------------------------------
-// tiled: 128 x 128 workgroup tile (DUAL: 128 rows x 64 gate + 64 up columns)
+// tiled: 128 x 128 workgroup tile (paired: 128 rows x 64 first + 64 paired cols)
 // --------------------------------------------------------------------------
-constexpr int TBM = 128, TBN = 128, TROWB = 128, TPAD = 16;  // bytes of K per stage row
+constexpr int TBM = 128, TBN = 128, TROWB = 128, TPAD = 16;  // TROWB: bytes of K per stage row
 
-template <typename T, bool DUAL, int EPI>
+template <typename T, int EPI>
 __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
+  constexpr int PAIR = EpiPair<EPI>::value;
   constexpr int KPF = ElemT<T>::kPerFrag;
   constexpr int KSTAGE = TROWB / (int)sizeof(T);  // elements of K per stage
   constexpr int LROW = TROWB + TPAD;              // LDS row stride, bytes
@@ -142,8 +197,19 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
   const int wm = wave >> 1, wn = wave & 1;
   const int z = blockIdx.z / p.splits, split = blockIdx.z % p.splits;
   const int m0 = blockIdx.y * TBM;
-  const int ncols = DUAL ? TBN / 2 : TBN;  // output columns per tile
-  const int n0 = blockIdx.x * ncols;
+  int n0, pair_off;
+  if constexpr (PAIR == PAIR_HEAD) {
+    const int half = p.qkv.head_dim >> 1, per_head = half / 64;
+    const int h = blockIdx.x / per_head;
+    n0 = h * p.qkv.head_dim + (blockIdx.x - h * per_head) * 64;
+    pair_off = half;
+  } else if constexpr (PAIR == PAIR_N) {
+    n0 = blockIdx.x * 64;
+    pair_off = p.N;
+  } else {
+    n0 = blockIdx.x * TBN;
+    pair_off = 0;
+  }
   const int kbeg = split * p.k_per_split;
   const int kend = min(p.K, kbeg + p.k_per_split);
   const int nstage = (kend - kbeg + KSTAGE - 1) / KSTAGE;
@@ -160,9 +226,9 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
     const int r = (tid >> 3) + 32 * i;
     ga[i] = A + (int64_t)min(m0 + r, p.M - 1) * p.lda + ch * KPF;
     int brw;
-    if (DUAL) {
-      const int c = min(n0 + (r & 63), p.N - 1);
-      brw = (r >= 64) ? p.N + c : c;
+    if (PAIR != PAIR_NONE) {
+      const int c = n0 + (r & 63);
+      brw = r >= 64 ? c + pair_off : c;
     } else {
       brw = min(n0 + r, p.N - 1);
     }
@@ -170,12 +236,12 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
   }
   uint4 ra[4], rb[4];
   auto gload = [&](int st) {
-    const int k = kbeg + st * KSTAGE + ch * KPF;
-    const bool ok = k < kend;
+    const int k0 = kbeg + st * KSTAGE;
+    const bool ok = k0 + ch * KPF < kend;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      ra[i] = ok ? ld16(ga[i] + (k - ch * KPF)) : zero16();
-      rb[i] = ok ? ld16(gb[i] + (k - ch * KPF)) : zero16();
+      ra[i] = ok ? ld16(ga[i] + k0) : zero16();
+      rb[i] = ok ? ld16(gb[i] + k0) : zero16();
     }
   };
   auto lstore = [&](int buf) {
@@ -196,7 +262,7 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
   int brow_l[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) {
-    if (DUAL)
+    if (PAIR != PAIR_NONE)
       brow_l[nb] = (nb < 2 ? 0 : 64) + wn * 32 + (nb & 1) * 16 + r16;
     else
       brow_l[nb] = wn * 64 + nb * 16 + r16;
@@ -234,11 +300,11 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
     for (int i = 0; i < 4; ++i) {
       const int grow = m0 + wm * 64 + mb * 16 + 4 * g + i;
       if (grow >= p.M) continue;
-      if (DUAL) {
+      if (PAIR != PAIR_NONE) {
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
           const int gcol = n0 + wn * 32 + nb * 16 + r16;
-          if (gcol < p.N) epilogue_store<EPI, T>(p, z, split, grow, gcol, acc[mb][nb][i], acc[mb][nb + 2][i]);
+          epilogue_store<EPI, T>(p, z, split, grow, gcol, acc[mb][nb][i], acc[mb][nb + 2][i]);
         }
       } else {
 #pragma unroll
@@ -259,11 +325,12 @@ static int skinny_mb(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 int gemm_pick_splits(int M, int N, int K, int elem_bytes) {
   const int ks = 64 / elem_bytes;
   if (M <= 64) {
-    const int cols = 32;  // two 16-column blocks per strip
+    const int cols = 32;
     const int base = (N + cols - 1) / cols;
-    int maxs = K / (ks * 4);
+    int maxs = K / (ks * 4 * 2);  // at least two k-steps per wave
     if (maxs < 1) maxs = 1;
-    int s = (512 + base - 1) / base;
+    int s = (256 + base - 1) / base;
+    if (s > 8) s = 8;
     return s < 1 ? 1 : (s > maxs ? maxs : s);
   }
   const int base = ((N + TBN - 1) / TBN) * ((M + TBM - 1) / TBM);
@@ -273,49 +340,63 @@ int gemm_pick_splits(int M, int N, int K, int elem_bytes) {
   return s > maxs ? maxs : s;
 }
 
-template <typename T, int MB, bool DUAL, int EPI>
+template <typename T, int MB, int EPI>
 static void launch_skinny_cfg(const GemmArgs& a, hipStream_t s) {
-  constexpr int NB = DUAL ? 1 : 2;
-  const int cols = 16 * NB;
+  constexpr int PAIR = EpiPair<EPI>::value;
+  constexpr int NB = PAIR ? 1 : 2;
+  int nx;
+  if (PAIR == PAIR_HEAD)
+    nx = a.N / 32;  // (N / head_dim) heads x (head_dim/2 / 16) strips
+  else if (PAIR == PAIR_N)
+    nx = a.N / 16;
+  else
+    nx = (a.N + 16 * NB - 1) / (16 * NB);
   const int mch = (a.M + 16 * MB - 1) / (16 * MB);
-  dim3 grid((a.N + cols - 1) / cols, mch * a.splits, a.batch);
-  RFX_LAUNCH((gemm_skinny<T, MB, NB, DUAL, EPI>), grid, dim3(256), 0, s, a);
+  dim3 grid(nx, mch * a.splits, a.batch);
+  RFX_LAUNCH((gemm_skinny<T, MB, NB, EPI>), grid, dim3(256), 0, s, a);
 }
 
-template <typename T, bool DUAL, int EPI>
+template <typename T, int EPI>
 static void launch_skinny(const GemmArgs& a, hipStream_t s) {
   switch (skinny_mb(a.M)) {
-    case 1: launch_skinny_cfg<T, 1, DUAL, EPI>(a, s); break;
-    case 2: launch_skinny_cfg<T, 2, DUAL, EPI>(a, s); break;
-    default: launch_skinny_cfg<T, 4, DUAL, EPI>(a, s); break;
+    case 1: launch_skinny_cfg<T, 1, EPI>(a, s); break;
+    case 2: launch_skinny_cfg<T, 2, EPI>(a, s); break;
+    default: launch_skinny_cfg<T, 4, EPI>(a, s); break;
   }
 }
 
-template <typename T, bool DUAL, int EPI>
+template <typename T, int EPI>
 static void launch_tiled(const GemmArgs& a, hipStream_t s) {
-  const int ncols = DUAL ? TBN / 2 : TBN;
-  dim3 grid((a.N + ncols - 1) / ncols, (a.M + TBM - 1) / TBM, a.batch * a.splits);
-  RFX_LAUNCH((gemm_tiled<T, DUAL, EPI>), grid, dim3(256), 0, s, a);
+  constexpr int PAIR = EpiPair<EPI>::value;
+  const int nx = PAIR == PAIR_NONE ? (a.N + TBN - 1) / TBN : a.N / (PAIR == PAIR_N ? 64 : 128);
+  dim3 grid(nx, (a.M + TBM - 1) / TBM, a.batch * a.splits);
+  RFX_LAUNCH((gemm_tiled<T, EPI>), grid, dim3(256), 0, s, a);
+}
+
+template <typename T, int EPI>
+static void launch_pick(const GemmArgs& a, hipStream_t s) {
+  bool skinny = a.M <= 64;
+  // paired tiles of the tiled kernel hold 64 first-half columns of one head
+  if (EPI == EPI_ROPE && a.qkv.head_dim < 128) skinny = true;
+  if (skinny)
+    launch_skinny<T, EPI>(a, s);
+  else
+    launch_tiled<T, EPI>(a, s);
 }
 
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s) {
-  const bool skinny = a.M <= 64;
+  if (a.M <= 0 || a.N <= 0 || a.K <= 0) return hipErrorInvalidValue;
+  if (epi == EPI_GELU && a.N % 64) return hipErrorInvalidValue;
+  if (epi == EPI_ROPE && (a.qkv.head_dim % 64 || a.N % a.qkv.head_dim)) return hipErrorInvalidValue;
+  if (epi != EPI_F32 && a.splits != 1) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_F32:
-      skinny ? launch_skinny<T, false, EPI_F32>(a, s) : launch_tiled<T, false, EPI_F32>(a, s);
-      break;
-    case EPI_MOD:
-      skinny ? launch_skinny<T, false, EPI_MOD>(a, s) : launch_tiled<T, false, EPI_MOD>(a, s);
-      break;
-    case EPI_SILU:
-      skinny ? launch_skinny<T, false, EPI_SILU>(a, s) : launch_tiled<T, false, EPI_SILU>(a, s);
-      break;
-    case EPI_GELU:
-      skinny ? launch_skinny<T, true, EPI_GELU>(a, s) : launch_tiled<T, true, EPI_GELU>(a, s);
-      break;
-    default:
-      return hipErrorInvalidValue;
+    case EPI_F32: launch_pick<T, EPI_F32>(a, s); break;
+    case EPI_MOD: launch_pick<T, EPI_MOD>(a, s); break;
+    case EPI_SILU: launch_pick<T, EPI_SILU>(a, s); break;
+    case EPI_GELU: launch_pick<T, EPI_GELU>(a, s); break;
+    case EPI_ROPE: launch_pick<T, EPI_ROPE>(a, s); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

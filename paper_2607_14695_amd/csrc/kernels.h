@@ -24,13 +24,23 @@ extern thread_local LaunchEvents g_launch_events;
 enum Epi : int {
   EPI_F32 = 0,   // out_f32[z][split][row][col] = acc (split-K partial sums)
   EPI_SILU = 1,  // out_t[z][row][col] = silu(acc)
-  EPI_GELU = 2,  // dual B: out_t[row][col] = gelu_tanh(acc_gate) * acc_up
+  EPI_GELU = 2,  // paired B rows c and N + c: out_t[row][c] = gelu_tanh(gate) * up
   EPI_MOD = 3,   // like EPI_F32 (one split); with mod_width > 0 the shift/gate
                  // columns are replaced by 0/1 (scale-only modulation)
+  EPI_ROPE = 4,  // packed QKV, paired columns d and d + head_dim/2 of a head:
+                 // RoPE on q and k heads, scattered to the attention layouts
 };
 
-// C[M][N] = A[M][K] * B[N][K]^T (+ epilogue).  For EPI_GELU the B rows
-// [0, N) are the gate projection and [N, 2N) the up projection.
+// Destinations of the EPI_ROPE epilogue (row m = b*T + i of the GEMM).
+struct QkvOut {
+  const float2* rope;  // [T][head_dim/2] (cos, sin) at the dynamic positions
+  void* q;             // [B][rows_pad][head_dim], row i*Hq + j  (RoPE applied)
+  void* k;             // [B][T][head_dim]                       (RoPE applied)
+  void* vt;            // [B][head_dim][tpad], column i          (V transposed)
+  int T, Hq, head_dim, rows_pad, tpad;
+};
+
+// C[M][N] = A[M][K] * B[N][K]^T (+ epilogue).
 struct GemmArgs {
   const void* A;
   const void* B;
@@ -39,10 +49,11 @@ struct GemmArgs {
   int64_t a_bstride, b_bstride;       // per blockIdx.z strides (elements)
   int64_t o_bstride, o_split_stride;  // output strides (elements)
   int M, N, K;
-  int splits;        // K split across blockIdx.y (EPI_F32 only)
+  int splits;        // K split across workgroups (EPI_F32 only)
   int k_per_split;   // multiple of the k-step
   int mod_width;     // EPI_MOD: width D, 0 = full modulation
   int batch;         // blockIdx.z extent
+  QkvOut qkv;        // EPI_ROPE only
 };
 
 template <typename T> hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);
@@ -51,10 +62,10 @@ int gemm_pick_splits(int M, int N, int K, int elem_bytes);
 
 // Partitioned-region attention (Eq. 1) for the dynamic rows of every env.
 struct AttnArgs {
-  const float* qkv;       // [qkv_splits][B*T][(Hq+2)*dh] fp32 partial sums, pre-RoPE
-  int64_t qkv_split_stride;
-  int qkv_splits;
-  const float2* rope;     // [T][dh/2] (cos, sin) at the dynamic positions
+  const void* q;          // [B][rows_pad][dh]  RoPE applied
+  const void* kd;         // [B][T][dh]         dynamic keys, RoPE applied
+  const void* vdt;        // [B][dh][tpad]      dynamic values, transposed, zero beyond T
+  int tpad;
   const void* cache_k;    // layer base: [B] stride ck_bstride, rows [R][dh]
   const void* cache_vt;   // layer base: [B] stride ck_bstride, [dh][R]
   int64_t ck_bstride;     // elements between envs (= L*R*dh)
@@ -65,7 +76,7 @@ struct AttnArgs {
   float* part_o;          // [B][nsplit][rows_pad][dh]
   float* part_ml;         // [B][nsplit][rows_pad][2]
   int rows_pad;
-  void* out;              // [B*T][Hq*dh] (written directly when nsplit == 1)
+  void* out;              // [B*T][Hq*dh]
 };
 template <typename T> hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
 template <typename T> hipError_t launch_attn_merge(const AttnArgs& a, int head_dim, hipStream_t s);

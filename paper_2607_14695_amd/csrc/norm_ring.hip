@@ -16,6 +16,41 @@
 
 namespace reflex {
 
+// 4 consecutive elements as fp32 (8-byte bf16 or 16-byte fp32 load)
+RFX_DEV float4 ld4f(const float* p) { return *reinterpret_cast<const float4*>(p); }
+RFX_DEV float4 ld4f(const bf16_t* p) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
+                     __uint_as_float(v.y & 0xffff0000u));
+}
+RFX_DEV void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+RFX_DEV void st4(bf16_t* p, float4 v) {
+  uint2 w;
+  w.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  w.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  *reinterpret_cast<uint2*>(p) = w;
+}
+RFX_DEV float4 f4add(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+
+// sum of nparts split-K partial rows, fixed order, loads issued in groups of 4
+RFX_DEV float4 sum_parts(const float* pp, int64_t stride, int nparts) {
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  int s = 0;
+  for (; s + 4 <= nparts; s += 4) {
+    const float4 a0 = ld4f(pp + (s + 0) * stride), a1 = ld4f(pp + (s + 1) * stride);
+    const float4 a2 = ld4f(pp + (s + 2) * stride), a3 = ld4f(pp + (s + 3) * stride);
+    acc = f4add(acc, a0); acc = f4add(acc, a1); acc = f4add(acc, a2); acc = f4add(acc, a3);
+  }
+  for (; s < nparts; ++s) acc = f4add(acc, ld4f(pp + s * stride));
+  return acc;
+}
+
+// y = v * r * (1 + scale) + shift for 4 columns
+RFX_DEV float4 ada4(float4 v, float r, float4 sc, float4 sh) {
+  return make_float4(v.x * r * (1.f + sc.x) + sh.x, v.y * r * (1.f + sc.y) + sh.y, v.z * r * (1.f + sc.z) + sh.z,
+                     v.w * r * (1.f + sc.w) + sh.w);
+}
+
 // ---------------------------------------------------------------------------
 // embedding + first norm: row m = b*T + t; t = 0 is the state token
 // ---------------------------------------------------------------------------
@@ -34,7 +69,15 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(EmbedArgs p) {
   for (int c = threadIdx.x; c < p.D; c += 256) {
     const T* w = W + (int64_t)c * n_in;
     float acc = 0.f;
-    for (int e = 0; e < n_in; ++e) acc += to_f(w[e]) * in[e];
+    int e = 0;
+    if ((n_in & 3) == 0) {
+      for (; e + 8 <= n_in; e += 8) {
+        const float4 w0 = ld4f(w + e), w1 = ld4f(w + e + 4);
+        acc += w0.x * in[e] + w0.y * in[e + 1] + w0.z * in[e + 2] + w0.w * in[e + 3];
+        acc += w1.x * in[e + 4] + w1.y * in[e + 5] + w1.z * in[e + 6] + w1.w * in[e + 7];
+      }
+    }
+    for (; e < n_in; ++e) acc += to_f(w[e]) * in[e];
     acc *= p.embed_scale;
     hs[c] = acc;
     ss += acc * acc;
@@ -57,35 +100,39 @@ hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// residual + norm
+// residual + norm: one block per row, 4 columns per thread
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void resid_norm_kernel(ResidArgs p) {
   __shared__ float red[4];
-  __shared__ float hs[16 * 256];
+  __shared__ float4 hs[4 * 256];
   const int m = blockIdx.x, b = m / p.T;
   const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
   const float* nmod = p.norm_mod + (int64_t)b * 3 * p.D;
+  const int D4 = p.D >> 2;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < p.D; c += 256) {
-    float acc = 0.f;
-    for (int s = 0; s < p.nparts; ++s) acc += p.parts[s * p.part_stride + (int64_t)m * p.D + c];
-    const float v = p.h[(int64_t)m * p.D + c] + gmod[c] * acc;
-    hs[c] = v;
-    ss += v * v;
+  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
+    const int c = c4 * 4;
+    const float4 acc = sum_parts(p.parts + (int64_t)m * p.D + c, p.part_stride, p.nparts);
+    const float4 h = ld4f(p.h + (int64_t)m * p.D + c);
+    const float4 gt = ld4f(gmod + c);
+    const float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+    hs[c4] = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float tot = block_sum_256(ss, red);
   const float r = rsqrtf(tot / (float)p.D + p.eps);
-  for (int c = threadIdx.x; c < p.D; c += 256) {
-    p.h[(int64_t)m * p.D + c] = hs[c];
-    const float y = hs[c] * r * (1.f + nmod[c]) + nmod[p.D + c];
-    reinterpret_cast<T*>(p.y)[(int64_t)m * p.D + c] = from_f<T>(y);
+  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
+    const int c = c4 * 4;
+    const float4 v = hs[c4];
+    st4(p.h + (int64_t)m * p.D + c, v);
+    st4(reinterpret_cast<T*>(p.y) + (int64_t)m * p.D + c, ada4(v, r, ld4f(nmod + c), ld4f(nmod + p.D + c)));
   }
 }
 
 template <typename T>
 hipError_t launch_resid_norm(const ResidArgs& a, hipStream_t s) {
-  if (a.D > 16 * 256) return hipErrorInvalidValue;
+  if (a.D > 16 * 256 || (a.D & 3)) return hipErrorInvalidValue;
   RFX_LAUNCH((resid_norm_kernel<T>), dim3(a.M), dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -96,38 +143,52 @@ hipError_t launch_resid_norm(const ResidArgs& a, hipStream_t s) {
 template <typename T>
 __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   __shared__ float red[4];
-  __shared__ float ys[16 * 256];
+  __shared__ float4 ys[4 * 256];
+  __shared__ float vpart[4][64];
   const int H = p.T - 1;
   const int b = blockIdx.x / H, i = blockIdx.x % H;
   const int64_t m = (int64_t)b * p.T + 1 + i;
   const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
   const float* fmod = p.final_mod + (int64_t)b * 3 * p.D;
+  const int D4 = p.D >> 2;
   float ss = 0.f;
-  for (int c = threadIdx.x; c < p.D; c += 256) {
-    float acc = 0.f;
-    for (int s = 0; s < p.nparts; ++s) acc += p.parts[s * p.part_stride + m * p.D + c];
-    const float v = p.h[m * p.D + c] + gmod[c] * acc;
-    ys[c] = v;
-    ss += v * v;
+  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
+    const int c = c4 * 4;
+    const float4 acc = sum_parts(p.parts + m * p.D + c, p.part_stride, p.nparts);
+    const float4 h = ld4f(p.h + m * p.D + c);
+    const float4 gt = ld4f(gmod + c);
+    const float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+    ys[c4] = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float tot = block_sum_256(ss, red);
   const float r = rsqrtf(tot / (float)p.D + p.eps);
-  for (int c = threadIdx.x; c < p.D; c += 256) ys[c] = ys[c] * r * (1.f + fmod[c]) + fmod[p.D + c];
+  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
+    const int c = c4 * 4;
+    ys[c4] = ada4(ys[c4], r, ld4f(fmod + c), ld4f(fmod + p.D + c));
+  }
   __syncthreads();
+  // v[a] = sum_c y[c] W[a][c]: wave w takes outputs a = w, w+4, ...; lanes stride the columns
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const T* W = reinterpret_cast<const T*>(p.w_aout);
-  const int64_t xo = ((int64_t)b * H + i) * p.da;
   for (int a = wave; a < p.da; a += 4) {
     float acc = 0.f;
-    for (int c = lane; c < p.D; c += 64) acc += ys[c] * to_f(W[(int64_t)a * p.D + c]);
+    for (int c4 = lane; c4 < D4; c4 += 64) {
+      const float4 w = ld4f(W + (int64_t)a * p.D + c4 * 4);
+      const float4 y = ys[c4];
+      acc += w.x * y.x + w.y * y.y + w.z * y.z + w.w * y.w;
+    }
     acc = warp_sum(acc);
-    if (lane == 0) p.x_out[xo + a] = p.x_in[xo + a] + p.dt * acc;
+    if (lane == 0) vpart[0][a] = acc;
   }
+  __syncthreads();
+  const int64_t xo = ((int64_t)b * H + i) * p.da;
+  for (int a = threadIdx.x; a < p.da; a += 256) p.x_out[xo + a] = p.x_in[xo + a] + p.dt * vpart[0][a];
 }
 
 template <typename T>
 hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s) {
-  if (a.D > 16 * 256) return hipErrorInvalidValue;
+  if (a.D > 16 * 256 || (a.D & 3) || a.da > 64) return hipErrorInvalidValue;
   RFX_LAUNCH((final_euler_kernel<T>), dim3(a.B * (a.T - 1)), dim3(256), 0, s, a);
   return hipGetLastError();
 }

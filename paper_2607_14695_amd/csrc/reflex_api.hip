@@ -56,7 +56,10 @@ struct Workspace {
   float* mod;
   float* h;
   void* y;
-  float* qkv;
+  void* q;
+  void* kd;
+  void* vdt;
+  int32_t* counters;
   void* o;
   float* part_o;
   float* part_ml;
@@ -65,13 +68,15 @@ struct Workspace {
   float* frame_scratch;
 };
 
+constexpr int kWsParts = 18;
+
 struct Plan {
-  int T, M, S, Nqkv, C, R, rows_pad, eb;
-  SplitK qkv, o, down, kv;
+  int T, M, S, Nqkv, C, R, rows_pad, tpad, nrb, eb;
+  SplitK o, down;
   int attn_splits;
   int max_parts;
   size_t cache_bytes, ws_bytes;
-  size_t off[15];
+  size_t off[kWsParts];
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -129,17 +134,17 @@ Plan make_plan(const reflex_config* c) {
   p.R = c->static_len + c->window_frames * c->frame_tokens;
   const int rows = p.T * c->n_q_heads;
   p.rows_pad = (rows + 63) / 64 * 64;
-  p.qkv = make_split(p.M, c->width, gemm_pick_splits(p.M, p.Nqkv, c->width, eb), eb);
+  p.nrb = p.rows_pad / 64;
+  p.tpad = (p.T + 63) / 64 * 64;
   p.o = make_split(p.M, c->n_q_heads * c->head_dim,
                    gemm_pick_splits(p.M, c->width, c->n_q_heads * c->head_dim, eb), eb);
   p.down = make_split(p.M, c->mlp_dim, gemm_pick_splits(p.M, c->width, c->mlp_dim, eb), eb);
-  p.kv = make_split(c->batch * c->frame_tokens, c->frame_dim > 0 ? c->frame_dim : 8, 1, eb);
   p.attn_splits = attention_pick_splits(c->batch, rows, p.R, c->head_dim);
   p.max_parts = p.o.splits > p.down.splits ? p.o.splits : p.down.splits;
 
   const size_t B = c->batch, L = c->n_layers, dh = c->head_dim, D = c->width, K = c->max_steps;
   p.cache_bytes = align256(B * L * p.R * dh * eb) * 2;
-  size_t sz[15];
+  size_t sz[kWsParts];
   sz[0] = 64;                                                             // tick
   sz[1] = (size_t)p.T * (dh / 2) * sizeof(float2);                        // rope_dyn
   sz[2] = (size_t)(c->static_len > c->frame_tokens ? c->static_len : c->frame_tokens) * (dh / 2) *
@@ -149,15 +154,18 @@ Plan make_plan(const reflex_config* c) {
   sz[5] = (size_t)p.S * K * B * 3 * D * sizeof(float);                    // mod
   sz[6] = (size_t)p.M * D * sizeof(float);                                // h
   sz[7] = (size_t)p.M * D * eb;                                           // y
-  sz[8] = (size_t)p.qkv.splits * p.M * p.Nqkv * sizeof(float);            // qkv
-  sz[9] = (size_t)p.M * c->n_q_heads * dh * eb;                           // o
-  sz[10] = B * p.attn_splits * (size_t)p.rows_pad * dh * sizeof(float);   // part_o
-  sz[11] = B * p.attn_splits * (size_t)p.rows_pad * 2 * sizeof(float);    // part_ml
-  sz[12] = (size_t)p.M * c->mlp_dim * eb;                                 // z
-  sz[13] = (size_t)p.max_parts * p.M * D * sizeof(float);                 // rparts
-  sz[14] = c->frame_dim > 0 ? B * c->frame_tokens * L * 2 * dh * sizeof(float) : 0;  // frame scratch
+  sz[8] = B * (size_t)p.rows_pad * dh * eb;                               // q
+  sz[9] = B * (size_t)p.T * dh * eb;                                      // kd
+  sz[10] = B * dh * (size_t)p.tpad * eb;                                  // vdt
+  sz[11] = B * (size_t)p.nrb * sizeof(int32_t);                           // counters
+  sz[12] = (size_t)p.M * c->n_q_heads * dh * eb;                          // o
+  sz[13] = B * p.attn_splits * (size_t)p.rows_pad * dh * sizeof(float);   // part_o
+  sz[14] = B * p.attn_splits * (size_t)p.rows_pad * 2 * sizeof(float);    // part_ml
+  sz[15] = (size_t)p.M * c->mlp_dim * eb;                                 // z
+  sz[16] = (size_t)p.max_parts * p.M * D * sizeof(float);                 // rparts
+  sz[17] = c->frame_dim > 0 ? B * c->frame_tokens * L * 2 * dh * sizeof(float) : 0;  // frame scratch
   size_t off = 0;
-  for (int i = 0; i < 15; ++i) {
+  for (int i = 0; i < kWsParts; ++i) {
     p.off[i] = off;
     off += align256(sz[i]);
   }
@@ -285,20 +293,20 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
       GemmArgs q{};
       q.A = W.y; q.lda = D;
       q.B = wqkv + (size_t)l * P.Nqkv * D * eb; q.ldb = D;
-      q.out = W.qkv; q.ldo = P.Nqkv; q.o_split_stride = (int64_t)M * P.Nqkv;
-      q.M = M; q.N = P.Nqkv; q.K = D; q.splits = P.qkv.splits; q.k_per_split = P.qkv.kps; q.batch = 1;
-      RFX_TRY(L.run(PC_QKV, [&] { return launch_gemm<T>(q, EPI_F32, st); }));
+      q.M = M; q.N = P.Nqkv; q.K = D; q.splits = 1; q.k_per_split = D + 128; q.batch = 1;
+      q.qkv = QkvOut{W.rope_dyn, W.q, W.kd, W.vdt, Tn, Hq, dh, P.rows_pad, P.tpad};
+      RFX_TRY(L.run(PC_QKV, [&] { return launch_gemm<T>(q, EPI_ROPE, st); }));
 
       AttnArgs aa{};
-      aa.qkv = W.qkv; aa.qkv_split_stride = (int64_t)M * P.Nqkv; aa.qkv_splits = P.qkv.splits;
-      aa.rope = W.rope_dyn;
+      aa.q = W.q; aa.kd = W.kd; aa.vdt = W.vdt; aa.tpad = P.tpad;
       aa.cache_k = (const char*)ctx->cache_k + (size_t)l * P.R * dh * eb;
       aa.cache_vt = (const char*)ctx->cache_vt + (size_t)l * P.R * dh * eb;
       aa.ck_bstride = (int64_t)c.n_layers * P.R * dh;
       aa.n_valid = reinterpret_cast<const int32_t*>(W.tick + 1);
       aa.static_len = c.static_len; aa.frame_tokens = c.frame_tokens; aa.R = P.R;
       aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits;
-      aa.part_o = W.part_o; aa.part_ml = W.part_ml; aa.rows_pad = P.rows_pad; aa.out = W.o;
+      aa.part_o = W.part_o; aa.part_ml = W.part_ml;
+      aa.rows_pad = P.rows_pad; aa.out = W.o;
       RFX_TRY(L.run(PC_ATTN, [&] { return launch_attention<T>(aa, dh, st); }));
       if (P.attn_splits > 1) RFX_TRY(L.run(PC_MERGE, [&] { return launch_attn_merge<T>(aa, dh, st); }));
 
@@ -481,19 +489,24 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
   W.mod = reinterpret_cast<float*>(base + P.off[5]);
   W.h = reinterpret_cast<float*>(base + P.off[6]);
   W.y = base + P.off[7];
-  W.qkv = reinterpret_cast<float*>(base + P.off[8]);
-  W.o = base + P.off[9];
-  W.part_o = reinterpret_cast<float*>(base + P.off[10]);
-  W.part_ml = reinterpret_cast<float*>(base + P.off[11]);
-  W.z = base + P.off[12];
-  W.rparts = reinterpret_cast<float*>(base + P.off[13]);
-  W.frame_scratch = reinterpret_cast<float*>(base + P.off[14]);
+  W.q = base + P.off[8];
+  W.kd = base + P.off[9];
+  W.vdt = base + P.off[10];
+  W.counters = reinterpret_cast<int32_t*>(base + P.off[11]);
+  W.o = base + P.off[12];
+  W.part_o = reinterpret_cast<float*>(base + P.off[13]);
+  W.part_ml = reinterpret_cast<float*>(base + P.off[14]);
+  W.z = base + P.off[15];
+  W.rparts = reinterpret_cast<float*>(base + P.off[16]);
+  W.frame_scratch = reinterpret_cast<float*>(base + P.off[17]);
   ctx->cache_k = cache_mem;
   ctx->cache_vt = reinterpret_cast<char*>(cache_mem) + P.cache_bytes / 2;
 
   // zeroed cache, as the paper's pre-allocated ring buffer (Appendix B.2)
   hipError_t e = hipMemsetAsync(cache_mem, 0, P.cache_bytes, ctx->stream);
-  if (e == hipSuccess) e = hipMemsetAsync(W.tick, 0, 64, ctx->stream);
+  // the workspace starts zeroed: tick state, split counters, the zero padding
+  // of the dynamic value columns beyond T
+  if (e == hipSuccess) e = hipMemsetAsync(workspace_mem, 0, P.ws_bytes, ctx->stream);
   if (e != hipSuccess) {
     delete ctx;
     return hip_fail(e);

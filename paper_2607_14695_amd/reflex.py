@@ -256,6 +256,8 @@ class ReflexEngine:
         after the denoise, so reading the result there is safe."""
         torch = self.torch
         k = num_steps if num_steps is not None else self.cfg.num_steps
+        if taus is None and self.cfg.tau_schedule is not None and k == self.cfg.num_steps:
+            taus = self.cfg.taus()  # the workload's own schedule
         caller = self._enter()
         with torch.cuda.stream(self.stream):
             s = self._staged("state", state)

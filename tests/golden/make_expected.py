@@ -1,0 +1,88 @@
+"""Write the oracle's expected action chunks for the pi0-scale GPU parity tests.
+
+Calls only the float64 oracle (``oracle/``) and the seeded input generator;
+nothing here touches the HIP library.  Run from the repository root:
+
+    python tests/golden/make_expected.py [case ...]
+
+Each case stores, per (tick, env) it samples, the final action chunk x_K and
+the per-step velocities v_k, in ``tests/golden/expected_<case>.npz`` together
+with a digest of the oracle and generator sources it was computed from.
+
+Sampled cases (the GPU test writes every frame of the stream in order; frames
+that have left the window before a sampled tick cannot affect it, so the test
+may write filler for those):
+  pi0_chunk_bf16   tick 0, env 0 (one direct-path frame in a 1-frame ring)
+  pi0_stream_bf16  ticks 0, 1, 2, 3, 250, 499, env 0 (embedding path, 2-frame ring)
+  pi0_batch32_bf16 ticks 0, 1, 2, 199, envs 0 and 31
+  pi0_long_bf16    tick 7 (ring of 8 full), envs 0 and 7, x64 embeddings, tau
+                   schedule concentrated near 0 and 1
+"""
+from __future__ import annotations
+
+import hashlib
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+from oracle import reflex_oracle as O  # noqa: E402
+from paper_2607_14695_amd import workloads as WL  # noqa: E402
+
+CASES = {
+    "pi0_chunk_bf16": {"ticks": [0], "envs": [0]},
+    "pi0_stream_bf16": {"ticks": [0, 1, 2, 3, 250, 499], "envs": [0]},
+    "pi0_batch32_bf16": {"ticks": [0, 1, 2, 199], "envs": [0, 31]},
+    "pi0_long_bf16": {"ticks": [7], "envs": [0, 7]},
+}
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for rel in ("oracle/reflex_oracle.py", "paper_2607_14695_amd/workloads.py"):
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def window_ticks(tick: int, window: int):
+    return list(range(max(0, tick + 1 - window), tick + 1))
+
+
+def compute_case(name: str) -> str:
+    cfg = WL.CONFIGS[name]
+    spec = CASES[name]
+    t0 = time.time()
+    w = {k: v.astype(np.float64) for k, v in WL.make_weights(cfg).items()}
+    sk, sv = WL.make_static_kv(cfg)
+    print(f"[{name}] inputs ready in {time.time() - t0:.1f} s", flush=True)
+    out = {}
+    for tick in spec["ticks"]:
+        frames = {}
+        for f in window_ticks(tick, cfg.window_frames):
+            frames[f] = {e: WL.make_frame_env(cfg, f, e) for e in spec["envs"]}
+        state = {e: WL.make_state(cfg, tick, [e])[0] for e in spec["envs"]}
+        noise = {e: WL.make_noise(cfg, tick, [e])[0] for e in spec["envs"]}
+        diag = {}
+        t1 = time.time()
+        xs = O.denoise_chunk(cfg, w, sk, sv, frames, tick + 1, state, noise, cfg.taus(),
+                             envs=spec["envs"], diag=diag)
+        for i, e in enumerate(spec["envs"]):
+            out[f"x_t{tick}_e{e}"] = xs[i]
+            out[f"v_t{tick}_e{e}"] = np.stack(diag["v"][i])
+        print(f"[{name}] tick {tick}: {time.time() - t1:.1f} s", flush=True)
+    path = os.path.join(HERE, f"expected_{name}.npz")
+    np.savez_compressed(path, digest=np.array(source_digest()), ticks=np.array(spec["ticks"]),
+                        envs=np.array(spec["envs"]), **out)
+    return path
+
+
+if __name__ == "__main__":
+    names = sys.argv[1:] or list(CASES)
+    for n in names:
+        print(compute_case(n), flush=True)
