@@ -54,24 +54,25 @@ def _device_inputs(cfg, torch, seed=0):
 def _class_bytes_flops(cfg):
     """Algorithmic HBM bytes and flops of ONE launch of each kernel class.
 
-    GEMMs: weight bytes + activation bytes in + one output copy (fp32 for the
-    split-K residual/QKV outputs, operand type for gate/up).  Attention: the
-    visible cached K and V rows + q/k/v in (fp32) + o out."""
-    T = cfg.action_horizon + 1
-    M = cfg.batch * T
+    GEMMs: weight bytes + activation bytes in + one copy of the output (fp32
+    for the split-K residual projections, the operand type otherwise).
+    Attention: the visible cached K and V rows + q and the dynamic k, v in +
+    o out, all in the operand type."""
+    B, T = cfg.batch, cfg.action_horizon + 1
+    M = B * T
     D, Fm, Hq, dh = cfg.width, cfg.mlp_dim, cfg.n_q_heads, cfg.head_dim
     eb = 2 if cfg.bf16 else 4
     nqkv = (Hq + 2) * dh
     Lc = cfg.static_len + cfg.window_frames * cfg.frame_tokens
     out = {
-        "gemm_qkv": (nqkv * D * eb + M * D * eb + M * nqkv * 4, 2.0 * M * nqkv * D),
+        "gemm_qkv": (nqkv * D * eb + M * D * eb + M * nqkv * eb, 2.0 * M * nqkv * D),
         "gemm_o": (D * Hq * dh * eb + M * Hq * dh * eb + M * D * 4, 2.0 * M * D * Hq * dh),
         "gemm_gate_up": (2 * Fm * D * eb + M * D * eb + M * Fm * eb, 2.0 * M * 2 * Fm * D),
         "gemm_down": (D * Fm * eb + M * Fm * eb + M * D * 4, 2.0 * M * D * Fm),
     }
-    vis = Lc * T + (1 + (T - 1) * T)  # visible keys summed over dynamic rows
-    out["attention"] = (cfg.batch * (2 * Lc * dh * eb + M * nqkv * 4 + M * Hq * dh * eb),
-                        cfg.batch * 4.0 * Hq * dh * vis)
+    vis = Lc * T + (1 + (T - 1) * T)  # visible keys summed over the dynamic rows of one env
+    out["attention"] = (B * (2 * Lc * dh * eb + T * Hq * dh * eb + 2 * T * dh * eb + T * Hq * dh * eb),
+                        B * 4.0 * Hq * dh * vis)
     return out
 
 

@@ -83,9 +83,12 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
   // ---- query fragments (RoPE applied by the projection epilogue) -----------
   uint4 qf[NKS];
   {
-    const T* qrow = reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + rq) * DH + g * KPF;
+    const T* qrow =
+        reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + (qvalid ? rq : 0)) * DH + g * KPF;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[ks] = qvalid ? ld16(qrow + ks * KSD) : zero16();
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = ld16(qrow + ks * KSD);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = qvalid ? qf[ks] : zero16();
   }
 
   // ---- key range of this split ---------------------------------------------
@@ -103,30 +106,38 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
   const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
   const float scale = rsqrtf((float)DH) * 1.4426950408889634f;  // 1/sqrt(d) * log2(e)
 
-  // global -> register staging of one tile (zero rows / columns past the end)
+  // global -> register staging of one tile.  Loads are unconditional from
+  // clamped (in-range) addresses and the out-of-range chunks are zeroed when
+  // they are written to LDS: a conditional load would make the compiler wait
+  // for every outstanding load at the branch join and serialise the prefetch.
   uint4 rk[NKL], rv[NVL];
+  uint32_t kmask = 0, vmask = 0;
   auto gload = [&](int t) {
     const bool dyn = t >= n_ct;
     const int base = dyn ? (t - n_ct) * AKT : t * AKT;
     const int lim = dyn ? T_ : Lc;
     const T* ksrc = dyn ? kdb : ck;
+    kmask = 0;
+    vmask = 0;
 #pragma unroll
     for (int i = 0; i < NKL; ++i) {
       const int c = tid + 256 * i;
       const int kr = c / KCH, cc = c % KCH;
       const int r = base + kr;
-      rk[i] = r < lim ? ld16(reinterpret_cast<const unsigned char*>(ksrc + (int64_t)r * DH) + cc * 16) : zero16();
+      const bool ok = r < lim;
+      kmask |= ok ? (1u << i) : 0u;
+      rk[i] = ld16(reinterpret_cast<const unsigned char*>(ksrc + (int64_t)(ok ? r : 0) * DH) + cc * 16);
     }
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int c = tid + 256 * i;
       const int d = c / VCH, cc = c % VCH;
       const int key = base + cc * (16 / ES);
-      if (dyn) {  // padded to tpad columns, zero beyond T
-        rv[i] = ld16(reinterpret_cast<const unsigned char*>(vdb + (int64_t)d * p.tpad + key));
-      } else {
-        rv[i] = key < lim ? ld16(reinterpret_cast<const unsigned char*>(cvt + (int64_t)d * p.R + key)) : zero16();
-      }
+      // dynamic values are padded to tpad columns and zero beyond T
+      const bool ok = dyn || key < lim;
+      vmask |= ok ? (1u << i) : 0u;
+      const T* vsrc = dyn ? vdb + (int64_t)d * p.tpad : cvt + (int64_t)d * p.R;
+      rv[i] = ld16(reinterpret_cast<const unsigned char*>(vsrc + (ok ? key : 0)));
     }
   };
 
@@ -142,12 +153,12 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
 #pragma unroll
     for (int i = 0; i < NKL; ++i) {
       const int c = tid + 256 * i;
-      st16(&Ks[(c / KCH) * KROW + (c % KCH) * 16], rk[i]);
+      st16(&Ks[(c / KCH) * KROW + (c % KCH) * 16], (kmask >> i) & 1u ? rk[i] : zero16());
     }
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int c = tid + 256 * i;
-      st16(&Vts[(c / VCH) * VROW + (c % VCH) * 16], rv[i]);
+      st16(&Vts[(c / VCH) * VROW + (c % VCH) * 16], (vmask >> i) & 1u ? rv[i] : zero16());
     }
     __syncthreads();
     if (t + 1 < t_end) gload(t + 1);  // in flight during this tile's math

@@ -140,21 +140,28 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
   constexpr int U = 4;
   for (int s0 = wave; s0 < nsteps; s0 += 4 * U) {
     uint4 bf[U][NBT], af[U][MB];
+    // unconditional loads (clamped to k = kbeg when past the end), masked to
+    // zero afterwards: no branch joins that would serialise the loads
+    bool okv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int k = kbeg + (s0 + 4 * u) * KS;
-      const bool ok = (s0 + 4 * u < nsteps) && (k + g * KPF < kend);
+      okv[u] = (s0 + 4 * u < nsteps) && (k + g * KPF < kend);
+      const int kc = okv[u] ? k : kbeg;
 #pragma unroll
-      for (int nb = 0; nb < NBT; ++nb) bf[u][nb] = ok ? ld16(brow[nb] + k) : zero16();
+      for (int nb = 0; nb < NBT; ++nb) bf[u][nb] = ld16(brow[nb] + kc);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) af[u][mb] = ok ? ld16(arow[mb] + k) : zero16();
+      for (int mb = 0; mb < MB; ++mb) af[u][mb] = ld16(arow[mb] + kc);
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int nb = 0; nb < NBT; ++nb) bf[u][nb] = okv[u] ? bf[u][nb] : zero16();
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < NBT; ++nb) mfma_step(acc[mb][nb], af[u][mb], bf[u][nb], T());
+    }
   }
 
 #pragma unroll
@@ -235,21 +242,23 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
     gb[i] = B + (int64_t)brw * p.ldb + ch * KPF;
   }
   uint4 ra[4], rb[4];
+  bool gok = false;
   auto gload = [&](int st) {
     const int k0 = kbeg + st * KSTAGE;
-    const bool ok = k0 + ch * KPF < kend;
+    gok = k0 + ch * KPF < kend;
+    const int kc = gok ? k0 : kbeg - ch * KPF;  // clamped: a valid address
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      ra[i] = ok ? ld16(ga[i] + k0) : zero16();
-      rb[i] = ok ? ld16(gb[i] + k0) : zero16();
+      ra[i] = ld16(ga[i] + kc);
+      rb[i] = ld16(gb[i] + kc);
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = (tid >> 3) + 32 * i;
-      st16(&As[buf][r * LROW + ch * 16], ra[i]);
-      st16(&Bs[buf][r * LROW + ch * 16], rb[i]);
+      st16(&As[buf][r * LROW + ch * 16], gok ? ra[i] : zero16());
+      st16(&Bs[buf][r * LROW + ch * 16], gok ? rb[i] : zero16());
     }
   };
 
