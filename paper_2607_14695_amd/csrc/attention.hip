@@ -58,7 +58,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
   constexpr int NKB = AKT / 16;       // 16-key blocks per tile
   constexpr int NDB = DH / 16;        // 16-wide d blocks of the output
   constexpr int KROW = DH * ES + 16;  // LDS bytes per K row
-  constexpr int VROW = AKT * ES + 16; // LDS bytes per V^T row
+  constexpr int VROW = AKT * ES + 8;  // LDS bytes per V^T row (8-byte pad: the 16 rows a
+                                      // lane group reads start on distinct banks)
   constexpr int KCH = DH * ES / 16;   // 16-byte chunks per K row
   constexpr int VCH = AKT * ES / 16;  // 16-byte chunks per V^T row (one tile)
   constexpr int NKL = AKT * KCH / 256;  // K chunks per thread
@@ -158,7 +159,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int c = tid + 256 * i;
-      st16(&Vts[(c / VCH) * VROW + (c % VCH) * 16], (vmask >> i) & 1u ? rv[i] : zero16());
+      const uint4 v = (vmask >> i) & 1u ? rv[i] : zero16();
+      unsigned char* dst = &Vts[(c / VCH) * VROW + (c % VCH) * 16];  // 8-byte aligned rows
+      *reinterpret_cast<uint2*>(dst) = make_uint2(v.x, v.y);
+      *reinterpret_cast<uint2*>(dst + 8) = make_uint2(v.z, v.w);
     }
     __syncthreads();
     if (t + 1 < t_end) gload(t + 1);  // in flight during this tile's math
@@ -236,9 +240,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
         const uint4 pf = f_to_frag(pv, T());
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const uint4 a =
-              *reinterpret_cast<const uint4*>(&Vts[(db * 16 + r16) * VROW + (kb * 16 + 4 * g) * ES]);
-          mfma_step(o[db], a, pf, T());
+          const unsigned char* vr = &Vts[(db * 16 + r16) * VROW + (kb * 16 + 4 * g) * ES];
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
+          mfma_step(o[db], make_uint4(lo.x, lo.y, hi.x, hi.y), pf, T());
         }
       }
     }
@@ -264,49 +269,44 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
 
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
 // splits combined in index order.  One thread per (query row, d).
-constexpr int kMaxSplits = 32;
+constexpr int kMaxSplits = 16;
 
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   constexpr int RPB = 256 / DH;  // rows per block
-  __shared__ float wts[RPB][kMaxSplits];
-  __shared__ float inv_l[RPB];
   const int b = blockIdx.y;
   const int rsub = threadIdx.x / DH, d = threadIdx.x % DH;
   const int rq = blockIdx.x * RPB + rsub;
   const int nrows = p.T * p.Hq;
-  const int64_t base = (int64_t)b * p.nsplit * p.rows_pad;
-  if (d == 0 && rq < nrows) {
-    float m[kMaxSplits], M = -INFINITY;
-#pragma unroll
-    for (int s = 0; s < kMaxSplits; ++s) {
-      m[s] = -INFINITY;
-      if (s < p.nsplit) {
-        const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + (base + (int64_t)s * p.rows_pad + rq) * 2);
-        m[s] = ml.x;
-        wts[rsub][s] = ml.y;
-        M = fmaxf(M, ml.x);
-      }
-    }
-    const float Mu = (M == -INFINITY) ? 0.f : M;
-    float L = 0.f;
-#pragma unroll
-    for (int s = 0; s < kMaxSplits; ++s)
-      if (s < p.nsplit) {
-        const float w = exp2f(m[s] - Mu);
-        L += w * wts[rsub][s];
-        wts[rsub][s] = w;
-      }
-    inv_l[rsub] = L > 0.f ? 1.f / L : 0.f;
-  }
-  __syncthreads();
   if (rq >= nrows) return;
-  float acc = 0.f;
-#pragma unroll 8
-  for (int s = 0; s < p.nsplit; ++s) acc += wts[rsub][s] * p.part_o[(base + (int64_t)s * p.rows_pad + rq) * DH + d];
+  const int64_t base = (int64_t)b * p.nsplit * p.rows_pad + rq;
+  // all loads of this thread are independent: one memory round trip
+  float2 ml[kMaxSplits];
+  float ov[kMaxSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) {
+    if (s < p.nsplit) {
+      const int64_t prow = base + (int64_t)s * p.rows_pad;
+      ml[s] = *reinterpret_cast<const float2*>(p.part_ml + prow * 2);
+      ov[s] = p.part_o[prow * DH + d];
+    }
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s)
+    if (s < p.nsplit) M = fmaxf(M, ml[s].x);
+  const float Mu = (M == -INFINITY) ? 0.f : M;
+  float L = 0.f, acc = 0.f;
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s)
+    if (s < p.nsplit) {
+      const float w = exp2f(ml[s].x - Mu);
+      L += w * ml[s].y;
+      acc += w * ov[s];
+    }
   const int i = rq / p.Hq, j = rq % p.Hq;
   T* dst = reinterpret_cast<T*>(p.out) + ((int64_t)b * p.T + i) * (int64_t)(p.Hq * DH) + j * DH + d;
-  *dst = from_f<T>(acc * inv_l[rsub]);
+  *dst = from_f<T>(L > 0.f ? acc / L : 0.f);
 }
 
 int attention_pick_splits(int B, int rows, int max_keys, int head_dim) {

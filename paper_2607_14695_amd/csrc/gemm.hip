@@ -81,15 +81,15 @@ RFX_DEV void epilogue_store(const GemmArgs& p, int z, int split, int row, int co
 // --------------------------------------------------------------------------
 // skinny: 16*MB rows per workgroup chunk, NB 16-col blocks per strip
 // --------------------------------------------------------------------------
-template <typename T, int MB, int NB, int EPI>
-__global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
+template <typename T, int MB, int NB, int EPI, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_skinny(GemmArgs p) {
   constexpr int PAIR = EpiPair<EPI>::value;
   constexpr int KPF = ElemT<T>::kPerFrag;
   constexpr int KS = 4 * KPF;                      // elements per k-step
   constexpr int NBT = PAIR ? 2 * NB : NB;          // B fragments per k-step
   constexpr int COLS = 16 * NB;                    // first columns per workgroup
   constexpr int RCOLS = 16 * NBT + 1;              // LDS reduction row (padded)
-  __shared__ float red[4][MB * 16][RCOLS];
+  __shared__ float red[NW][MB * 16][RCOLS];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -138,15 +138,15 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
 
   const int nsteps = (kend - kbeg + KS - 1) / KS;
   constexpr int U = 4;
-  for (int s0 = wave; s0 < nsteps; s0 += 4 * U) {
+  for (int s0 = wave; s0 < nsteps; s0 += NW * U) {
     uint4 bf[U][NBT], af[U][MB];
     // unconditional loads (clamped to k = kbeg when past the end), masked to
     // zero afterwards: no branch joins that would serialise the loads
     bool okv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = kbeg + (s0 + 4 * u) * KS;
-      okv[u] = (s0 + 4 * u < nsteps) && (k + g * KPF < kend);
+      const int k = kbeg + (s0 + NW * u) * KS;
+      okv[u] = (s0 + NW * u < nsteps) && (k + g * KPF < kend);
       const int kc = okv[u] ? k : kbeg;
 #pragma unroll
       for (int nb = 0; nb < NBT; ++nb) bf[u][nb] = ld16(brow[nb] + kc);
@@ -172,15 +172,17 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs p) {
       for (int i = 0; i < 4; ++i) red[wave][mb * 16 + 4 * g + i][nb * 16 + r16] = acc[mb][nb][i];
   __syncthreads();
 
-  for (int e = threadIdx.x; e < MB * 16 * COLS; e += 256) {
+  for (int e = threadIdx.x; e < MB * 16 * COLS; e += 64 * NW) {
     const int row = e / COLS, col = e % COLS;
     const int grow = m0 + row;
-    const int gcol = PAIR == PAIR_NONE ? n0 + col : n0 + col;
+    const int gcol = n0 + col;
     if (grow >= p.M || (PAIR == PAIR_NONE && gcol >= p.N)) continue;
-    const float v = red[0][row][col] + red[1][row][col] + red[2][row][col] + red[3][row][col];
-    float u = 0.f;
-    if (PAIR) u = red[0][row][col + COLS] + red[1][row][col + COLS] + red[2][row][col + COLS] +
-                  red[3][row][col + COLS];
+    float v = 0.f, u = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      v += red[w][row][col];
+      if (PAIR) u += red[w][row][col + COLS];
+    }
     epilogue_store<EPI, T>(p, z, split, grow, gcol, v, u);
   }
 }
@@ -362,7 +364,13 @@ static void launch_skinny_cfg(const GemmArgs& a, hipStream_t s) {
     nx = (a.N + 16 * NB - 1) / (16 * NB);
   const int mch = (a.M + 16 * MB - 1) / (16 * MB);
   dim3 grid(nx, mch * a.splits, a.batch);
-  RFX_LAUNCH((gemm_skinny<T, MB, NB, EPI>), grid, dim3(256), 0, s, a);
+  // eight waves when a workgroup's K range has at least 32 k-steps: every
+  // wave then issues all its loads in one round trip
+  const int ks = 64 / (int)sizeof(T);
+  if (a.k_per_split >= 32 * ks && a.K >= 32 * ks)
+    RFX_LAUNCH((gemm_skinny<T, MB, NB, EPI, 8>), grid, dim3(512), 0, s, a);
+  else
+    RFX_LAUNCH((gemm_skinny<T, MB, NB, EPI, 4>), grid, dim3(256), 0, s, a);
 }
 
 template <typename T, int EPI>
