@@ -267,6 +267,253 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
   if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
 }
 
+
+// ---------------------------------------------------------------------------
+// bf16 variant with 32x32x16 MFMAs and direct global->LDS tile loads.
+//
+// Each wave owns 32 query rows, a workgroup of 4 waves 128 rows, so every K/V
+// tile in LDS feeds 128 rows and each 16-byte LDS fragment feeds a 32x32 MFMA.
+// Tiles are written by global_load_lds_dwordx4 (CDNA4): no staging registers,
+// which leaves the register room the compiler needs to issue LDS fragment
+// reads ahead of the MFMAs.  Two LDS stages: tile t+1 streams in while tile t
+// is consumed.  The LDS layout is unpadded and XOR-swizzled on 16-byte
+// chunks (K: chunk ^ (row mod chunks-per-row); V^T: chunk ^ ((d >> 1) mod 8)),
+// so the rows a lane group reads fall on distinct banks.  The DMA writes 1 KB
+// per wave instruction at consecutive LDS addresses, so the swizzle is
+// applied on the global side: each lane fetches the logical chunk that belongs
+// at its physical position.  Rows past the valid range are fetched from a
+// clamped valid address (finite data): their scores are masked to -inf and
+// their values meet zero probabilities, so they never contribute.
+//
+// S^T lane layout: key 8*(q >> 2) + 4*h + (q & 3) of a 32-key block, query
+// (lane & 31), h = lane >> 5; O^T holds d 8*(q >> 2) + 4*h + (q & 3) of a
+// 32-wide block for the same query.
+// ---------------------------------------------------------------------------
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// releases global memory, which makes the compiler wait for every outstanding
+// vector-memory operation, including the LDS DMA of the next tile that is
+// meant to stay in flight; DMA completion is awaited explicitly instead.
+RFX_DEV void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <int DH>
+__global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
+  using T = bf16_t;
+  constexpr int NKS = DH / 16;         // 16-wide d steps of S^T
+  constexpr int NDB = DH / 32;         // 32-wide d blocks of O^T
+  constexpr int KRB = DH * 2;          // bytes per K row in LDS
+  constexpr int KCH = DH / 8;          // 16-byte chunks per K row
+  constexpr int VRB = AKT * 2;         // bytes per V^T row (128)
+  constexpr int KBYTES = AKT * KRB;    // K tile bytes
+  constexpr int VBYTES = DH * VRB;     // V^T tile bytes
+  constexpr int STAGE = KBYTES + VBYTES;
+  constexpr int NIK = KBYTES / 1024 / 4;  // 1-KB DMA instructions per wave, K
+  constexpr int NIV = VBYTES / 1024 / 4;  // same for V^T
+  // two stages as distinct LDS objects: the compiler can then tell the DMA
+  // into one stage from the reads of the other and keep the DMA in flight
+  __shared__ __attribute__((aligned(16))) unsigned char stage0[STAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char stage1[STAGE];
+
+  int group, rb;
+  if (!attn_decode(blockIdx.x, p.B * p.nsplit, p.rows_pad / 128, group, rb)) return;
+  const int b = group / p.nsplit, split = group - b * p.nsplit;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r32 = lane & 31, h = lane >> 5;
+  const int T_ = p.T, Hq = p.Hq;
+  const int nrows = T_ * Hq;
+  const int rq = rb * 128 + wave * 32 + r32;
+  const bool qvalid = rq < nrows;
+  const int iq = qvalid ? rq / Hq : 0;
+  const int jq = qvalid ? rq % Hq : 0;
+  const int64_t mrow0 = (int64_t)b * T_;
+
+  uint4 qf[NKS];
+  {
+    const T* qrow = reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + (qvalid ? rq : 0)) * DH + h * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = ld16(qrow + ks * 16);
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = qvalid ? qf[ks] : zero16();
+  }
+
+  const int Lc = p.static_len + (*p.n_valid) * p.frame_tokens;
+  const int n_ct = (Lc + AKT - 1) / AKT;
+  const int n_dt = (T_ + AKT - 1) / AKT;
+  const int total = n_ct + n_dt;
+  const int per = (total + p.nsplit - 1) / p.nsplit;
+  const int t_beg = split * per;
+  const int t_end = min(total, t_beg + per);
+
+  const T* ck = reinterpret_cast<const T*>(p.cache_k) + (int64_t)b * p.ck_bstride;
+  const T* cvt = reinterpret_cast<const T*>(p.cache_vt) + (int64_t)b * p.ck_bstride;
+  const T* kdb = reinterpret_cast<const T*>(p.kd) + (int64_t)b * T_ * DH;
+  const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
+  const float scale = rsqrtf((float)DH) * 1.4426950408889634f;
+
+  // issue the DMA of tile t into stage st (NIK + NIV instructions per wave)
+  auto issue = [&](int t, unsigned char* sk) {
+    const bool dyn = t >= n_ct;
+    const int base = dyn ? (t - n_ct) * AKT : t * AKT;
+    const int lim = dyn ? T_ : Lc;
+    const T* ksrc = dyn ? kdb : ck;
+    unsigned char* sv = sk + KBYTES;
+#pragma unroll
+    for (int j = 0; j < NIK; ++j) {
+      const int q = (wave * NIK + j) * 64 + lane;  // physical 16-byte chunk
+      const int row = q / KCH, pc = q % KCH;
+      const int lc = pc ^ (row & (KCH - 1));
+      const int r = base + row;
+      const T* src = ksrc + (int64_t)(r < lim ? r : 0) * DH + lc * 8;
+      __builtin_amdgcn_global_load_lds(src, sk + (wave * NIK + j) * 1024, 16, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < NIV; ++j) {
+      const int q = (wave * NIV + j) * 64 + lane;
+      const int d = q >> 3, pc = q & 7;
+      const int lc = pc ^ ((d >> 1) & 7);
+      const int key = base + lc * 8;
+      const T* src = dyn ? vdb + (int64_t)d * p.tpad + key
+                         : cvt + (int64_t)d * p.R + (key < lim ? key : 0);
+      __builtin_amdgcn_global_load_lds(src, sv + (wave * NIV + j) * 1024, 16, 0, 0);
+    }
+  };
+
+  f32x16_v o[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int q = 0; q < 16; ++q) o[db][q] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  auto step = [&](int t, const unsigned char* cur, unsigned char* nxt) {
+      const bool dyn = t >= n_ct;
+      // tile t's DMA (the only one outstanding) completes, then every wave's
+      // part is visible after the barrier; tile t+1 streams in during the math
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+      lds_barrier();
+      if (t + 1 < t_end) issue(t + 1, nxt);
+      const unsigned char* sk = cur;
+      const unsigned char* sv = sk + KBYTES;
+
+      // S^T = K Q^T, two 32-key blocks
+      f32x16_v s[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) s[kb][q] = 0.f;
+      // fragments are read in batches ahead of their MFMAs so the LDS latency
+      // overlaps the matrix work
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int row = kb * 32 + r32;
+        const unsigned char* krow = sk + row * KRB;
+#pragma unroll
+        for (int k0 = 0; k0 < NKS; k0 += 8) {
+          uint4 a[8];
+#pragma unroll
+          for (int u = 0; u < 8 && k0 + u < NKS; ++u)
+            a[u] = *reinterpret_cast<const uint4*>(krow + ((2 * (k0 + u) + h) ^ (row & (KCH - 1))) * 16);
+#pragma unroll
+          for (int u = 0; u < 8 && k0 + u < NKS; ++u) mfma32_step(s[kb], a[u], qf[k0 + u]);
+        }
+      }
+      float mt = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int kidx = kb * 32 + 8 * (q >> 2) + 4 * h + (q & 3);
+          bool ok;
+          if (!dyn) {
+            ok = t * AKT + kidx < Lc;
+          } else {
+            const int kd = (t - n_ct) * AKT + kidx;
+            ok = kd < T_ && (iq > 0 || kd == 0);
+          }
+          const float v = ok ? s[kb][q] * scale : -INFINITY;
+          s[kb][q] = v;
+          mt = fmaxf(mt, v);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float m_new = fmaxf(m_run, mt);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float corr = exp2f(m_run - m_use);
+      float psum = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const float e = exp2f(s[kb][q] - m_use);
+          s[kb][q] = e;
+          psum += e;
+        }
+      psum += __shfl_xor(psum, 32, 64);
+      l_run = l_run * corr + psum;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] *= corr;
+
+      // O^T += V^T P^T in 16-key steps: step ps uses keys {16ps + 4h + [0,4)} and
+      // {16ps + 8 + 4h + [0,4)} of lane group h, i.e. s[ps >> 1][8*(ps & 1) + [0,8)]
+#pragma unroll
+      for (int ps = 0; ps < 4; ++ps) {
+        float pv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pv[i] = s[ps >> 1][8 * (ps & 1) + i];
+        const uint4 pf = f_to_frag(pv, T());
+        uint4 vf[NDB];
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const int d = db * 32 + r32;
+          const int sw = (d >> 1) & 7;
+          const unsigned char* vr = sv + d * VRB + h * 8;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr + ((2 * ps) ^ sw) * 16);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + ((2 * ps + 1) ^ sw) * 16);
+          vf[db] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) mfma32_step(o[db], vf[db], pf);
+      }
+      lds_barrier();  // this stage is refilled two tiles later
+  };
+
+  if (t_beg < t_end) issue(t_beg, stage0);
+  for (int t = t_beg; t < t_end; t += 2) {
+    step(t, stage0, stage1);
+    if (t + 1 < t_end) step(t + 1, stage1, stage0);
+  }
+
+  if (!qvalid) return;
+  if (p.nsplit == 1) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    T* dst = reinterpret_cast<T*>(p.out) + (mrow0 + iq) * (int64_t)(Hq * DH) + jq * DH;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int d = db * 32 + 8 * j + 4 * h;
+        uint2 w;
+        w.x = (uint32_t)f2bf(o[db][4 * j] * inv) | ((uint32_t)f2bf(o[db][4 * j + 1] * inv) << 16);
+        w.y = (uint32_t)f2bf(o[db][4 * j + 2] * inv) | ((uint32_t)f2bf(o[db][4 * j + 3] * inv) << 16);
+        *reinterpret_cast<uint2*>(dst + d) = w;
+      }
+    return;
+  }
+  const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq;
+  float* dst = p.part_o + prow * DH;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<float4*>(dst + db * 32 + 8 * j + 4 * h) =
+          make_float4(o[db][4 * j], o[db][4 * j + 1], o[db][4 * j + 2], o[db][4 * j + 3]);
+  if (h == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
+}
+
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
 // splits combined in index order.  One thread per (query row, d).
 constexpr int kMaxSplits = 16;
@@ -309,9 +556,12 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   *dst = from_f<T>(L > 0.f ? acc / L : 0.f);
 }
 
-int attention_pick_splits(int B, int rows, int max_keys, int head_dim) {
-  (void)head_dim;
-  const int rbs = (rows + 63) / 64;
+// Query rows per attention workgroup: 128 on the bf16 (32x32 MFMA) path, 64 on fp32.
+int attention_rows_per_block(int elem_bytes) { return elem_bytes == 2 ? 128 : 64; }
+
+int attention_pick_splits(int B, int rows, int max_keys, int elem_bytes) {
+  const int rpb = attention_rows_per_block(elem_bytes);
+  const int rbs = (rows + rpb - 1) / rpb;
   const int base = B * rbs;
   const int tiles = (max_keys + AKT - 1) / AKT + 1;
   // one workgroup per CU is resident (register bound): aim for ~1 wave of
@@ -325,9 +575,14 @@ int attention_pick_splits(int B, int rows, int max_keys, int head_dim) {
 
 template <typename T, int DH>
 static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
-  const int groups = a.B * a.nsplit, nrb = a.rows_pad / 64;
-  const int nwg = ((groups + 7) / 8) * 8 * nrb;
-  RFX_LAUNCH((attn_kernel<T, DH>), dim3(nwg), dim3(256), 0, s, a);
+  const int groups = a.B * a.nsplit;
+  if constexpr (sizeof(T) == 2) {
+    const int nwg = ((groups + 7) / 8) * 8 * (a.rows_pad / 128);
+    RFX_LAUNCH((attn32_kernel<DH>), dim3(nwg), dim3(256), 0, s, a);
+  } else {
+    const int nwg = ((groups + 7) / 8) * 8 * (a.rows_pad / 64);
+    RFX_LAUNCH((attn_kernel<T, DH>), dim3(nwg), dim3(256), 0, s, a);
+  }
 }
 
 template <typename T, int DH>
@@ -339,7 +594,7 @@ static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
 
 template <typename T>
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
-  if (a.nsplit < 1 || a.nsplit > kMaxSplits || a.rows_pad % 64) return hipErrorInvalidValue;
+  if (a.nsplit < 1 || a.nsplit > kMaxSplits || a.rows_pad % 128) return hipErrorInvalidValue;
   switch (head_dim) {
     case 64: launch_attn_dh<T, 64>(a, s); break;
     case 128: launch_attn_dh<T, 128>(a, s); break;

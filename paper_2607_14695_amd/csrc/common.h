@@ -19,6 +19,7 @@ namespace reflex {
 typedef uint16_t bf16_t;  // bfloat16 bit pattern
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_v;
 typedef __attribute__((ext_vector_type(4))) float f32x4_v;
+typedef __attribute__((ext_vector_type(16))) float f32x16_v;
 
 #define RFX_DEV __device__ __forceinline__
 
@@ -57,6 +58,14 @@ RFX_DEV void mfma_step(f32x4_v& acc, const uint4& a, const uint4& b, float) {
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+}
+
+// One 32x32x16 bf16 MFMA: lane l supplies row / column (l & 31) and the 8
+// contraction elements 8*(l >> 5) + [0, 8); the 32x32 fp32 result sits in lane
+// l as rows 8*(q >> 2) + 4*(l >> 5) + (q & 3), q < 16, column (l & 31).
+RFX_DEV void mfma32_step(f32x16_v& acc, const uint4& a, const uint4& b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_v, a), __builtin_bit_cast(bf16x8_v, b), acc,
+                                                0, 0, 0);
 }
 
 RFX_DEV uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }

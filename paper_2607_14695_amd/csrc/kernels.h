@@ -80,7 +80,8 @@ struct AttnArgs {
 };
 template <typename T> hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
 template <typename T> hipError_t launch_attn_merge(const AttnArgs& a, int head_dim, hipStream_t s);
-int attention_pick_splits(int B, int rows, int max_keys, int head_dim);
+int attention_pick_splits(int B, int rows, int max_keys, int elem_bytes);
+int attention_rows_per_block(int elem_bytes);
 
 // Token embedding + first AdaRMSNorm: h = embed_scale*[s W_s^T ; x W_ain^T], y = ada(h).
 struct EmbedArgs {

@@ -133,13 +133,13 @@ Plan make_plan(const reflex_config* c) {
   p.C = c->width + c->state_dim;
   p.R = c->static_len + c->window_frames * c->frame_tokens;
   const int rows = p.T * c->n_q_heads;
-  p.rows_pad = (rows + 63) / 64 * 64;
+  p.rows_pad = (rows + 127) / 128 * 128;
   p.nrb = p.rows_pad / 64;
   p.tpad = (p.T + 63) / 64 * 64;
   p.o = make_split(p.M, c->n_q_heads * c->head_dim,
                    gemm_pick_splits(p.M, c->width, c->n_q_heads * c->head_dim, eb), eb);
   p.down = make_split(p.M, c->mlp_dim, gemm_pick_splits(p.M, c->width, c->mlp_dim, eb), eb);
-  p.attn_splits = attention_pick_splits(c->batch, rows, p.R, c->head_dim);
+  p.attn_splits = attention_pick_splits(c->batch, rows, p.R, eb);
   p.max_parts = p.o.splits > p.down.splits ? p.o.splits : p.down.splits;
 
   const size_t B = c->batch, L = c->n_layers, dh = c->head_dim, D = c->width, K = c->max_steps;
