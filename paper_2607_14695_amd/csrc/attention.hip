@@ -277,7 +277,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
 // which leaves the register room the compiler needs to issue LDS fragment
 // reads ahead of the MFMAs.  Two LDS stages: tile t+1 streams in while tile t
 // is consumed.  The LDS layout is unpadded and XOR-swizzled on 16-byte
-// chunks (K: chunk ^ (row mod chunks-per-row); V^T: chunk ^ ((d >> 1) mod 8)),
+// chunks (K: chunk ^ (row mod 8); V^T: chunk ^ ((d >> 1) mod 8)),
 // so the rows a lane group reads fall on distinct banks.  The DMA writes 1 KB
 // per wave instruction at consecutive LDS addresses, so the swizzle is
 // applied on the global side: each lane fetches the logical chunk that belongs
@@ -321,7 +321,8 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
   if (!attn_decode(blockIdx.x, p.B * p.nsplit, p.rows_pad / 128, group, rb)) return;
   const int b = group / p.nsplit, split = group - b * p.nsplit;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: keep it (and the offsets built on it) scalar
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r32 = lane & 31, h = lane >> 5;
   const int T_ = p.T, Hq = p.Hq;
   const int nrows = T_ * Hq;
@@ -334,10 +335,9 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
   uint4 qf[NKS];
   {
     const T* qrow = reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + (qvalid ? rq : 0)) * DH + h * 8;
+    // rows past the valid range compute on row 0's data and are never stored
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[ks] = ld16(qrow + ks * 16);
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[ks] = qvalid ? qf[ks] : zero16();
   }
 
   const int Lc = p.static_len + (*p.n_valid) * p.frame_tokens;
@@ -354,31 +354,49 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
   const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
   const float scale = rsqrtf((float)DH) * 1.4426950408889634f;
 
-  // issue the DMA of tile t into stage st (NIK + NIV instructions per wave)
-  auto issue = [&](int t, unsigned char* sk) {
+  // issue the DMA of tile t into stage sk (NIK + NIV instructions per wave).
+  // The per-lane offsets are rebuilt from an opaque copy of the lane id on
+  // every call: hoisted out of the tile loop they would pin ~40 registers.
+  const int tpad = p.tpad, Rrow = p.R;  // copied: a lambda must not capture the kernel argument
+  constexpr int RPI = 64 / KCH;  // K rows per DMA instruction
+  auto issue = [&](int t, unsigned char* sk) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
     const bool dyn = t >= n_ct;
     const int base = dyn ? (t - n_ct) * AKT : t * AKT;
-    const int lim = dyn ? T_ : Lc;
-    const T* ksrc = dyn ? kdb : ck;
+    const int last = (dyn ? T_ : Lc) - 1;
     unsigned char* sv = sk + KBYTES;
+    const int kl = ln % KCH, kr = ln / KCH;
+    const int vd = ln >> 3, vc = ln & 7;
+    if (dyn) {
 #pragma unroll
-    for (int j = 0; j < NIK; ++j) {
-      const int q = (wave * NIK + j) * 64 + lane;  // physical 16-byte chunk
-      const int row = q / KCH, pc = q % KCH;
-      const int lc = pc ^ (row & (KCH - 1));
-      const int r = base + row;
-      const T* src = ksrc + (int64_t)(r < lim ? r : 0) * DH + lc * 8;
-      __builtin_amdgcn_global_load_lds(src, sk + (wave * NIK + j) * 1024, 16, 0, 0);
-    }
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        const int r = min(base + row, last);
+        __builtin_amdgcn_global_load_lds(kdb + r * DH + (kl ^ (row & 7)) * 8, sk + (wave * NIK + j) * 1024,
+                                         16, 0, 0);
+      }
 #pragma unroll
-    for (int j = 0; j < NIV; ++j) {
-      const int q = (wave * NIV + j) * 64 + lane;
-      const int d = q >> 3, pc = q & 7;
-      const int lc = pc ^ ((d >> 1) & 7);
-      const int key = base + lc * 8;
-      const T* src = dyn ? vdb + (int64_t)d * p.tpad + key
-                         : cvt + (int64_t)d * p.R + (key < lim ? key : 0);
-      __builtin_amdgcn_global_load_lds(src, sv + (wave * NIV + j) * 1024, 16, 0, 0);
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        __builtin_amdgcn_global_load_lds(vdb + d * tpad + base + (vc ^ ((d >> 1) & 7)) * 8,
+                                         sv + (wave * NIV + j) * 1024, 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        const int r = min(base + row, last);
+        __builtin_amdgcn_global_load_lds(ck + (int64_t)r * DH + (kl ^ (row & 7)) * 8,
+                                         sk + (wave * NIK + j) * 1024, 16, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        const int key = base + (vc ^ ((d >> 1) & 7)) * 8;
+        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + (key <= last ? key : 0),
+                                         sv + (wave * NIV + j) * 1024, 16, 0, 0);
+      }
     }
   };
 
@@ -389,7 +407,10 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
     for (int q = 0; q < 16; ++q) o[db][q] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  auto step = [&](int t, const unsigned char* cur, unsigned char* nxt) {
+  int koff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) koff[j] = ((2 * j) ^ (h ^ (r32 & 7))) * 16;
+  auto step = [&](int t, const unsigned char* cur, unsigned char* nxt) __attribute__((always_inline)) {
       const bool dyn = t >= n_ct;
       // tile t's DMA (the only one outstanding) completes, then every wave's
       // part is visible after the barrier; tile t+1 streams in during the math
@@ -398,6 +419,7 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
       if (t + 1 < t_end) issue(t + 1, nxt);
       const unsigned char* sk = cur;
       const unsigned char* sv = sk + KBYTES;
+      const unsigned char* krd = sk + r32 * KRB;
 
       // S^T = K Q^T, two 32-key blocks
       f32x16_v s[2];
@@ -407,41 +429,48 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
         for (int q = 0; q < 16; ++q) s[kb][q] = 0.f;
       // fragments are read in batches ahead of their MFMAs so the LDS latency
       // overlaps the matrix work
+      // chunk 2ks + h of row kb*32 + r32 sits at 2ks ^ (h ^ (r32 & 7)): the
+      // per-lane part takes 4 values (ks mod 4), the rest is an immediate
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const int row = kb * 32 + r32;
-        const unsigned char* krow = sk + row * KRB;
 #pragma unroll
         for (int k0 = 0; k0 < NKS; k0 += 8) {
           uint4 a[8];
 #pragma unroll
-          for (int u = 0; u < 8 && k0 + u < NKS; ++u)
-            a[u] = *reinterpret_cast<const uint4*>(krow + ((2 * (k0 + u) + h) ^ (row & (KCH - 1))) * 16);
+          for (int u = 0; u < 8 && k0 + u < NKS; ++u) {
+            const int ks = k0 + u;
+            a[u] = *reinterpret_cast<const uint4*>(krd + kb * 32 * KRB + (ks >> 2) * 128 + koff[ks & 3]);
+          }
 #pragma unroll
           for (int u = 0; u < 8 && k0 + u < NKS; ++u) mfma32_step(s[kb], a[u], qf[k0 + u]);
         }
       }
+      // key kidx of the tile is visible iff kidx < lim: the cached rows below
+      // Lc; among the dynamic rows the state row (iq == 0) sees only key 0
+      const int lim = (dyn ? (iq > 0 ? T_ : 1) - (t - n_ct) * AKT : Lc - t * AKT) - 4 * h;
       float mt = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
-          const int kidx = kb * 32 + 8 * (q >> 2) + 4 * h + (q & 3);
-          bool ok;
-          if (!dyn) {
-            ok = t * AKT + kidx < Lc;
-          } else {
-            const int kd = (t - n_ct) * AKT + kidx;
-            ok = kd < T_ && (iq > 0 || kd == 0);
-          }
-          const float v = ok ? s[kb][q] * scale : -INFINITY;
+          const int kc = kb * 32 + 8 * (q >> 2) + (q & 3);  // key index minus 4h
+          const float v = kc < lim ? s[kb][q] * scale : -INFINITY;
           s[kb][q] = v;
           mt = fmaxf(mt, v);
         }
       mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float m_new = fmaxf(m_run, mt);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float corr = exp2f(m_run - m_use);
+      // lazy rescaling: the running max only moves when some row's tile max
+      // exceeds it by more than 8 (log2 units), so the probabilities stay
+      // below 2^8 and the O rescale (accumulator round trip) is rare
+      if (__any(mt > m_run + 8.f)) {
+        const float m_new = fmaxf(m_run, mt);
+        const float corr = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+        l_run *= corr;
+        m_run = m_new;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) o[db] *= corr;
+      }
+      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
       float psum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -452,10 +481,7 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
           psum += e;
         }
       psum += __shfl_xor(psum, 32, 64);
-      l_run = l_run * corr + psum;
-      m_run = m_new;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] *= corr;
+      l_run += psum;
 
       // O^T += V^T P^T in 16-key steps: step ps uses keys {16ps + 4h + [0,4)} and
       // {16ps + 8 + 4h + [0,4)} of lane group h, i.e. s[ps >> 1][8*(ps & 1) + [0,8)]
