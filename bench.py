@@ -93,6 +93,23 @@ def _time_ticks(eng, frames, state, noise, steps, warmup, torch, denoise_only=Fa
     return (time.perf_counter() - t0) / steps
 
 
+def _chunk_latencies(eng, state, noise, n, torch):
+    """Device time of n back-to-back single chunks, each bracketed by events on
+    the engine's stream (ms): mean and percentiles."""
+    import numpy as np
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in evs:
+        a.record(eng.stream)
+        eng.denoise(state, noise)
+        b.record(eng.stream)
+    eng.synchronize()
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in evs])
+    return {"mean": round(float(ms.mean()), 4), "p50": round(float(np.percentile(ms, 50)), 4),
+            "p95": round(float(np.percentile(ms, 95)), 4), "p99": round(float(np.percentile(ms, 99)), 4), "n": n}
+
+
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
     10 Euler steps, one frame in the window), median of two runs."""
@@ -137,6 +154,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-b32", action="store_true")
+    ap.add_argument("--no-latency", action="store_true",
+                    help="skip the per-chunk event-timed latency distribution (for counter-collection runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -172,6 +191,10 @@ def main():
     log(f"tick {tick_s * 1e3:.3f} ms")
     chunk_s = _time_ticks(eng, frames, state, noise, args.steps, args.warmup, torch, denoise_only=True)
     log(f"chunk {chunk_s * 1e3:.3f} ms")
+    lat = None
+    if not args.no_latency:
+        lat = _chunk_latencies(eng, state, noise, max(20, args.steps), torch)
+        log(f"chunk latency p50 {lat['p50']:.3f} ms, p99 {lat['p99']:.3f} ms")
     prof = eng.profile(state, noise)
     log("profile: " + ", ".join(f"{k}={v[0]:.3f}ms/{v[1]}" for k, v in prof.items() if v[1]))
     bf = _class_bytes_flops(cfg)
@@ -179,6 +202,9 @@ def main():
     ms, n = prof[dominant]
     avg_s = ms / n / 1e3
     achieved = bf[dominant][0] / avg_s / 1e9
+    from paper_2607_14695_amd.profiling import load_traffic
+
+    traffic = load_traffic(os.path.join(ROOT, "profiles", f"traffic_{cfg.name}.json"), dominant)
     attn_ms, attn_n = prof["attention"]
     attn_gbs = bf["attention"][0] / (attn_ms / attn_n / 1e3) / 1e9
     kernel_avg_us = {k: round(v[0] / v[1] * 1e3, 3) for k, v in prof.items() if v[1]}
@@ -238,6 +264,7 @@ def main():
         },
         "denoise_step_us": round(chunk_s / cfg.num_steps * 1e6, 2),
         "chunk_ms": round(chunk_s * 1e3, 4),
+        "chunk_latency_ms": lat,
         "attn_hbm_gbs": round(attn_gbs, 1),
         "kernel_avg_us": kernel_avg_us,
         "roofline": {
@@ -247,7 +274,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": traffic,
         },
         "b32": b32,
         "cpu_baseline": cpu,

@@ -1,0 +1,189 @@
+"""Reduce rocprofv3 output for the denoise kernels to short text summaries.
+
+Two inputs are used:
+
+* the kernel-trace statistics CSV (``--kernel-trace --stats``), which gives
+  calls and average duration per kernel;
+* two counter-collection CSVs, one from a ``--pmc FETCH_SIZE`` run and one from
+  a ``--pmc WRITE_SIZE`` run of the same command. Each gives KiB per dispatch.
+
+The counters are calibrated against a plain elementwise copy of known size,
+launched in the same process before the workload (``bench.py
+--calibrate-copy``: 256 MiB read and 256 MiB written per launch). Each
+counter's factor is the copy's true bytes divided by what the counter reported
+for the copy. The factor then scales the same counter for the kernel of
+interest.
+
+The traffic record written here carries a digest of the kernel's source files.
+``bench.py`` reports the measured traffic only while that digest still matches
+the sources, so a stale figure is never attached to a changed kernel.
+
+Usage::
+
+    python -m paper_2607_14695_amd.profiling --stats KT_kernel_stats.csv \\
+        --fetch FETCH_counter_collection.csv --write WRITE_counter_collection.csv \\
+        --kernel attn32_kernel --kernel-class attention --workload pi0_chunk_bf16 \\
+        --command-kt "..." --command-fetch "..." --command-write "..." \\
+        --out-md profiles/attention_pi0_chunk_bf16.md \\
+        --out-json profiles/traffic_pi0_chunk_bf16.json
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import re
+from typing import Dict, List, Optional, Tuple
+
+CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+
+# source files that determine each kernel class's machine code
+KERNEL_SOURCES: Dict[str, Tuple[str, ...]] = {
+    "attention": ("attention.hip", "common.h", "kernels.h"),
+    "attn_merge": ("attention.hip", "common.h", "kernels.h"),
+    "gemm_qkv": ("gemm.hip", "common.h", "kernels.h"),
+    "gemm_o": ("gemm.hip", "common.h", "kernels.h"),
+    "gemm_gate_up": ("gemm.hip", "common.h", "kernels.h"),
+    "gemm_down": ("gemm.hip", "common.h", "kernels.h"),
+    "resid_norm": ("norm_ring.hip", "common.h", "kernels.h"),
+    "embed_norm": ("norm_ring.hip", "common.h", "kernels.h"),
+    "final_euler": ("norm_ring.hip", "common.h", "kernels.h"),
+}
+
+COPY_BYTES = 256 << 20  # bytes read, and bytes written, by one calibration copy
+COPY_PATTERN = re.compile(r"MulFunctor")
+
+
+def source_digest(kernel_class: str) -> str:
+    """sha256 over the source files of a kernel class (names and contents)."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel_class]:
+        h.update(name.encode())
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def _rows(path: str) -> List[dict]:
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def counter_per_dispatch(path: str, counter: str, kernel_pattern: str) -> Tuple[float, int, float]:
+    """(average value per matching dispatch, matching dispatches, copy value).
+
+    A dispatch can be listed once per counter instance; values of one
+    dispatch are summed first."""
+    per_dispatch: Dict[Tuple[str, str], float] = {}
+    names: Dict[Tuple[str, str], str] = {}
+    for r in _rows(path):
+        if r["Counter_Name"] != counter:
+            continue
+        key = (r["Dispatch_Id"], r.get("Agent_Id", ""))
+        per_dispatch[key] = per_dispatch.get(key, 0.0) + float(r["Counter_Value"])
+        names[key] = r["Kernel_Name"]
+    pat = re.compile(kernel_pattern)
+    vals = [v for k, v in per_dispatch.items() if pat.search(names[k])]
+    copies = [v for k, v in per_dispatch.items() if COPY_PATTERN.search(names[k])]
+    if not vals:
+        raise ValueError(f"no dispatch of {kernel_pattern!r} with counter {counter} in {path}")
+    if not copies:
+        raise ValueError(f"no calibration copy dispatch in {path}")
+    return sum(vals) / len(vals), len(vals), sorted(copies)[len(copies) // 2]
+
+
+def kernel_stats(path: str) -> List[dict]:
+    out = []
+    for r in _rows(path):
+        out.append({"name": r["Name"], "calls": int(r["Calls"]), "total_ns": float(r["TotalDurationNs"]),
+                    "avg_ns": float(r["AverageNs"]), "min_ns": float(r["MinNs"]), "max_ns": float(r["MaxNs"]),
+                    "pct": float(r["Percentage"])})
+    out.sort(key=lambda d: -d["total_ns"])
+    return out
+
+
+def _short(name: str) -> str:
+    name = re.sub(r"^void ", "", name)
+    return re.sub(r"\(.*\)$", "", name)
+
+
+def stats_markdown(stats: List[dict], command: str, limit: int = 20) -> str:
+    lines = ["| kernel | calls | avg us | min us | max us | % of GPU time |", "|---|---|---|---|---|---|"]
+    for d in stats[:limit]:
+        lines.append(f"| `{_short(d['name'])}` | {d['calls']} | {d['avg_ns'] / 1e3:.2f} | {d['min_ns'] / 1e3:.2f} | "
+                     f"{d['max_ns'] / 1e3:.2f} | {d['pct']:.2f} |")
+    return f"Command:\n\n```\n{command}\n```\n\n" + "\n".join(lines) + "\n"
+
+
+def main(argv: Optional[List[str]] = None) -> None:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--stats", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--kernel", required=True, help="regex selecting the kernel's dispatches")
+    ap.add_argument("--kernel-class", required=True, choices=sorted(KERNEL_SOURCES))
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--command-kt", required=True)
+    ap.add_argument("--command-fetch", default="")
+    ap.add_argument("--command-write", default="")
+    ap.add_argument("--out-md", required=True)
+    ap.add_argument("--out-json")
+    args = ap.parse_args(argv)
+
+    stats = kernel_stats(args.stats)
+    pat = re.compile(args.kernel)
+    mine = [d for d in stats if pat.search(d["name"])]
+    md = [f"# rocprofv3 summary: {args.kernel_class} on {args.workload}\n",
+          "## Kernel trace statistics\n", stats_markdown(stats, args.command_kt)]
+    rec = None
+    if args.fetch and args.write:
+        f_avg, f_n, f_copy = counter_per_dispatch(args.fetch, "FETCH_SIZE", args.kernel)
+        w_avg, w_n, w_copy = counter_per_dispatch(args.write, "WRITE_SIZE", args.kernel)
+        f_fac = COPY_BYTES / (f_copy * 1024.0)
+        w_fac = COPY_BYTES / (w_copy * 1024.0)
+        total = f_avg * 1024.0 * f_fac + w_avg * 1024.0 * w_fac
+        rec = {
+            "workload": args.workload, "kernel_class": args.kernel_class, "kernel_regex": args.kernel,
+            "digest": source_digest(args.kernel_class),
+            "fetch_kib_per_dispatch": round(f_avg, 3), "write_kib_per_dispatch": round(w_avg, 3),
+            "dispatches": [f_n, w_n],
+            "copy_fetch_kib": f_copy, "copy_write_kib": w_copy,
+            "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4),
+            "hbm_bytes_per_launch": round(total),
+            "avg_duration_us": round(mine[0]["avg_ns"] / 1e3, 3) if mine else None,
+            "commands": {"kernel_trace": args.command_kt, "fetch": args.command_fetch, "write": args.command_write},
+        }
+        md += ["## HBM traffic from counters\n",
+               f"Commands:\n\n```\n{args.command_fetch}\n{args.command_write}\n```\n",
+               "| quantity | value |", "|---|---|",
+               f"| calibration copy FETCH_SIZE (KiB, 256 MiB read) | {f_copy:.1f} |",
+               f"| calibration copy WRITE_SIZE (KiB, 256 MiB written) | {w_copy:.1f} |",
+               f"| fetch factor | {f_fac:.4f} |", f"| write factor | {w_fac:.4f} |",
+               f"| {args.kernel_class} FETCH_SIZE per dispatch (KiB, raw) | {f_avg:.1f} ({f_n} dispatches) |",
+               f"| {args.kernel_class} WRITE_SIZE per dispatch (KiB, raw) | {w_avg:.1f} ({w_n} dispatches) |",
+               f"| {args.kernel_class} calibrated HBM bytes per launch | {total / 1e6:.3f} MB |", ""]
+    with open(args.out_md, "w") as f:
+        f.write("\n".join(md))
+    if rec is not None and args.out_json:
+        with open(args.out_json, "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
+
+
+def load_traffic(path: str, kernel_class: str) -> Optional[int]:
+    """HBM bytes per launch from a traffic record, or None when the record is
+    missing, is for another kernel class, or the kernel's sources changed."""
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_class") != kernel_class or rec.get("digest") != source_digest(kernel_class):
+        return None
+    return int(rec["hbm_bytes_per_launch"])
+
+
+if __name__ == "__main__":
+    main()
