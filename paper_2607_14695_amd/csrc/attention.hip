@@ -540,6 +540,272 @@ __global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
   if (h == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
 }
 
+// ---------------------------------------------------------------------------
+// bf16 variant: eight waves of 16 query rows (16x16x32 MFMAs), two waves per
+// SIMD.  With 16 rows a wave holds its Q fragments (32 registers), its O^T
+// accumulator (64) and the scores (16) with room to keep eight LDS fragment
+// reads in flight, and the second wave on the SIMD covers the latency the
+// first one waits on.  A workgroup covers 128 query rows, like the launch
+// geometry of the other variants, and stages each 64-key tile once in LDS for
+// all eight waves.
+//
+// Tiles reach LDS by global_load_lds_dwordx4 into two stages (tile t+1 in
+// flight during tile t).  16-byte chunks are XOR-swizzled on the global side
+// of the DMA: K chunk c of row r sits at c ^ RFX_KSWZ(r), V^T chunk c of row d at
+// c ^ (d mod 8).  Every per-lane LDS offset takes at most eight values, the
+// rest being instruction immediates.
+//
+// Key order.  S^T block kb = 2j + e (16 keys x 16 queries) takes as its A
+// operand row r the key 32j + 8*(r >> 2) + 4e + (r & 3).  Its result then
+// leaves lane l (g = l >> 4) holding keys 32j + 8g + 4e + i, i < 4: over the
+// two blocks of chunk j the lane owns the 8 consecutive keys 32j + 8g + [0, 8),
+// which is exactly the contraction slice a B operand lane supplies to the
+// 16x16x32 MFMA of O^T = V^T P^T.  The probabilities are used where they were
+// computed, and each V^T fragment is one 16-byte chunk of one V^T row.
+// ---------------------------------------------------------------------------
+// K swizzle: 16 distinct values over the 16 rows a block's lanes read
+// (8 for 64-wide heads, whose rows have 8 chunks)
+#define RFX_KSWZ(r, kch) ((kch) >= 16 ? (((r) & 3) | (((r) >> 1) & 12)) : (((r) & 3) | (((r) >> 1) & 4)))
+
+RFX_DEV uint32_t pack_bf16x2(float a, float b) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_v;
+  const bf16x2_v v = {(__bf16)a, (__bf16)b};  // v_cvt_pk_bf16_f32, round to nearest even
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+template <int DH>
+__global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
+  using T = bf16_t;
+  constexpr int NW = 8;
+  constexpr int NKS = DH / 32;            // 32-wide d steps of S^T
+  constexpr int NDB = DH / 16;            // 16-wide d blocks of O^T
+  constexpr int KRB = DH * 2;             // bytes per K row in LDS
+  constexpr int KCH = DH / 8;             // 16-byte chunks per K row
+  constexpr int NKO = KCH >= 16 ? 4 : 2;  // distinct per-lane K chunk offsets per parity
+  constexpr int VRB = AKT * 2;            // bytes per V^T row (128)
+  constexpr int KBYTES = AKT * KRB;
+  constexpr int VBYTES = DH * VRB;
+  constexpr int STAGE = KBYTES + VBYTES;
+  constexpr int NIK = KBYTES / 1024 / NW;  // 1-KB DMA instructions per wave, K
+  constexpr int NIV = VBYTES / 1024 / NW;  // same for V^T
+  static_assert(NIK >= 1 && NIV >= 1, "tile smaller than one DMA round");
+  __shared__ __attribute__((aligned(16))) unsigned char stage0[STAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char stage1[STAGE];
+
+  int group, rb;
+  if (!attn_decode(blockIdx.x, p.B * p.nsplit, p.rows_pad / 128, group, rb)) return;
+  const int b = group / p.nsplit, split = group - b * p.nsplit;
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int T_ = p.T, Hq = p.Hq;
+  const int nrows = T_ * Hq;
+  const int rq = rb * 128 + wave * 16 + r16;
+  const bool qvalid = rq < nrows;
+  const int iq = qvalid ? rq / Hq : 0;
+  const int jq = qvalid ? rq % Hq : 0;
+
+  uint4 qf[NKS];
+  {
+    // rows past the valid range compute on row 0's data and are never stored
+    const T* qrow = reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + (qvalid ? rq : 0)) * DH + g * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = ld16(qrow + ks * 32);
+  }
+
+  const int Lc = p.static_len + (*p.n_valid) * p.frame_tokens;
+  const int n_ct = (Lc + AKT - 1) / AKT;
+  const int n_dt = (T_ + AKT - 1) / AKT;
+  const int total = n_ct + n_dt;
+  const int per = (total + p.nsplit - 1) / p.nsplit;
+  const int t_beg = split * per;
+  const int t_end = min(total, t_beg + per);
+
+  const T* ck = reinterpret_cast<const T*>(p.cache_k) + (int64_t)b * p.ck_bstride;
+  const T* cvt = reinterpret_cast<const T*>(p.cache_vt) + (int64_t)b * p.ck_bstride;
+  const T* kdb = reinterpret_cast<const T*>(p.kd) + (int64_t)b * T_ * DH;
+  const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
+  const float scale = rsqrtf((float)DH) * 1.4426950408889634f;
+  const int tpad = p.tpad, Rrow = p.R;  // copied: a lambda must not capture the kernel argument
+  constexpr int RPI = 64 / KCH;         // K rows per DMA instruction
+
+  // DMA of tile t into stage sk.  Per-lane offsets are rebuilt from an opaque
+  // copy of the lane id on every call so they are not hoisted into registers.
+  auto issue = [&](int t, unsigned char* sk) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const bool dyn = t >= n_ct;
+    const int base = dyn ? (t - n_ct) * AKT : t * AKT;
+    const int last = (dyn ? T_ : Lc) - 1;
+    unsigned char* sv = sk + KBYTES;
+    const int kl = ln % KCH, kr = ln / KCH;
+    const int vd = ln >> 3, vc = ln & 7;
+    if (dyn) {
+#pragma unroll
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        const int r = min(base + row, last);
+        __builtin_amdgcn_global_load_lds(kdb + r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8, sk + (wave * NIK + j) * 1024, 16,
+                                         0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        __builtin_amdgcn_global_load_lds(vdb + d * tpad + base + (vc ^ (d & 7)) * 8, sv + (wave * NIV + j) * 1024, 16,
+                                         0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        const int r = min(base + row, last);
+        __builtin_amdgcn_global_load_lds(ck + (int64_t)r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8,
+                                         sk + (wave * NIK + j) * 1024, 16, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        const int key = base + (vc ^ (d & 7)) * 8;
+        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + (key <= last ? key : 0),
+                                         sv + (wave * NIV + j) * 1024, 16, 0, 0);
+      }
+    }
+  };
+
+  f32x4_v o[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) o[db] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // per-lane LDS read offsets (bytes).  K: row rho = 8*(r16 >> 2) + 4e +
+  // (r16 & 3) of a 32-key chunk, d-chunk 4*ks + g, the low bits of ks in x.
+  // V^T: row db*16 + r16, key chunk 4j + g.
+  int koff[2][NKO], voff[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int rho = 8 * (r16 >> 2) + 4 * e + (r16 & 3);
+#pragma unroll
+    for (int x = 0; x < NKO; ++x) koff[e][x] = rho * KRB + ((4 * x + g) ^ RFX_KSWZ(rho, KCH)) * 16;
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) voff[j] = r16 * VRB + ((4 * j + g) ^ (r16 & 7)) * 16;
+
+  auto step = [&](int t, const unsigned char* cur, unsigned char* nxt) __attribute__((always_inline)) {
+    const bool dyn = t >= n_ct;
+    // tile t's DMA (the only one outstanding) completes; after the barrier
+    // every wave's part of it is visible and every wave has finished reading
+    // the other stage, which tile t+1 then overwrites during the math
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    lds_barrier();
+    if (t + 1 < t_end) issue(t + 1, nxt);
+    const unsigned char* sk = cur;
+    const unsigned char* sv = cur + KBYTES;
+
+    // S^T = K Q^T: four 16-key blocks, their accumulation chains interleaved
+    f32x4_v s[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) s[kb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k0 = 0; k0 < NKS; k0 += 2) {
+      uint4 a[2][4];
+#pragma unroll
+      for (int u = 0; u < 2 && k0 + u < NKS; ++u)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          const int ks = k0 + u;
+          a[u][kb] = *reinterpret_cast<const uint4*>(sk + (kb >> 1) * 32 * KRB + (ks / NKO) * NKO * 64 +
+                                                     koff[kb & 1][ks % NKO]);
+        }
+#pragma unroll
+      for (int u = 0; u < 2 && k0 + u < NKS; ++u)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) mfma_step(s[kb], a[u][kb], qf[k0 + u], T());
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+
+    // block kb = 2j + e holds keys 32j + 8g + 4e + i; visible iff below lim
+    const int lim = (dyn ? (iq > 0 ? T_ : 1) - (t - n_ct) * AKT : Lc - t * AKT) - 8 * g;
+    float mt = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = (kb >> 1) * 32 + 4 * (kb & 1) + i < lim ? s[kb][i] * scale : -INFINITY;
+        s[kb][i] = v;
+        mt = fmaxf(mt, v);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    // lazy rescaling (see attn32_kernel): probabilities stay below 2^8
+    if (__any(mt > m_run + 8.f)) {
+      const float m_new = fmaxf(m_run, mt);
+      const float corr = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+      l_run *= corr;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] *= corr;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    // scores are at most m_run + 8: the plain hardware exp2 (no denormal
+    // range handling) is exact enough; masked keys give exp2(-inf) = 0
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = __builtin_amdgcn_exp2f(s[kb][i] - m_use);
+        s[kb][i] = e;
+        psum += e;
+      }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    l_run += psum;
+
+    // O^T += V^T P^T, two 32-key chunks; slot 8g + 4e + i <-> key 32j + 8g + 4e + i
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint4 pf = make_uint4(pack_bf16x2(s[2 * j][0], s[2 * j][1]), pack_bf16x2(s[2 * j][2], s[2 * j][3]),
+                                  pack_bf16x2(s[2 * j + 1][0], s[2 * j + 1][1]),
+                                  pack_bf16x2(s[2 * j + 1][2], s[2 * j + 1][3]));
+#pragma unroll
+      for (int d0 = 0; d0 < NDB; d0 += 8) {
+        uint4 vf[8];
+#pragma unroll
+        for (int u = 0; u < 8 && d0 + u < NDB; ++u)
+          vf[u] = *reinterpret_cast<const uint4*>(sv + (d0 + u) * 16 * VRB + voff[j]);
+#pragma unroll
+        for (int u = 0; u < 8 && d0 + u < NDB; ++u) mfma_step(o[d0 + u], vf[u], pf, T());
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+      }
+    }
+  };
+
+  if (t_beg < t_end) issue(t_beg, stage0);
+  for (int t = t_beg; t < t_end; t += 2) {
+    step(t, stage0, stage1);
+    if (t + 1 < t_end) step(t + 1, stage1, stage0);
+  }
+
+  if (!qvalid) return;
+  if (p.nsplit == 1) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    T* dst = reinterpret_cast<T*>(p.out) + ((int64_t)b * T_ + iq) * (int64_t)(Hq * DH) + jq * DH + 4 * g;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      *reinterpret_cast<uint2*>(dst + db * 16) =
+          make_uint2(pack_bf16x2(o[db][0] * inv, o[db][1] * inv), pack_bf16x2(o[db][2] * inv, o[db][3] * inv));
+    return;
+  }
+  const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq;
+  float* dst = p.part_o + prow * DH + 4 * g;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+    *reinterpret_cast<float4*>(dst + db * 16) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+  if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
+}
+
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
 // splits combined in index order.  One thread per (query row, d).
 constexpr int kMaxSplits = 16;
@@ -604,7 +870,7 @@ static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
   const int groups = a.B * a.nsplit;
   if constexpr (sizeof(T) == 2) {
     const int nwg = ((groups + 7) / 8) * 8 * (a.rows_pad / 128);
-    RFX_LAUNCH((attn32_kernel<DH>), dim3(nwg), dim3(256), 0, s, a);
+    RFX_LAUNCH((attn16_kernel<DH>), dim3(nwg), dim3(512), 0, s, a);
   } else {
     const int nwg = ((groups + 7) / 8) * 8 * (a.rows_pad / 64);
     RFX_LAUNCH((attn_kernel<T, DH>), dim3(nwg), dim3(256), 0, s, a);

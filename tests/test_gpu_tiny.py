@@ -179,6 +179,33 @@ def test_ragged_multi_env(frame_dim):
     eng.close()
 
 
+BF16_REL, BF16_ABS = 1e-2, 5e-2
+
+
+@pytest.mark.parametrize("head_dim,frame_dim", [(64, 72), (128, 0), (256, 48)])
+def test_ragged_bf16(head_dim, frame_dim):
+    """The bf16 path (bf16 attention tiles, bf16 GEMM operands) at every head
+    width it supports, with ragged tiles and blocks: Ls = 40 and F = 24 leave
+    partial 64-key tiles, T*Hq = 18 a partial 128-row query block; three envs;
+    a 3-slot ring wrapped twice.  Tolerance: relative-L2 1e-2 and max-abs 5e-2
+    on the action chunk (bf16 operands, fp32 accumulation)."""
+    cfg = RAGGED.replace(name=f"ragged_bf16_{head_dim}", dtype="bf16", head_dim=head_dim, frame_dim=frame_dim)
+    w, sk, sv, frames = _setup(cfg, 7)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(7):
+        eng.write_frame(frames[t])
+        if t in (0, 2, 6):
+            state, noise = WL.make_state(cfg, t), WL.make_noise(cfg, t)
+            got = eng.denoise(state, noise).cpu().numpy()
+            eng.synchronize()
+            ref = O.denoise_chunk(cfg, w, sk, sv, frames, t + 1, state, noise, cfg.taus())
+            rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+            mx = float(np.max(np.abs(got - ref)))
+            print(f"bf16 dh={head_dim} tick {t}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+            assert rel <= BF16_REL and mx <= BF16_ABS, (t, rel, mx)
+    eng.close()
+
+
 def test_dtype_probe_rejects_mismatch(tiny):
     cfg, w, sk, sv, frames = tiny
     with pytest.raises(R.ReflexError) as ei:
