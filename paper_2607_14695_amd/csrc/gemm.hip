@@ -188,6 +188,183 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny(GemmArgs p) {
 }
 
 // --------------------------------------------------------------------------
+// skinny, bf16, activations staged in LDS.  The activation rows of the
+// workgroup's K range are copied to LDS with global_load_lds_dwordx4, each
+// instruction moving 1 KB of consecutive bytes of one row, instead of being
+// fetched as MFMA fragments (16 rows x 64 bytes per instruction) straight
+// from global memory by every wave.  16-byte chunks are XOR-swizzled by
+// (row mod 8) so the fragment reads are conflict-free.  Weights are still
+// streamed as fragments into registers; the activation copy is issued first,
+// so the wait for it leaves the weight loads in flight.  After the MFMAs the
+// same LDS holds the cross-wave reduction.
+// --------------------------------------------------------------------------
+RFX_DEV void wg_barrier_lds() {
+  // all of this wave's LDS reads are complete; then a plain barrier (the
+  // memory clobber keeps the compiler from moving LDS accesses across it)
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int MB, int NB, int EPI, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_skinny_lds(GemmArgs p) {
+  using T = bf16_t;
+  constexpr int PAIR = EpiPair<EPI>::value;
+  constexpr int KS = 32;                           // elements per k-step
+  constexpr int NBT = PAIR ? 2 * NB : NB;          // B fragments per k-step
+  constexpr int COLS = 16 * NB;                    // first columns per workgroup
+  constexpr int RCOLS = 16 * NBT + 1;              // reduction row (padded)
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int z = blockIdx.z;
+  const int mchunk = blockIdx.y / p.splits, split = blockIdx.y % p.splits;
+  const int m0 = mchunk * (16 * MB);
+  int n0, pair_off;
+  if constexpr (PAIR == PAIR_HEAD) {
+    const int half = p.qkv.head_dim >> 1, per_head = half / COLS;
+    const int h = blockIdx.x / per_head;
+    n0 = h * p.qkv.head_dim + (blockIdx.x - h * per_head) * COLS;
+    pair_off = half;
+  } else {
+    n0 = blockIdx.x * COLS;
+    pair_off = p.N;
+  }
+  const int kbeg = split * p.k_per_split;
+  const int kend = min(p.K, kbeg + p.k_per_split);
+  const int nsteps = (kend - kbeg) / KS;  // K and k_per_split are multiples of 32
+  const int rs = p.k_per_split * 2;       // LDS bytes per activation row
+  const int cpr = rs >> 4;                // 16-byte chunks per row
+
+  const T* A = reinterpret_cast<const T*>(p.A) + (int64_t)z * p.a_bstride;
+  const T* B = reinterpret_cast<const T*>(p.B) + (int64_t)z * p.b_bstride;
+
+  // 1. activation rows m0 .. m0+16*MB-1 (rows past M repeat row M-1), chunks
+  //    kbeg/8 .. ; chunk position q of row r holds logical chunk q ^ (r & 7)
+  {
+    const int total = 16 * MB * cpr;  // chunks
+    const int kchunks = (kend - kbeg) >> 3;
+    for (int i0 = wave * 64; i0 < total; i0 += NW * 64) {
+      const int q = i0 + lane;
+      const int r = q / cpr, pos = q - r * cpr;
+      int lc = pos ^ (r & 7);
+      lc = lc < kchunks ? lc : 0;  // past the end of a short last split: any valid chunk
+      const T* src = A + (int64_t)min(m0 + r, p.M - 1) * p.lda + kbeg + lc * 8;
+      __builtin_amdgcn_global_load_lds(src, smem + i0 * 16, 16, 0, 0);
+    }
+  }
+
+  // 2. weight fragments of this wave's k-steps (s = wave, wave + NW, ...)
+  const T* brow[NBT];
+#pragma unroll
+  for (int nb = 0; nb < NBT; ++nb) {
+    int brw;
+    if (PAIR == PAIR_NONE) {
+      brw = min(n0 + nb * 16 + r16, p.N - 1);
+    } else {
+      const int c = n0 + (nb % NB) * 16 + r16;
+      brw = nb >= NB ? c + pair_off : c;
+    }
+    brow[nb] = B + (int64_t)brw * p.ldb + kbeg + g * 8;
+  }
+
+  f32x4_v acc[MB][NBT];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NBT; ++nb) acc[mb][nb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+
+  // per-lane activation fragment offset: row 16mb + r16, chunk 4s + g at
+  // position (4s + g) ^ (r16 & 7) = 8*(s >> 1) + ((4*(s & 1) + g) ^ (r16 & 7))
+  const int aoff0 = r16 * rs + ((g) ^ (r16 & 7)) * 16;
+  const int aoff1 = r16 * rs + ((4 + g) ^ (r16 & 7)) * 16;
+
+  constexpr int U = 4;
+  bool first = true;
+  for (int s0 = wave; s0 < nsteps; s0 += NW * U) {
+    uint4 bf[U][NBT];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = s0 + NW * u;
+      const int sc = s < nsteps ? s : s0;  // clamped: a valid address, result unused
+#pragma unroll
+      for (int nb = 0; nb < NBT; ++nb) bf[u][nb] = ld16(brow[nb] + sc * KS);
+    }
+    if (first) {
+      // the activation copy was issued before these weight loads and loads
+      // complete in order: wait for it, leave the weight loads in flight
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | ((U * NBT) & 15) | (((U * NBT) >> 4) << 14));
+      wg_barrier_lds();
+      first = false;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = s0 + NW * u;
+      if (s >= nsteps) break;
+      const unsigned char* ab = smem + (s >> 1) * 128 + ((s & 1) ? aoff1 : aoff0);
+      uint4 af[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) af[mb] = *reinterpret_cast<const uint4*>(ab + mb * 16 * rs);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBT; ++nb) mfma_step(acc[mb][nb], af[mb], bf[u][nb], T());
+    }
+  }
+  if (first) {  // waves without k-steps still take part in the barrier
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+    wg_barrier_lds();
+  }
+
+  // 3. cross-wave reduction through the (now free) activation LDS
+  wg_barrier_lds();
+  float* red = reinterpret_cast<float*>(smem);  // [NW][MB*16][RCOLS]
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NBT; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[(wave * MB * 16 + mb * 16 + 4 * g + i) * RCOLS + nb * 16 + r16] = acc[mb][nb][i];
+  __syncthreads();
+  for (int e = threadIdx.x; e < MB * 16 * COLS; e += 64 * NW) {
+    const int row = e / COLS, col = e % COLS;
+    const int grow = m0 + row;
+    const int gcol = n0 + col;
+    if (grow >= p.M || (PAIR == PAIR_NONE && gcol >= p.N)) continue;
+    float v = 0.f, u = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      v += red[(w * MB * 16 + row) * RCOLS + col];
+      if (PAIR) u += red[(w * MB * 16 + row) * RCOLS + col + COLS];
+    }
+    epilogue_store<EPI, bf16_t>(p, z, split, grow, gcol, v, u);
+  }
+}
+
+// launch helper for the LDS-staged skinny kernel (bf16, M <= 64)
+template <int MB, int EPI>
+static void launch_skinny_lds_cfg(const GemmArgs& a, hipStream_t s, int nw) {
+  constexpr int PAIR = EpiPair<EPI>::value;
+  constexpr int NB = PAIR ? 1 : 2;
+  constexpr int NBT = PAIR ? 2 * NB : NB;
+  int nx;
+  if (PAIR == PAIR_HEAD)
+    nx = a.N / 32;
+  else if (PAIR == PAIR_N)
+    nx = a.N / 16;
+  else
+    nx = (a.N + 16 * NB - 1) / (16 * NB);
+  const int mch = (a.M + 16 * MB - 1) / (16 * MB);
+  dim3 grid(nx, mch * a.splits, a.batch);
+  const size_t tile = (size_t)16 * MB * a.k_per_split * 2;
+  const size_t red = (size_t)nw * MB * 16 * (16 * NBT + 1) * 4;
+  const size_t shm = tile > red ? tile : red;
+  if (nw == 8)
+    RFX_LAUNCH((gemm_skinny_lds<MB, NB, EPI, 8>), grid, dim3(512), shm, s, a);
+  else
+    RFX_LAUNCH((gemm_skinny_lds<MB, NB, EPI, 4>), grid, dim3(256), shm, s, a);
+}
+
+// --------------------------------------------------------------------------
 // tiled: 128 x 128 workgroup tile (paired: 128 rows x 64 first + 64 paired cols)
 // --------------------------------------------------------------------------
 constexpr int TBM = 128, TBN = 128, TROWB = 128, TPAD = 16;  // TROWB: bytes of K per stage row
@@ -373,8 +550,38 @@ static void launch_skinny_cfg(const GemmArgs& a, hipStream_t s) {
     RFX_LAUNCH((gemm_skinny<T, MB, NB, EPI, 4>), grid, dim3(256), 0, s, a);
 }
 
+// dynamic LDS above the default 64 KB limit must be allowed per kernel, once
+template <typename K>
+static void allow_large_lds(K kernel) {
+  static const hipError_t once =
+      hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  (void)once;
+}
+
+template <int MB, int EPI>
+static void launch_skinny_lds_pick(const GemmArgs& a, hipStream_t s) {
+  constexpr int PAIR = EpiPair<EPI>::value;
+  constexpr int NB = PAIR ? 1 : 2;
+  // eight waves when every wave gets at least two k-steps
+  const int nw = a.k_per_split >= 16 * 32 ? 8 : 4;
+  if (nw == 8)
+    allow_large_lds(gemm_skinny_lds<MB, NB, EPI, 8>);
+  else
+    allow_large_lds(gemm_skinny_lds<MB, NB, EPI, 4>);
+  launch_skinny_lds_cfg<MB, EPI>(a, s, nw);
+}
+
 template <typename T, int EPI>
 static void launch_skinny(const GemmArgs& a, hipStream_t s) {
+  // bf16 with the activation K range fitting in LDS: stage it there
+  if (sizeof(T) == 2 && (size_t)16 * skinny_mb(a.M) * a.k_per_split * 2 <= 160 * 1024 && a.k_per_split % 32 == 0 &&
+      a.K % 32 == 0) {
+    switch (skinny_mb(a.M)) {
+      case 1: launch_skinny_lds_pick<1, EPI>(a, s); return;
+      case 2: launch_skinny_lds_pick<2, EPI>(a, s); return;
+      default: launch_skinny_lds_pick<4, EPI>(a, s); return;
+    }
+  }
   switch (skinny_mb(a.M)) {
     case 1: launch_skinny_cfg<T, 1, EPI>(a, s); break;
     case 2: launch_skinny_cfg<T, 2, EPI>(a, s); break;
