@@ -506,6 +506,207 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
 }
 
 // --------------------------------------------------------------------------
+// tiled, bf16, direct global->LDS pipeline.  Same 128x128 workgroup tile and
+// 2x2 waves of 64x64 as gemm_tiled, but each 64-element K stage (128 bytes of
+// every A and B row) is copied by global_load_lds_dwordx4 (1 KB of whole rows
+// per instruction) instead of through registers.  NS = 2: double-buffered,
+// 64 KB of LDS, two workgroups per CU (the other workgroup's MFMAs cover a
+// stage's copy latency); NS = 4: a ring of four stages, three in flight, one
+// workgroup per CU.  Two stages measured faster at the batch-32 shapes.
+// 16-byte chunks are XOR-swizzled (RFX_GSWZ).  K and the split length must be
+// multiples of 64 (no partial stage to zero-fill).
+// --------------------------------------------------------------------------
+constexpr int DST = 64;                  // K elements per stage
+constexpr int DROWB = DST * 2;           // bytes per stage row (128)
+constexpr int DSTAGE = (TBM + TBN) * DROWB;  // bytes per stage (32 KB)
+
+// chunk swizzle of stage row r: 16 distinct bank positions over 16
+// consecutive 128-byte rows (the row parity picks the half of the 256-byte
+// bank window, the XOR the 16-byte slot)
+#define RFX_GSWZ(r) (((r) & 7) ^ (((r) >> 3) & 1))
+
+// Workgroup -> tile.  Workgroups are dispatched round-robin over the 8 XCDs,
+// each with its own L2.  With a 1-D grid, XCD x receives the tiles
+// [x*per, (x+1)*per) of the tile sequence in which the M tile varies fastest,
+// so the workgroups sharing an L2 also share B (weight) tiles and a band of
+// A tiles instead of touching every tile of both operands.
+template <int PAIR>
+RFX_DEV bool dma_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
+  const int nx = PAIR == PAIR_NONE ? (p.N + TBN - 1) / TBN : p.N / (PAIR == PAIR_N ? 64 : 128);
+  const int ny = (p.M + TBM - 1) / TBM;
+  const int total = nx * ny * p.batch * p.splits;
+  const int per = (total + 7) / 8;
+  const int t = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (t >= total) return false;
+  by = t % ny;
+  const int rest = t / ny;
+  bx = rest % nx;
+  bz = rest / nx;
+  return true;
+}
+
+template <int EPI, int NS>
+__global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
+  using T = bf16_t;
+  constexpr int PAIR = EpiPair<EPI>::value;
+  static_assert(NS == 2 || NS == 4, "two or four stages");
+  __shared__ __attribute__((aligned(16))) unsigned char st0[DSTAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char st1[DSTAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char st2[NS == 4 ? DSTAGE : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char st3[NS == 4 ? DSTAGE : 16];
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;
+  int bx, by, bz;
+  if (!dma_tile<PAIR>(p, bx, by, bz)) return;
+  const int z = bz / p.splits, split = bz % p.splits;
+  const int m0 = by * TBM;
+  int n0, pair_off;
+  if constexpr (PAIR == PAIR_HEAD) {
+    const int half = p.qkv.head_dim >> 1, per_head = half / 64;
+    const int h = bx / per_head;
+    n0 = h * p.qkv.head_dim + (bx - h * per_head) * 64;
+    pair_off = half;
+  } else if constexpr (PAIR == PAIR_N) {
+    n0 = bx * 64;
+    pair_off = p.N;
+  } else {
+    n0 = bx * TBN;
+    pair_off = 0;
+  }
+  const int kbeg = split * p.k_per_split;
+  const int kend = min(p.K, kbeg + p.k_per_split);
+  const int nst = (kend - kbeg) / DST;
+
+  const T* A = reinterpret_cast<const T*>(p.A) + (int64_t)z * p.a_bstride;
+  const T* B = reinterpret_cast<const T*>(p.B) + (int64_t)z * p.b_bstride;
+
+  // DMA: wave w, instruction j covers stage rows 8*(4w + j) + (lane >> 3) of A
+  // (j < 4) or B (j >= 4), physical chunk lane & 7 = logical (lane & 7) ^ (row & 7)
+  const T* gsrc[8];
+  {
+    const int rr = lane >> 3, pc = lane & 7;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = 8 * (4 * wave + (j & 3)) + rr + (j >= 4 ? 0 : 0);
+      const int lc = pc ^ RFX_GSWZ(row);
+      if (j < 4) {
+        gsrc[j] = A + (int64_t)min(m0 + row, p.M - 1) * p.lda + kbeg + lc * 8;
+      } else {
+        int brw;
+        if (PAIR != PAIR_NONE) {
+          const int c = n0 + (row & 63);
+          brw = row >= 64 ? c + pair_off : c;
+        } else {
+          brw = min(n0 + row, p.N - 1);
+        }
+        gsrc[j] = B + (int64_t)brw * p.ldb + kbeg + lc * 8;
+      }
+    }
+  }
+  // stage layout: A rows 0..127 then B rows 0..127, 128 bytes each
+  auto issue = [&](int st, unsigned char* buf) __attribute__((always_inline)) {
+    const int k0 = st * DST;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = 8 * (4 * wave + (j & 3));
+      __builtin_amdgcn_global_load_lds(gsrc[j] + k0, buf + ((j >= 4 ? TBM : 0) + row) * DROWB, 16, 0, 0);
+    }
+  };
+
+  f32x4_v acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+
+  // fragment offsets: row r (r & 7 == r16 & 7), k-step kk of the stage,
+  // chunk 4kk + g at (4kk + g) ^ (r16 & 7)
+  int foff[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) foff[kk] = r16 * DROWB + ((4 * kk + g) ^ RFX_GSWZ(r16)) * 16;
+  int brow_l[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    if (PAIR != PAIR_NONE)
+      brow_l[nb] = (nb < 2 ? 0 : 64) + wn * 32 + (nb & 1) * 16;
+    else
+      brow_l[nb] = wn * 64 + nb * 16;
+  }
+
+  // four stages: st, st+1, st+2 in flight at the start of stage st (eight
+  // instructions each); two stages: only st
+  auto step = [&](int st, const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt)
+                  __attribute__((always_inline)) {
+    if (NS == 4 && st + 2 < nst)
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 0 | (1 << 14));  // vmcnt(16)
+    else if (NS == 4 && st + 1 < nst)
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 8);  // vmcnt(8)
+    else
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    // every wave's share of stage st is in LDS and every wave has finished
+    // stage st-1, whose buffer the next copy overwrites
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (st + NS - 1 < nst) issue(st + NS - 1, nxt);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      uint4 af[4], bf[4];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+        af[mb] = *reinterpret_cast<const uint4*>(cur + (wm * 64 + mb * 16) * DROWB + foff[kk]);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+        bf[nb] = *reinterpret_cast<const uint4*>(cur + (TBM + brow_l[nb]) * DROWB + foff[kk]);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) mfma_step(acc[mb][nb], af[mb], bf[nb], T());
+    }
+  };
+
+  if constexpr (NS == 4) {
+    if (nst > 0) issue(0, st0);
+    if (nst > 1) issue(1, st1);
+    if (nst > 2) issue(2, st2);
+    for (int st = 0; st < nst; st += 4) {
+      step(st, st0, st3);
+      if (st + 1 < nst) step(st + 1, st1, st0);
+      if (st + 2 < nst) step(st + 2, st2, st1);
+      if (st + 3 < nst) step(st + 3, st3, st2);
+    }
+  } else {
+    if (nst > 0) issue(0, st0);
+    for (int st = 0; st < nst; st += 2) {
+      step(st, st0, st1);
+      if (st + 1 < nst) step(st + 1, st1, st0);
+    }
+  }
+
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int grow = m0 + wm * 64 + mb * 16 + 4 * g + i;
+      if (grow >= p.M) continue;
+      if (PAIR != PAIR_NONE) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          const int gcol = n0 + wn * 32 + nb * 16 + r16;
+          epilogue_store<EPI, T>(p, z, split, grow, gcol, acc[mb][nb][i], acc[mb][nb + 2][i]);
+        }
+      } else {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+          const int gcol = n0 + wn * 64 + nb * 16 + r16;
+          if (gcol < p.N) epilogue_store<EPI, T>(p, z, split, grow, gcol, acc[mb][nb][i], 0.f);
+        }
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------------------
 // host side
 // --------------------------------------------------------------------------
 static int skinny_mb(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
@@ -594,7 +795,12 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
   constexpr int PAIR = EpiPair<EPI>::value;
   const int nx = PAIR == PAIR_NONE ? (a.N + TBN - 1) / TBN : a.N / (PAIR == PAIR_N ? 64 : 128);
   dim3 grid(nx, (a.M + TBM - 1) / TBM, a.batch * a.splits);
-  RFX_LAUNCH((gemm_tiled<T, EPI>), grid, dim3(256), 0, s, a);
+  if (sizeof(T) == 2 && a.K % DST == 0 && a.k_per_split % DST == 0) {
+    const int total = grid.x * grid.y * grid.z;
+    RFX_LAUNCH((gemm_dma<EPI, 2>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+  }
+  else
+    RFX_LAUNCH((gemm_tiled<T, EPI>), grid, dim3(256), 0, s, a);
 }
 
 template <typename T, int EPI>
