@@ -856,11 +856,11 @@ int attention_pick_splits(int B, int rows, int max_keys, int elem_bytes) {
   const int rbs = (rows + rpb - 1) / rpb;
   const int base = B * rbs;
   const int tiles = (max_keys + AKT - 1) / AKT + 1;
-  // one workgroup per CU is resident (register bound): aim for ~1 wave of
-  // workgroups over 256 CUs, at least two tiles per split
+  // one workgroup per CU is resident (LDS bound): aim for ~1 wave of
+  // workgroups over 256 CUs.  Down to one tile per split: at a few envs the
+  // latency of a tile's copy and math outweighs the larger merge.
   int s = 256 / base;
-  const int cap = (tiles + 1) / 2;
-  if (s > cap) s = cap;
+  if (s > tiles) s = tiles;
   if (s > kMaxSplits) s = kMaxSplits;
   return s < 1 ? 1 : s;
 }
