@@ -168,18 +168,24 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
     ys[c4] = ada4(ys[c4], r, ld4f(fmod + c), ld4f(fmod + p.D + c));
   }
   __syncthreads();
-  // v[a] = sum_c y[c] W[a][c]: wave w takes outputs a = w, w+4, ...; lanes stride the columns
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // v[a] = sum_c y[c] W[a][c]: eight threads per output, each a strided
+  // eighth of the columns, so the weight loads of a pass are independent and
+  // in flight together; the eight partial sums meet in three xor shuffles
   const T* W = reinterpret_cast<const T*>(p.w_aout);
-  for (int a = wave; a < p.da; a += 4) {
+  const int part = threadIdx.x & 7;
+  for (int a0 = 0; a0 < p.da; a0 += 32) {
+    const int a = a0 + (threadIdx.x >> 3);
+    const int ar = a < p.da ? a : p.da - 1;  // clamped row: a valid address, result unused
     float acc = 0.f;
-    for (int c4 = lane; c4 < D4; c4 += 64) {
-      const float4 w = ld4f(W + (int64_t)a * p.D + c4 * 4);
+    for (int c4 = part; c4 < D4; c4 += 8) {
+      const float4 w = ld4f(W + (int64_t)ar * p.D + c4 * 4);
       const float4 y = ys[c4];
       acc += w.x * y.x + w.y * y.y + w.z * y.z + w.w * y.w;
     }
-    acc = warp_sum(acc);
-    if (lane == 0) vpart[0][a] = acc;
+    acc += __shfl_xor(acc, 1, 64);
+    acc += __shfl_xor(acc, 2, 64);
+    acc += __shfl_xor(acc, 4, 64);
+    if (part == 0 && a < p.da) vpart[0][a] = acc;
   }
   __syncthreads();
   const int64_t xo = ((int64_t)b * H + i) * p.da;
