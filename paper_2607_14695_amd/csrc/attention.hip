@@ -807,27 +807,28 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
 }
 
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
-// splits combined in index order.  One thread per (query row, d).
+// splits combined in index order.  One thread per (query row, 4 consecutive d).
 constexpr int kMaxSplits = 16;
 
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
-  constexpr int RPB = 256 / DH;  // rows per block
+  constexpr int TPR = DH / 4;     // threads per row, four consecutive d each
+  constexpr int RPB = 256 / TPR;  // rows per block
   const int b = blockIdx.y;
-  const int rsub = threadIdx.x / DH, d = threadIdx.x % DH;
+  const int rsub = threadIdx.x / TPR, d = (threadIdx.x % TPR) * 4;
   const int rq = blockIdx.x * RPB + rsub;
   const int nrows = p.T * p.Hq;
   if (rq >= nrows) return;
   const int64_t base = (int64_t)b * p.nsplit * p.rows_pad + rq;
   // all loads of this thread are independent: one memory round trip
   float2 ml[kMaxSplits];
-  float ov[kMaxSplits];
+  float4 ov[kMaxSplits];
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s) {
     if (s < p.nsplit) {
       const int64_t prow = base + (int64_t)s * p.rows_pad;
       ml[s] = *reinterpret_cast<const float2*>(p.part_ml + prow * 2);
-      ov[s] = p.part_o[prow * DH + d];
+      ov[s] = *reinterpret_cast<const float4*>(p.part_o + prow * DH + d);
     }
   }
   float M = -INFINITY;
@@ -835,17 +836,28 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   for (int s = 0; s < kMaxSplits; ++s)
     if (s < p.nsplit) M = fmaxf(M, ml[s].x);
   const float Mu = (M == -INFINITY) ? 0.f : M;
-  float L = 0.f, acc = 0.f;
+  float L = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s)
     if (s < p.nsplit) {
       const float w = exp2f(ml[s].x - Mu);
       L += w * ml[s].y;
-      acc += w * ov[s];
+      acc.x += w * ov[s].x;
+      acc.y += w * ov[s].y;
+      acc.z += w * ov[s].z;
+      acc.w += w * ov[s].w;
     }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
   const int i = rq / p.Hq, j = rq % p.Hq;
   T* dst = reinterpret_cast<T*>(p.out) + ((int64_t)b * p.T + i) * (int64_t)(p.Hq * DH) + j * DH + d;
-  *dst = from_f<T>(L > 0.f ? acc / L : 0.f);
+  const float v[4] = {acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv};
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<uint2*>(dst) = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                                                (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+  } else {
+    *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+  }
 }
 
 // Query rows per attention workgroup: 128 on the bf16 (32x32 MFMA) path, 64 on fp32.
@@ -879,7 +891,7 @@ static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
 
 template <typename T, int DH>
 static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
-  constexpr int RPB = 256 / DH;
+  constexpr int RPB = 256 / (DH / 4);
   dim3 grid((a.T * a.Hq + RPB - 1) / RPB, a.B);
   RFX_LAUNCH((attn_merge_kernel<T, DH>), grid, dim3(256), 0, s, a);
 }
