@@ -76,6 +76,66 @@ def _class_bytes_flops(cfg):
     return out
 
 
+def _norm_bytes(cfg):
+    """Algorithmic bytes of one residual + AdaRMSNorm launch: read h and the
+    projection output, write h (fp32) and y (operand type), plus the gate,
+    scale and shift rows of every env."""
+    M = cfg.batch * (cfg.action_horizon + 1)
+    eb = 2 if cfg.bf16 else 4
+    return M * cfg.width * (4 + 4 + 4 + eb) + cfg.batch * 3 * cfg.width * 4
+
+
+def _ring_bytes(cfg, prof_w):
+    """(bytes, flops) of the ring writer's launches for one frame of all envs.
+    Direct path: pre-RoPE K/V in, RoPE'd K and V^T out.  Embedding path: the
+    frame projection GEMM (frame + per-layer Wk/Wv in, fp32 K/V scratch out)
+    and the ring kernel (scratch in, cache out)."""
+    eb = 2 if cfg.bf16 else 4
+    kv = cfg.batch * cfg.n_layers * 2 * cfg.frame_tokens * cfg.head_dim  # K and V elements
+    if cfg.frame_dim == 0:
+        return {"ring_write": (2 * kv * eb, 0.0)}
+    n = cfg.n_layers * 2 * cfg.head_dim
+    m = cfg.batch * cfg.frame_tokens
+    return {"frame_proj": (m * cfg.frame_dim * eb + n * cfg.frame_dim * eb + m * n * 4, 2.0 * m * n * cfg.frame_dim),
+            "ring_write": (kv * 4 + kv * eb, 0.0)}
+
+
+def _stream_ticks(eng, frames, state, noise, ticks, warmup, torch, period_s=0.020):
+    """Tick latency on a release grid: a tick is released every period_s; its
+    latency runs from the release to the action chunk synced on the device
+    (frame write + denoise).  A tick that would start after its release is
+    started at once (no queue builds up behind a slow tick: the next release
+    is the first grid point not already passed)."""
+    import numpy as np
+
+    for i in range(warmup):
+        eng.write_frame(frames[i % len(frames)])
+        eng.denoise(state, noise)
+    eng.synchronize()
+    torch.cuda.synchronize()
+    lat = []
+    t0 = time.perf_counter()
+    k = 0
+    for i in range(ticks):
+        release = t0 + k * period_s
+        now = time.perf_counter()
+        if now < release:
+            time.sleep(max(0.0, release - now - 0.0005))
+            while time.perf_counter() < release:
+                pass
+        eng.write_frame(frames[i % len(frames)])
+        eng.denoise(state, noise)
+        eng.synchronize()
+        torch.cuda.synchronize()
+        done = time.perf_counter()
+        lat.append(done - release)
+        k = int((done - t0) / period_s) + 1
+    a = np.array(lat) * 1e3
+    return {"period_ms": period_s * 1e3, "ticks": ticks, "p50_ms": round(float(np.percentile(a, 50)), 3),
+            "p99_ms": round(float(np.percentile(a, 99)), 3), "mean_ms": round(float(a.mean()), 3),
+            "misses": int((a > period_s * 1e3).sum())}
+
+
 def _time_ticks(eng, frames, state, noise, steps, warmup, torch, denoise_only=False):
     for i in range(warmup):
         if not denoise_only:
@@ -191,6 +251,10 @@ def main():
     log(f"tick {tick_s * 1e3:.3f} ms")
     chunk_s = _time_ticks(eng, frames, state, noise, args.steps, args.warmup, torch, denoise_only=True)
     log(f"chunk {chunk_s * 1e3:.3f} ms")
+    pw = eng.profile_write(frames[0])
+    rb = _ring_bytes(cfg, pw)
+    rw_ms, rw_n = pw["ring_write"]
+    ring_gbs = rb["ring_write"][0] / (rw_ms / rw_n / 1e3) / 1e9
     lat = None
     if not args.no_latency:
         lat = _chunk_latencies(eng, state, noise, max(20, args.steps), torch)
@@ -208,6 +272,8 @@ def main():
     attn_ms, attn_n = prof["attention"]
     attn_gbs = bf["attention"][0] / (attn_ms / attn_n / 1e3) / 1e9
     kernel_avg_us = {k: round(v[0] / v[1] * 1e3, 3) for k, v in prof.items() if v[1]}
+    n_ms, n_n = prof["resid_norm"]
+    norm_gbs = _norm_bytes(cfg) / (n_ms / n_n / 1e3) / 1e9
     eng.close()
     del eng, w
 
@@ -220,6 +286,8 @@ def main():
         t32 = _time_ticks(e32, fr32, st32, nz32, steps32, 2, torch)
         c32s = _time_ticks(e32, fr32, st32, nz32, steps32, 1, torch, denoise_only=True)
         p32 = e32.profile(st32, nz32)
+        pw32 = e32.profile_write(fr32[0])
+        rb32 = _ring_bytes(c32, pw32)
         bf32 = _class_bytes_flops(c32)
         a_ms, a_n = p32["attention"]
         b32 = {
@@ -235,8 +303,30 @@ def main():
         for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
             ms_k, n_k = p32[k]
             b32[f"{k}_mfma_tflops"] = round(bf32[k][1] / (ms_k / n_k / 1e3) / 1e12, 1)
+        fp_ms, fp_n = pw32["frame_proj"]
+        rw_ms32, rw_n32 = pw32["ring_write"]
+        b32["frame_proj_mfma_tflops"] = round(rb32["frame_proj"][1] / (fp_ms / fp_n / 1e3) / 1e12, 1)
+        b32["ring_write_gbs"] = round(rb32["ring_write"][0] / (rw_ms32 / rw_n32 / 1e3) / 1e9, 1)
+        b32["write_us"] = {k: round(v[0] / v[1] * 1e3, 3) for k, v in pw32.items() if v[1]}
+        n32_ms, n32_n = p32["resid_norm"]
+        b32["norm_gbs"] = round(_norm_bytes(c32) / (n32_ms / n32_n / 1e3) / 1e9, 1)
+        if not args.no_latency:
+            b32["stream_ticks"] = _stream_ticks(e32, fr32, st32, nz32, 30, 3, torch)
+            log(f"b32 stream ticks: {b32['stream_ticks']}")
         e32.close()
         log(f"b32 tick {t32 * 1e3:.3f} ms, chunk {c32s * 1e3:.3f} ms")
+
+    stream = None
+    if not args.no_latency:
+        cs = WL.CONFIGS["pi0_stream_bf16"]
+        ws_, sks, svs, frs, sts, nzs = _device_inputs(cs, torch, seed=2)
+        es = ReflexEngine(cs, ws_, sks, svs)
+        stream = _stream_ticks(es, frs, sts, nzs, 100, 5, torch)
+        stream["workload"] = ("pi0_stream_bf16: 1 env, 768-token frames of width 2048 through the per-layer Wk/Wv "
+                              "projection into a 2-frame ring, 10-step denoise per tick, ticks released every 20 ms")
+        log(f"stream ticks: {stream}")
+        es.close()
+        del es, ws_
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, log)
 
@@ -266,6 +356,10 @@ def main():
         "chunk_ms": round(chunk_s * 1e3, 4),
         "chunk_latency_ms": lat,
         "attn_hbm_gbs": round(attn_gbs, 1),
+        "norm_gbs": round(norm_gbs, 1),
+        "ring_write_gbs": round(ring_gbs, 1),
+        "ring_write_us": round(rw_ms / rw_n * 1e3, 3),
+        "stream_ticks": stream,
         "kernel_avg_us": kernel_avg_us,
         "roofline": {
             "kernel": dominant,

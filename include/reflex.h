@@ -243,12 +243,14 @@ int reflex_ring_plan(int64_t frames_written, int32_t window_frames, int32_t fram
 int64_t reflex_frames_written(const reflex_ctx* ctx);
 
 /*
- * Per-kernel-class device timing of the next denoise call (diagnostics).
- * When enabled, the next reflex_denoise_chunk runs its launches eagerly (no
- * graph) with hipEvents around each launch; reflex_profile_read then returns
- * the summed milliseconds and launch counts per class (the class names are
- * "embed_norm", "gemm_qkv", "attention", "attn_merge", "gemm_o", "resid_norm",
- * "gemm_gate_up", "gemm_down", "final_euler", "modulation", "rope_table").
+ * Per-kernel-class device timing (diagnostics).  While enabled, every
+ * reflex_denoise_chunk and reflex_cache_write_frame runs its launches eagerly
+ * (no graph) with hipEvents around each launch and synchronizes the context's
+ * stream before returning; reflex_profile_read then returns the summed
+ * milliseconds and launch counts per class of the last such call (the class
+ * names are "embed_norm", "gemm_qkv", "attention", "attn_merge", "gemm_o",
+ * "resid_norm", "gemm_gate_up", "gemm_down", "final_euler", "modulation",
+ * "rope_table", "frame_proj", "ring_write").
  * n_classes in/out: capacity of the arrays in, number written out.
  */
 int reflex_profile_enable(reflex_ctx* ctx, int enable);

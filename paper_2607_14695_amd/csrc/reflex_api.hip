@@ -27,11 +27,13 @@ namespace {
 thread_local char g_hip_err[256] = "";
 
 enum ProfClass {
-  PC_EMBED = 0, PC_QKV, PC_ATTN, PC_MERGE, PC_O, PC_RESID, PC_GU, PC_DOWN, PC_FINAL, PC_MOD, PC_ROPE, PC_N
+  PC_EMBED = 0, PC_QKV, PC_ATTN, PC_MERGE, PC_O, PC_RESID, PC_GU, PC_DOWN, PC_FINAL, PC_MOD, PC_ROPE, PC_FRAME_PROJ,
+  PC_RING, PC_N
 };
 const char* const kProfNames[PC_N] = {"embed_norm", "gemm_qkv",     "attention", "attn_merge",
                                       "gemm_o",     "resid_norm",   "gemm_gate_up", "gemm_down",
-                                      "final_euler", "modulation",  "rope_table"};
+                                      "final_euler", "modulation",  "rope_table",   "frame_proj",
+                                      "ring_write"};
 
 struct SplitK {
   int splits = 1;
@@ -387,12 +389,14 @@ int write_static(reflex_ctx* ctx, const void* sk, const void* sv) {
 }
 
 template <typename T>
-int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp) {
+int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool prof) {
   const reflex_config& c = ctx->cfg;
   const Plan& P = ctx->plan;
-  hipError_t e = launch_rope_table(ctx->ws.rope_frame, nullptr, stp.pos0, c.frame_tokens, c.head_dim,
-                                   c.rope_theta, ctx->stream);
-  if (e != hipSuccess) return hip_fail(e);
+  Launcher L{ctx, prof};
+  hipStream_t st = ctx->stream;
+  RFX_TRY(L.run(PC_ROPE, [&] {
+    return launch_rope_table(ctx->ws.rope_frame, nullptr, stp.pos0, c.frame_tokens, c.head_dim, c.rope_theta, st);
+  }));
   RingWriteArgs a{};
   const int dh = c.head_dim;
   a.rope = ctx->ws.rope_frame;
@@ -409,23 +413,40 @@ int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp)
     g.out = ctx->ws.frame_scratch; g.ldo = N;
     g.M = c.batch * c.frame_tokens; g.N = N; g.K = c.frame_dim;
     g.splits = 1; g.k_per_split = c.frame_dim + 128; g.batch = 1;
-    e = launch_gemm<T>(g, EPI_F32, ctx->stream);
-    if (e != hipSuccess) return hip_fail(e);
+    RFX_TRY(L.run(PC_FRAME_PROJ, [&] { return launch_gemm<T>(g, EPI_F32, st); }));
     a.src_k = ctx->ws.frame_scratch;
     a.src_v = ctx->ws.frame_scratch + dh;
     a.sb = (int64_t)c.frame_tokens * N;
     a.sl = 2 * dh;
     a.sj = N;
-    e = launch_ring_write<T, float>(a, dh, ctx->stream);
+    RFX_TRY(L.run(PC_RING, [&] { return launch_ring_write<T, float>(a, dh, st); }));
   } else {
     a.src_k = frame;
     a.src_v = (const char*)frame + (size_t)c.frame_tokens * dh * sizeof(T);
     a.sb = (int64_t)c.n_layers * 2 * c.frame_tokens * dh;
     a.sl = (int64_t)2 * c.frame_tokens * dh;
     a.sj = dh;
-    e = launch_ring_write<T, T>(a, dh, ctx->stream);
+    RFX_TRY(L.run(PC_RING, [&] { return launch_ring_write<T, T>(a, dh, st); }));
   }
-  return e == hipSuccess ? REFLEX_OK : hip_fail(e);
+  return REFLEX_OK;
+}
+
+// Sum the per-launch events of a profiled call into the per-class totals.
+int collect_profile(reflex_ctx* ctx) {
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  for (int i = 0; i < PC_N; ++i) {
+    ctx->prof_ms[i] = 0.0;
+    ctx->prof_launches[i] = 0;
+  }
+  for (auto& pe : ctx->ev_pending) {
+    float ms = 0.f;
+    (void)hipEventElapsedTime(&ms, pe.second.first, pe.second.second);
+    ctx->prof_ms[pe.first] += ms;
+    ctx->prof_launches[pe.first] += 1;
+  }
+  ctx->ev_pending.clear();
+  return REFLEX_OK;
 }
 
 }  // namespace
@@ -529,7 +550,11 @@ int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_
   reflex_ring_step stp;
   int rc = reflex_ring_plan(ctx->frames_written, c.window_frames, c.frame_tokens, c.static_len, &stp);
   if (rc != REFLEX_OK) return rc;
-  rc = c.dtype == REFLEX_DTYPE_BF16 ? write_frame<bf16_t>(ctx, frame, stp) : write_frame<float>(ctx, frame, stp);
+  const bool prof = ctx->prof_enabled != 0;
+  if (prof) ctx->ev_pending.clear();
+  rc = c.dtype == REFLEX_DTYPE_BF16 ? write_frame<bf16_t>(ctx, frame, stp, prof)
+                                    : write_frame<float>(ctx, frame, stp, prof);
+  if (rc == REFLEX_OK && prof) rc = collect_profile(ctx);
   if (rc != REFLEX_OK) return rc;
   ctx->frames_written += 1;
   if (frame_index_out) *frame_index_out = stp.frame_index;
@@ -550,20 +575,7 @@ int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise
     ctx->ev_pending.clear();
     int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, true);
     if (rc != REFLEX_OK) return rc;
-    hipError_t e = hipStreamSynchronize(ctx->stream);
-    if (e != hipSuccess) return hip_fail(e);
-    for (int i = 0; i < PC_N; ++i) {
-      ctx->prof_ms[i] = 0.0;
-      ctx->prof_launches[i] = 0;
-    }
-    for (auto& pe : ctx->ev_pending) {
-      float ms = 0.f;
-      (void)hipEventElapsedTime(&ms, pe.second.first, pe.second.second);
-      ctx->prof_ms[pe.first] += ms;
-      ctx->prof_launches[pe.first] += 1;
-    }
-    ctx->ev_pending.clear();
-    return REFLEX_OK;
+    return collect_profile(ctx);
   }
 
   GraphEntry* hit = nullptr;

@@ -303,13 +303,12 @@ class ReflexEngine:
         v = self.cache[half: half + n * esz].view(self.dtype).view(c.batch, c.n_layers, c.head_dim, R)
         return k, v
 
-    def profile(self, state, noise, num_steps: Optional[int] = None) -> Dict[str, Tuple[float, int]]:
-        """Run one denoise eagerly with per-launch events; {class: (ms, launches)}."""
+    def _profiled(self, call) -> Dict[str, Tuple[float, int]]:
         _check(self.lib.reflex_profile_enable(self.ctx, 1), "reflex_profile_enable")
         try:
-            self.denoise(state, noise, num_steps)
+            call()
             self.synchronize()
-            n = 16
+            n = 32
             names = (ctypes.c_char_p * n)()
             ms = (c_f64 * n)()
             cnt = (c_i32 * n)()
@@ -318,6 +317,14 @@ class ReflexEngine:
             return {names[i].decode(): (ms[i], cnt[i]) for i in range(nc.value)}
         finally:
             self.lib.reflex_profile_enable(self.ctx, 0)
+
+    def profile(self, state, noise, num_steps: Optional[int] = None) -> Dict[str, Tuple[float, int]]:
+        """Run one denoise eagerly with per-launch events; {class: (ms, launches)}."""
+        return self._profiled(lambda: self.denoise(state, noise, num_steps))
+
+    def profile_write(self, frame) -> Dict[str, Tuple[float, int]]:
+        """Write one frame eagerly with per-launch events; {class: (ms, launches)}."""
+        return self._profiled(lambda: self.write_frame(frame))
 
     def close(self):
         if self.ctx:
