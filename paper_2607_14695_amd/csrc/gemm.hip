@@ -78,6 +78,62 @@ RFX_DEV void epilogue_store(const GemmArgs& p, int z, int split, int row, int co
   }
 }
 
+// Store four consecutive outputs (columns col .. col+3, col a multiple of 4)
+// of one row; for paired epilogues u holds the four paired values.  Used by
+// the tiled kernel, whose transposed MFMA layout gives each lane four
+// consecutive columns of a row: 8- and 16-byte stores instead of scalars.
+template <int EPI>
+RFX_DEV void epilogue_store4(const GemmArgs& p, int z, int split, int row, int col, const float* v, const float* u) {
+  using T = bf16_t;
+  if constexpr (EPI == EPI_F32 || EPI == EPI_MOD) {
+    float w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      w[e] = v[e];
+      if (EPI == EPI_MOD && p.mod_width > 0 && col + e >= p.mod_width) w[e] = (col + e < 2 * p.mod_width) ? 0.f : 1.f;
+    }
+    float* o = reinterpret_cast<float*>(p.out) + (int64_t)z * p.o_bstride + (int64_t)split * p.o_split_stride +
+               (int64_t)row * p.ldo + col;
+    *reinterpret_cast<float4*>(o) = make_float4(w[0], w[1], w[2], w[3]);
+  } else if constexpr (EPI == EPI_SILU || EPI == EPI_GELU) {
+    float w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = EPI == EPI_SILU ? silu(v[e]) : gelu_tanh(v[e]) * u[e];
+    T* o = reinterpret_cast<T*>(p.out) + (int64_t)z * p.o_bstride + (int64_t)row * p.ldo + col;
+    *reinterpret_cast<uint2*>(o) = make_uint2((uint32_t)f2bf(w[0]) | ((uint32_t)f2bf(w[1]) << 16),
+                                              (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16));
+  } else {  // EPI_ROPE
+    const QkvOut& q = p.qkv;
+    const int dh = q.head_dim, half = dh >> 1;
+    const int head = col / dh, d = col - head * dh;  // d .. d+3 < half
+    const int b = row / q.T, i = row - b * q.T;
+    if (head <= q.Hq) {
+      const float4 c01 = *reinterpret_cast<const float4*>(q.rope + i * half + d);      // (cos, sin) of d, d+1
+      const float4 c23 = *reinterpret_cast<const float4*>(q.rope + i * half + d + 2);  // of d+2, d+3
+      const float cs[4] = {c01.x, c01.z, c23.x, c23.z}, sn[4] = {c01.y, c01.w, c23.y, c23.w};
+      float lo[4], hi[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo[e] = v[e] * cs[e] - u[e] * sn[e];
+        hi[e] = u[e] * cs[e] + v[e] * sn[e];
+      }
+      T* dst = head < q.Hq ? reinterpret_cast<T*>(q.q) + ((int64_t)b * q.rows_pad + i * q.Hq + head) * dh
+                           : reinterpret_cast<T*>(q.k) + ((int64_t)b * q.T + i) * dh;
+      *reinterpret_cast<uint2*>(dst + d) = make_uint2((uint32_t)f2bf(lo[0]) | ((uint32_t)f2bf(lo[1]) << 16),
+                                                      (uint32_t)f2bf(lo[2]) | ((uint32_t)f2bf(lo[3]) << 16));
+      *reinterpret_cast<uint2*>(dst + d + half) = make_uint2((uint32_t)f2bf(hi[0]) | ((uint32_t)f2bf(hi[1]) << 16),
+                                                             (uint32_t)f2bf(hi[2]) | ((uint32_t)f2bf(hi[3]) << 16));
+    } else {
+      T* dst = reinterpret_cast<T*>(q.vt) + (int64_t)b * dh * q.tpad;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dst[(int64_t)(d + e) * q.tpad + i] = f2bf(v[e]);
+        dst[(int64_t)(d + e + half) * q.tpad + i] = f2bf(u[e]);
+      }
+    }
+  }
+}
+
 // --------------------------------------------------------------------------
 // skinny: 16*MB rows per workgroup chunk, NB 16-col blocks per strip
 // --------------------------------------------------------------------------
@@ -661,7 +717,7 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) mfma_step(acc[mb][nb], af[mb], bf[nb], T());
+        for (int nb = 0; nb < 4; ++nb) mfma_step(acc[mb][nb], bf[nb], af[mb], T());  // C^T blocks
     }
   };
 
@@ -683,23 +739,31 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
     }
   }
 
+  // acc[mb][nb] holds the transposed 16x16 block: lane (r16, g) has output
+  // row m0 + wm*64 + mb*16 + r16, columns 4g .. 4g+3 of column block nb
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
+    const int grow = m0 + wm * 64 + mb * 16 + r16;
+    if (grow >= p.M) continue;
+    if (PAIR != PAIR_NONE) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int grow = m0 + wm * 64 + mb * 16 + 4 * g + i;
-      if (grow >= p.M) continue;
-      if (PAIR != PAIR_NONE) {
+      for (int nb = 0; nb < 2; ++nb) {
+        const int gcol = n0 + wn * 32 + nb * 16 + 4 * g;
+        const float v[4] = {acc[mb][nb][0], acc[mb][nb][1], acc[mb][nb][2], acc[mb][nb][3]};
+        const float u[4] = {acc[mb][nb + 2][0], acc[mb][nb + 2][1], acc[mb][nb + 2][2], acc[mb][nb + 2][3]};
+        epilogue_store4<EPI>(p, z, split, grow, gcol, v, u);
+      }
+    } else {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-          const int gcol = n0 + wn * 32 + nb * 16 + r16;
-          epilogue_store<EPI, T>(p, z, split, grow, gcol, acc[mb][nb][i], acc[mb][nb + 2][i]);
-        }
-      } else {
+      for (int nb = 0; nb < 4; ++nb) {
+        const int gcol = n0 + wn * 64 + nb * 16 + 4 * g;
+        const float v[4] = {acc[mb][nb][0], acc[mb][nb][1], acc[mb][nb][2], acc[mb][nb][3]};
+        if (gcol + 3 < p.N) {
+          epilogue_store4<EPI>(p, z, split, grow, gcol, v, v);
+        } else {
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) {
-          const int gcol = n0 + wn * 64 + nb * 16 + r16;
-          if (gcol < p.N) epilogue_store<EPI, T>(p, z, split, grow, gcol, acc[mb][nb][i], 0.f);
+          for (int e = 0; e < 4; ++e)
+            if (gcol + e < p.N) epilogue_store<EPI, T>(p, z, split, grow, gcol + e, v[e], 0.f);
         }
       }
     }
@@ -795,7 +859,8 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
   constexpr int PAIR = EpiPair<EPI>::value;
   const int nx = PAIR == PAIR_NONE ? (a.N + TBN - 1) / TBN : a.N / (PAIR == PAIR_N ? 64 : 128);
   dim3 grid(nx, (a.M + TBM - 1) / TBM, a.batch * a.splits);
-  if (sizeof(T) == 2 && a.K % DST == 0 && a.k_per_split % DST == 0) {
+  // (vector epilogue stores: output rows start 16-byte aligned)
+  if (sizeof(T) == 2 && a.K % DST == 0 && a.k_per_split % DST == 0 && a.N % 4 == 0 && a.ldo % 4 == 0) {
     const int total = grid.x * grid.y * grid.z;
     RFX_LAUNCH((gemm_dma<EPI, 2>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
   }
