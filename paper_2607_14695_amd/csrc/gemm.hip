@@ -601,7 +601,7 @@ RFX_DEV bool dma_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
   return true;
 }
 
-template <int EPI, int NS>
+template <int EPI, int NS, int NSTC>
 __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   using T = bf16_t;
   constexpr int PAIR = EpiPair<EPI>::value;
@@ -633,7 +633,11 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   }
   const int kbeg = split * p.k_per_split;
   const int kend = min(p.K, kbeg + p.k_per_split);
-  const int nst = (kend - kbeg) / DST;
+  // NSTC > 0: the stage count is a compile-time constant and the stage loop is
+  // fully unrolled, so the compiler tracks which LDS buffer every copy in
+  // flight targets (a loop would merge that knowledge at its header and make
+  // it wait for all copies there)
+  const int nst = NSTC > 0 ? NSTC : (kend - kbeg) / DST;
 
   const T* A = reinterpret_cast<const T*>(p.A) + (int64_t)z * p.a_bstride;
   const T* B = reinterpret_cast<const T*>(p.B) + (int64_t)z * p.b_bstride;
@@ -721,7 +725,15 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
     }
   };
 
-  if constexpr (NS == 4) {
+  if constexpr (NSTC > 0) {
+    static_assert(NS == 4, "unrolled pipeline uses four stages");
+    unsigned char* const bufs[4] = {st0, st1, st2, st3};
+    issue(0, bufs[0]);
+    if (NSTC > 1) issue(1, bufs[1]);
+    if (NSTC > 2) issue(2, bufs[2]);
+#pragma unroll
+    for (int st = 0; st < NSTC; ++st) step(st, bufs[st & 3], bufs[(st + 3) & 3]);
+  } else if constexpr (NS == 4) {
     if (nst > 0) issue(0, st0);
     if (nst > 1) issue(1, st1);
     if (nst > 2) issue(2, st2);
@@ -787,6 +799,14 @@ int gemm_pick_splits(int M, int N, int K, int elem_bytes) {
     return s < 1 ? 1 : (s > maxs ? maxs : s);
   }
   const int base = ((N + TBN - 1) / TBN) * ((M + TBM - 1) / TBM);
+  if (elem_bytes == 2) {
+    // bf16 tiled path: the largest power-of-two split that keeps one wave of
+    // workgroups (<= 256, one per CU for the four-stage pipeline) and at
+    // least 8 stages of 64 per split
+    int s = 1;
+    while (base * s * 2 <= 256 && K % (64 * s * 2) == 0 && K / (s * 2) >= 512) s *= 2;
+    return s;
+  }
   if (base >= 256 || K < 1024) return 1;
   int s = (256 + base - 1) / base;
   const int maxs = K / 512;
@@ -862,7 +882,19 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
   // (vector epilogue stores: output rows start 16-byte aligned)
   if (sizeof(T) == 2 && a.K % DST == 0 && a.k_per_split % DST == 0 && a.N % 4 == 0 && a.ldo % 4 == 0) {
     const int total = grid.x * grid.y * grid.z;
-    RFX_LAUNCH((gemm_dma<EPI, 2>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+    // four-stage unrolled pipeline (one workgroup per CU) when one wave of
+    // workgroups covers the grid; else the two-stage one (two per CU)
+    const int nst = a.k_per_split / DST;
+    if (total > 256) {
+      RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+    } else if (a.K == a.k_per_split * a.splits && nst == 8) {
+      RFX_LAUNCH((gemm_dma<EPI, 4, 8>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+    } else if (a.K == a.k_per_split * a.splits && nst == 16)
+      RFX_LAUNCH((gemm_dma<EPI, 4, 16>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+    else if (a.K == a.k_per_split * a.splits && nst == 32)
+      RFX_LAUNCH((gemm_dma<EPI, 4, 32>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+    else
+      RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
   }
   else
     RFX_LAUNCH((gemm_tiled<T, EPI>), grid, dim3(256), 0, s, a);
