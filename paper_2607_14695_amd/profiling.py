@@ -22,7 +22,7 @@ Usage::
 
     python -m paper_2607_14695_amd.profiling --stats KT_kernel_stats.csv \\
         --fetch FETCH_counter_collection.csv --write WRITE_counter_collection.csv \\
-        --kernel attn32_kernel --kernel-class attention --workload pi0_chunk_bf16 \\
+        --kernel "attn16_kernel<256>" --kernel-class attention --workload pi0_chunk_bf16 \\
         --command-kt "..." --command-fetch "..." --command-write "..." \\
         --out-md profiles/attention_pi0_chunk_bf16.md \\
         --out-json profiles/traffic_pi0_chunk_bf16.json
@@ -50,6 +50,7 @@ KERNEL_SOURCES: Dict[str, Tuple[str, ...]] = {
     "resid_norm": ("norm_ring.hip", "common.h", "kernels.h"),
     "embed_norm": ("norm_ring.hip", "common.h", "kernels.h"),
     "final_euler": ("norm_ring.hip", "common.h", "kernels.h"),
+    "all": ("attention.hip", "gemm.hip", "norm_ring.hip", "reflex_api.hip", "common.h", "kernels.h"),
 }
 
 COPY_BYTES = 256 << 20  # bytes read, and bytes written, by one calibration copy
@@ -106,7 +107,42 @@ def kernel_stats(path: str) -> List[dict]:
 
 def _short(name: str) -> str:
     name = re.sub(r"^void ", "", name)
-    return re.sub(r"\(.*\)$", "", name)
+    depth, cut = 0, len(name)
+    for i in range(len(name) - 1, -1, -1):  # strip the outermost trailing "( ... )"
+        if name[i] == ")":
+            depth += 1
+        elif name[i] == "(":
+            depth -= 1
+            if depth == 0:
+                cut = i
+                break
+    name = name[:cut] if name.endswith(")") else name
+    return name if len(name) <= 90 else name[:87] + "..."
+
+
+def dispatch_groups(trace_csv: str) -> List[dict]:
+    """Kernel-trace dispatches grouped by (kernel, grid size): the same kernel
+    launched for different workloads (batch sizes) keeps separate rows."""
+    groups: Dict[Tuple[str, str], List[float]] = {}
+    for r in _rows(trace_csv):
+        if r.get("Kind", "KERNEL_DISPATCH") != "KERNEL_DISPATCH":
+            continue
+        key = (r["Kernel_Name"], r["Grid_Size_X"])
+        groups.setdefault(key, []).append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
+    out = []
+    for (name, grid), d in groups.items():
+        out.append({"name": name, "grid": int(grid), "calls": len(d), "avg_ns": sum(d) / len(d),
+                    "min_ns": min(d), "max_ns": max(d), "total_ns": sum(d)})
+    out.sort(key=lambda x: -x["total_ns"])
+    return out
+
+
+def groups_markdown(groups: List[dict], command: str, limit: int = 24) -> str:
+    lines = ["| kernel | grid (threads) | calls | avg us | min us | max us |", "|---|---|---|---|---|---|"]
+    for d in groups[:limit]:
+        lines.append(f"| `{_short(d['name'])}` | {d['grid']} | {d['calls']} | {d['avg_ns'] / 1e3:.2f} | "
+                     f"{d['min_ns'] / 1e3:.2f} | {d['max_ns'] / 1e3:.2f} |")
+    return f"Command:\n\n```\n{command}\n```\n\n" + "\n".join(lines) + "\n"
 
 
 def stats_markdown(stats: List[dict], command: str, limit: int = 20) -> str:
@@ -130,6 +166,7 @@ def main(argv: Optional[List[str]] = None) -> None:
     ap.add_argument("--command-write", default="")
     ap.add_argument("--out-md", required=True)
     ap.add_argument("--out-json")
+    ap.add_argument("--trace", help="kernel-trace CSV: add a table grouped by (kernel, grid size)")
     args = ap.parse_args(argv)
 
     stats = kernel_stats(args.stats)
@@ -137,6 +174,8 @@ def main(argv: Optional[List[str]] = None) -> None:
     mine = [d for d in stats if pat.search(d["name"])]
     md = [f"# rocprofv3 summary: {args.kernel_class} on {args.workload}\n",
           "## Kernel trace statistics\n", stats_markdown(stats, args.command_kt)]
+    if args.trace:
+        md += ["## Dispatches grouped by kernel and grid size\n", groups_markdown(dispatch_groups(args.trace), args.command_kt)]
     rec = None
     if args.fetch and args.write:
         f_avg, f_n, f_copy = counter_per_dispatch(args.fetch, "FETCH_SIZE", args.kernel)
