@@ -268,27 +268,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
 }
 
 
-// ---------------------------------------------------------------------------
-// bf16 variant with 32x32x16 MFMAs and direct global->LDS tile loads.
-//
-// Each wave owns 32 query rows, a workgroup of 4 waves 128 rows, so every K/V
-// tile in LDS feeds 128 rows and each 16-byte LDS fragment feeds a 32x32 MFMA.
-// Tiles are written by global_load_lds_dwordx4 (CDNA4): no staging registers,
-// which leaves the register room the compiler needs to issue LDS fragment
-// reads ahead of the MFMAs.  Two LDS stages: tile t+1 streams in while tile t
-// is consumed.  The LDS layout is unpadded and XOR-swizzled on 16-byte
-// chunks (K: chunk ^ (row mod 8); V^T: chunk ^ ((d >> 1) mod 8)),
-// so the rows a lane group reads fall on distinct banks.  The DMA writes 1 KB
-// per wave instruction at consecutive LDS addresses, so the swizzle is
-// applied on the global side: each lane fetches the logical chunk that belongs
-// at its physical position.  Rows past the valid range are fetched from a
-// clamped valid address (finite data): their scores are masked to -inf and
-// their values meet zero probabilities, so they never contribute.
-//
-// S^T lane layout: key 8*(q >> 2) + 4*h + (q & 3) of a 32-key block, query
-// (lane & 31), h = lane >> 5; O^T holds d 8*(q >> 2) + 4*h + (q & 3) of a
-// 32-wide block for the same query.
-// ---------------------------------------------------------------------------
 // Workgroup barrier that orders LDS accesses only.  __syncthreads() also
 // releases global memory, which makes the compiler wait for every outstanding
 // vector-memory operation, including the LDS DMA of the next tile that is
@@ -297,247 +276,6 @@ RFX_DEV void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-template <int DH>
-__global__ __launch_bounds__(256) void attn32_kernel(AttnArgs p) {
-  using T = bf16_t;
-  constexpr int NKS = DH / 16;         // 16-wide d steps of S^T
-  constexpr int NDB = DH / 32;         // 32-wide d blocks of O^T
-  constexpr int KRB = DH * 2;          // bytes per K row in LDS
-  constexpr int KCH = DH / 8;          // 16-byte chunks per K row
-  constexpr int VRB = AKT * 2;         // bytes per V^T row (128)
-  constexpr int KBYTES = AKT * KRB;    // K tile bytes
-  constexpr int VBYTES = DH * VRB;     // V^T tile bytes
-  constexpr int STAGE = KBYTES + VBYTES;
-  constexpr int NIK = KBYTES / 1024 / 4;  // 1-KB DMA instructions per wave, K
-  constexpr int NIV = VBYTES / 1024 / 4;  // same for V^T
-  // two stages as distinct LDS objects: the compiler can then tell the DMA
-  // into one stage from the reads of the other and keep the DMA in flight
-  __shared__ __attribute__((aligned(16))) unsigned char stage0[STAGE];
-  __shared__ __attribute__((aligned(16))) unsigned char stage1[STAGE];
-
-  int group, rb;
-  if (!attn_decode(blockIdx.x, p.B * p.nsplit, p.rows_pad / 128, group, rb)) return;
-  const int b = group / p.nsplit, split = group - b * p.nsplit;
-
-  // the wave index is uniform: keep it (and the offsets built on it) scalar
-  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int r32 = lane & 31, h = lane >> 5;
-  const int T_ = p.T, Hq = p.Hq;
-  const int nrows = T_ * Hq;
-  const int rq = rb * 128 + wave * 32 + r32;
-  const bool qvalid = rq < nrows;
-  const int iq = qvalid ? rq / Hq : 0;
-  const int jq = qvalid ? rq % Hq : 0;
-  const int64_t mrow0 = (int64_t)b * T_;
-
-  uint4 qf[NKS];
-  {
-    const T* qrow = reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + (qvalid ? rq : 0)) * DH + h * 8;
-    // rows past the valid range compute on row 0's data and are never stored
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[ks] = ld16(qrow + ks * 16);
-  }
-
-  const int Lc = p.static_len + (*p.n_valid) * p.frame_tokens;
-  const int n_ct = (Lc + AKT - 1) / AKT;
-  const int n_dt = (T_ + AKT - 1) / AKT;
-  const int total = n_ct + n_dt;
-  const int per = (total + p.nsplit - 1) / p.nsplit;
-  const int t_beg = split * per;
-  const int t_end = min(total, t_beg + per);
-
-  const T* ck = reinterpret_cast<const T*>(p.cache_k) + (int64_t)b * p.ck_bstride;
-  const T* cvt = reinterpret_cast<const T*>(p.cache_vt) + (int64_t)b * p.ck_bstride;
-  const T* kdb = reinterpret_cast<const T*>(p.kd) + (int64_t)b * T_ * DH;
-  const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
-  const float scale = rsqrtf((float)DH) * 1.4426950408889634f;
-
-  // issue the DMA of tile t into stage sk (NIK + NIV instructions per wave).
-  // The per-lane offsets are rebuilt from an opaque copy of the lane id on
-  // every call: hoisted out of the tile loop they would pin ~40 registers.
-  const int tpad = p.tpad, Rrow = p.R;  // copied: a lambda must not capture the kernel argument
-  constexpr int RPI = 64 / KCH;  // K rows per DMA instruction
-  auto issue = [&](int t, unsigned char* sk) __attribute__((always_inline)) {
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
-    const bool dyn = t >= n_ct;
-    const int base = dyn ? (t - n_ct) * AKT : t * AKT;
-    const int last = (dyn ? T_ : Lc) - 1;
-    unsigned char* sv = sk + KBYTES;
-    const int kl = ln % KCH, kr = ln / KCH;
-    const int vd = ln >> 3, vc = ln & 7;
-    if (dyn) {
-#pragma unroll
-      for (int j = 0; j < NIK; ++j) {
-        const int row = RPI * (wave * NIK + j) + kr;
-        const int r = min(base + row, last);
-        __builtin_amdgcn_global_load_lds(kdb + r * DH + (kl ^ (row & 7)) * 8, sk + (wave * NIK + j) * 1024,
-                                         16, 0, 0);
-      }
-#pragma unroll
-      for (int j = 0; j < NIV; ++j) {
-        const int d = (wave * NIV + j) * 8 + vd;
-        __builtin_amdgcn_global_load_lds(vdb + d * tpad + base + (vc ^ ((d >> 1) & 7)) * 8,
-                                         sv + (wave * NIV + j) * 1024, 16, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < NIK; ++j) {
-        const int row = RPI * (wave * NIK + j) + kr;
-        const int r = min(base + row, last);
-        __builtin_amdgcn_global_load_lds(ck + (int64_t)r * DH + (kl ^ (row & 7)) * 8,
-                                         sk + (wave * NIK + j) * 1024, 16, 0, 0);
-      }
-#pragma unroll
-      for (int j = 0; j < NIV; ++j) {
-        const int d = (wave * NIV + j) * 8 + vd;
-        const int key = base + (vc ^ ((d >> 1) & 7)) * 8;
-        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + (key <= last ? key : 0),
-                                         sv + (wave * NIV + j) * 1024, 16, 0, 0);
-      }
-    }
-  };
-
-  f32x16_v o[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db)
-#pragma unroll
-    for (int q = 0; q < 16; ++q) o[db][q] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-
-  int koff[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) koff[j] = ((2 * j) ^ (h ^ (r32 & 7))) * 16;
-  auto step = [&](int t, const unsigned char* cur, unsigned char* nxt) __attribute__((always_inline)) {
-      const bool dyn = t >= n_ct;
-      // tile t's DMA (the only one outstanding) completes, then every wave's
-      // part is visible after the barrier; tile t+1 streams in during the math
-      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
-      lds_barrier();
-      if (t + 1 < t_end) issue(t + 1, nxt);
-      const unsigned char* sk = cur;
-      const unsigned char* sv = sk + KBYTES;
-      const unsigned char* krd = sk + r32 * KRB;
-
-      // S^T = K Q^T, two 32-key blocks
-      f32x16_v s[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) s[kb][q] = 0.f;
-      // fragments are read in batches ahead of their MFMAs so the LDS latency
-      // overlaps the matrix work
-      // chunk 2ks + h of row kb*32 + r32 sits at 2ks ^ (h ^ (r32 & 7)): the
-      // per-lane part takes 4 values (ks mod 4), the rest is an immediate
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int k0 = 0; k0 < NKS; k0 += 8) {
-          uint4 a[8];
-#pragma unroll
-          for (int u = 0; u < 8 && k0 + u < NKS; ++u) {
-            const int ks = k0 + u;
-            a[u] = *reinterpret_cast<const uint4*>(krd + kb * 32 * KRB + (ks >> 2) * 128 + koff[ks & 3]);
-          }
-#pragma unroll
-          for (int u = 0; u < 8 && k0 + u < NKS; ++u) mfma32_step(s[kb], a[u], qf[k0 + u]);
-        }
-      }
-      // key kidx of the tile is visible iff kidx < lim: the cached rows below
-      // Lc; among the dynamic rows the state row (iq == 0) sees only key 0
-      const int lim = (dyn ? (iq > 0 ? T_ : 1) - (t - n_ct) * AKT : Lc - t * AKT) - 4 * h;
-      float mt = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int kc = kb * 32 + 8 * (q >> 2) + (q & 3);  // key index minus 4h
-          const float v = kc < lim ? s[kb][q] * scale : -INFINITY;
-          s[kb][q] = v;
-          mt = fmaxf(mt, v);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      // lazy rescaling: the running max only moves when some row's tile max
-      // exceeds it by more than 8 (log2 units), so the probabilities stay
-      // below 2^8 and the O rescale (accumulator round trip) is rare
-      if (__any(mt > m_run + 8.f)) {
-        const float m_new = fmaxf(m_run, mt);
-        const float corr = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
-        l_run *= corr;
-        m_run = m_new;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) o[db] *= corr;
-      }
-      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-      float psum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const float e = exp2f(s[kb][q] - m_use);
-          s[kb][q] = e;
-          psum += e;
-        }
-      psum += __shfl_xor(psum, 32, 64);
-      l_run += psum;
-
-      // O^T += V^T P^T in 16-key steps: step ps uses keys {16ps + 4h + [0,4)} and
-      // {16ps + 8 + 4h + [0,4)} of lane group h, i.e. s[ps >> 1][8*(ps & 1) + [0,8)]
-#pragma unroll
-      for (int ps = 0; ps < 4; ++ps) {
-        float pv[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pv[i] = s[ps >> 1][8 * (ps & 1) + i];
-        const uint4 pf = f_to_frag(pv, T());
-        uint4 vf[NDB];
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const int d = db * 32 + r32;
-          const int sw = (d >> 1) & 7;
-          const unsigned char* vr = sv + d * VRB + h * 8;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vr + ((2 * ps) ^ sw) * 16);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vr + ((2 * ps + 1) ^ sw) * 16);
-          vf[db] = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        }
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) mfma32_step(o[db], vf[db], pf);
-      }
-      lds_barrier();  // this stage is refilled two tiles later
-  };
-
-  if (t_beg < t_end) issue(t_beg, stage0);
-  for (int t = t_beg; t < t_end; t += 2) {
-    step(t, stage0, stage1);
-    if (t + 1 < t_end) step(t + 1, stage1, stage0);
-  }
-
-  if (!qvalid) return;
-  if (p.nsplit == 1) {
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    T* dst = reinterpret_cast<T*>(p.out) + (mrow0 + iq) * (int64_t)(Hq * DH) + jq * DH;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int d = db * 32 + 8 * j + 4 * h;
-        uint2 w;
-        w.x = (uint32_t)f2bf(o[db][4 * j] * inv) | ((uint32_t)f2bf(o[db][4 * j + 1] * inv) << 16);
-        w.y = (uint32_t)f2bf(o[db][4 * j + 2] * inv) | ((uint32_t)f2bf(o[db][4 * j + 3] * inv) << 16);
-        *reinterpret_cast<uint2*>(dst + d) = w;
-      }
-    return;
-  }
-  const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq;
-  float* dst = p.part_o + prow * DH;
-#pragma unroll
-  for (int db = 0; db < NDB; ++db)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<float4*>(dst + db * 32 + 8 * j + 4 * h) =
-          make_float4(o[db][4 * j], o[db][4 * j + 1], o[db][4 * j + 2], o[db][4 * j + 3]);
-  if (h == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
 }
 
 // ---------------------------------------------------------------------------
@@ -724,7 +462,9 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
       __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     }
 
-    // block kb = 2j + e holds keys 32j + 8g + 4e + i; visible iff below lim
+    // block kb = 2j + e holds keys 32j + 8g + 4e + i; visible iff below lim:
+    // the cached rows below Lc; among the dynamic rows the state row (iq == 0)
+    // sees only key 0
     const int lim = (dyn ? (iq > 0 ? T_ : 1) - (t - n_ct) * AKT : Lc - t * AKT) - 8 * g;
     float mt = -INFINITY;
 #pragma unroll
@@ -737,7 +477,9 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
       }
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    // lazy rescaling (see attn32_kernel): probabilities stay below 2^8
+    // lazy rescaling: the running max only moves when some row's tile max
+    // exceeds it by more than 8 (log2 units), so the probabilities stay below
+    // 2^8 and the O rescale is rare
     if (__any(mt > m_run + 8.f)) {
       const float m_new = fmaxf(m_run, mt);
       const float corr = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
@@ -860,7 +602,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   }
 }
 
-// Query rows per attention workgroup: 128 on the bf16 (32x32 MFMA) path, 64 on fp32.
+// Query rows per attention workgroup: 128 on the bf16 path, 64 on fp32.
 int attention_rows_per_block(int elem_bytes) { return elem_bytes == 2 ? 128 : 64; }
 
 int attention_pick_splits(int B, int rows, int max_keys, int elem_bytes) {
