@@ -206,6 +206,31 @@ def test_ragged_bf16(head_dim, frame_dim):
     eng.close()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_limits_t64_no_static_prefix(dtype):
+    """Boundary shapes: 63 actions (T = 64, a full dynamic tile and T*Hq = 192
+    query rows), no static prefix (the cached keys are ring rows only),
+    state and action widths of 64, a 5-slot ring of 8-token frames."""
+    cfg = RAGGED.replace(name=f"limits_{dtype}", dtype=dtype, batch=2, static_len=0, frame_tokens=8,
+                         window_frames=5, action_horizon=63, action_dim=64, state_dim=64, n_q_heads=3,
+                         head_dim=64, width=128, mlp_dim=128, cond_hidden=64, frame_dim=0, num_steps=2)
+    w, sk, sv, frames = _setup(cfg, 7)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(7):
+        eng.write_frame(frames[t])
+        if t in (0, 6):
+            state, noise = WL.make_state(cfg, t), WL.make_noise(cfg, t)
+            got = eng.denoise(state, noise).cpu().numpy()
+            eng.synchronize()
+            ref = O.denoise_chunk(cfg, w, sk, sv, frames, t + 1, state, noise, cfg.taus())
+            if dtype == "f32":
+                assert np.max(np.abs(got - ref)) <= FP32_TOL, t
+            else:
+                rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+                assert rel <= BF16_REL and float(np.max(np.abs(got - ref))) <= BF16_ABS, (t, rel)
+    eng.close()
+
+
 def test_dtype_probe_rejects_mismatch(tiny):
     cfg, w, sk, sv, frames = tiny
     with pytest.raises(R.ReflexError) as ei:
