@@ -170,6 +170,31 @@ def _chunk_latencies(eng, state, noise, n, torch):
             "p95": round(float(np.percentile(ms, 95)), 4), "p99": round(float(np.percentile(ms, 99)), 4), "n": n}
 
 
+def _mode_chunks(eng, state, noise, torch, n):
+    """Device time per chunk (ms, mean of n back-to-back chunks between two
+    events on the engine's stream) under each cache strategy, once the ring is
+    full, plus how far the naive strategy's actions land from the method's."""
+    out, acts = {}, {}
+    for mode in ("reflex", "standard", "naive"):
+        acts[mode] = eng.denoise(state, noise, mode=mode).clone()  # captures the graph
+        eng.denoise(state, noise, mode=mode)
+        eng.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(eng.stream)
+        for _ in range(n):
+            eng.denoise(state, noise, mode=mode)
+        b.record(eng.stream)
+        eng.synchronize()
+        out[f"{mode}_chunk_ms"] = round(a.elapsed_time(b) / n, 4)
+    out["standard_over_reflex"] = round(out["standard_chunk_ms"] / out["reflex_chunk_ms"], 3)
+    out["standard_equals_reflex"] = bool(torch.equal(acts["reflex"], acts["standard"]))
+    d = (acts["naive"] - acts["reflex"]).double()
+    out["naive_vs_reflex_mse"] = float((d * d).mean())
+    out["naive_vs_reflex_maxabs"] = float(d.abs().max())
+    out["chunks_timed"] = n
+    return out
+
+
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
     10 Euler steps, one frame in the window), median of two runs."""
@@ -216,6 +241,8 @@ def main():
     ap.add_argument("--no-b32", action="store_true")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the per-chunk event-timed latency distribution (for counter-collection runs)")
+    ap.add_argument("--no-baselines", action="store_true",
+                    help="skip the Standard / Naive-cache strategy timings")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -313,18 +340,33 @@ def main():
         if not args.no_latency:
             b32["stream_ticks"] = _stream_ticks(e32, fr32, st32, nz32, 30, 3, torch)
             log(f"b32 stream ticks: {b32['stream_ticks']}")
+        if not args.no_baselines:
+            b32["strategies"] = _mode_chunks(e32, st32, nz32, torch, 3)
+            log(f"b32 strategies: {b32['strategies']}")
         e32.close()
         log(f"b32 tick {t32 * 1e3:.3f} ms, chunk {c32s * 1e3:.3f} ms")
 
-    stream = None
-    if not args.no_latency:
+    stream = strategies = None
+    if not (args.no_latency and args.no_baselines):
         cs = WL.CONFIGS["pi0_stream_bf16"]
         ws_, sks, svs, frs, sts, nzs = _device_inputs(cs, torch, seed=2)
         es = ReflexEngine(cs, ws_, sks, svs)
-        stream = _stream_ticks(es, frs, sts, nzs, 100, 5, torch)
-        stream["workload"] = ("pi0_stream_bf16: 1 env, 768-token frames of width 2048 through the per-layer Wk/Wv "
-                              "projection into a 2-frame ring, 10-step denoise per tick, ticks released every 20 ms")
-        log(f"stream ticks: {stream}")
+        if not args.no_latency:
+            stream = _stream_ticks(es, frs, sts, nzs, 100, 5, torch)
+            stream["workload"] = ("pi0_stream_bf16: 1 env, 768-token frames of width 2048 through the per-layer "
+                                  "Wk/Wv projection into a 2-frame ring, 10-step denoise per tick, ticks released "
+                                  "every 20 ms")
+            log(f"stream ticks: {stream}")
+        if not args.no_baselines:
+            while es.frames_written() < cs.window_frames:
+                es.write_frame(frs[es.frames_written() % len(frs)])
+            strategies = _mode_chunks(es, sts, nzs, torch, 20)
+            strategies["workload"] = ("pi0_stream_bf16 chunk with a full 2-frame ring: Standard re-encodes the 48 "
+                                      "static tokens and both 768-token frames (Wk/Wv projection + RoPE) before "
+                                      "every Euler step; Naive reuses the first step's dynamic K/V")
+            pst = es.profile(sts, nzs, mode="standard")
+            strategies["standard_class_ms"] = {k: round(v[0], 4) for k, v in pst.items() if v[1]}
+            log(f"strategies: {strategies}")
         es.close()
         del es, ws_
 
@@ -360,6 +402,7 @@ def main():
         "ring_write_gbs": round(ring_gbs, 1),
         "ring_write_us": round(rw_ms / rw_n * 1e3, 3),
         "stream_ticks": stream,
+        "strategies": strategies,
         "kernel_avg_us": kernel_avg_us,
         "roofline": {
             "kernel": dominant,

@@ -222,6 +222,47 @@ int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_
 int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
                          const float* tau_schedule, float* actions_out);
 
+/* Cache strategies of the comparison in Section 4 (Baselines) and the
+ * partitioned-attention ablation table of Section 4.6. */
+#define REFLEX_MODE_REFLEX 0   /* the method: cached regions read, dynamic K/V fresh at every step */
+#define REFLEX_MODE_STANDARD 1 /* full history recomputation: before every Euler step the static
+                                  prefix and every window frame are encoded into the cache again */
+#define REFLEX_MODE_NAIVE 2    /* a K/V cache that ignores the timestep: the dynamic K/V computed at
+                                  the first Euler step are reused at every later step */
+
+/* Sources the Standard strategy re-encodes at every step. */
+typedef struct reflex_sources {
+  const void* static_k;       /* device, as given to reflex_cache_init (may be NULL if static_len == 0) */
+  const void* static_v;
+  const void* const* frames;  /* host array of n_frames device pointers, each laid out as the frame
+                                 argument of reflex_cache_write_frame, oldest first: frames[i] is frame
+                                 number frames_written - n_frames + i */
+  int32_t n_frames;           /* must equal n_valid = min(frames_written, window_frames) */
+  int32_t reserved;
+} reflex_sources;
+
+/*
+ * reflex_denoise_chunk under a chosen cache strategy, for the comparisons of
+ * Section 4: the full-recomputation "Standard" baseline and the "Naive Cache"
+ * negative control.  Arguments as reflex_denoise_chunk, plus:
+ *   mode: REFLEX_MODE_REFLEX (identical to reflex_denoise_chunk),
+ *         REFLEX_MODE_STANDARD or REFLEX_MODE_NAIVE;
+ *   src:  required for REFLEX_MODE_STANDARD, ignored otherwise (may be NULL).
+ *         The frame and static buffers are read by the device work of this
+ *         call and must stay unchanged until it completes.
+ * Standard re-writes every window frame into its own slot at its own absolute
+ * positions and the static prefix at positions 0..static_len-1 before each
+ * step, with the same kernels as reflex_cache_write_frame; the cache bytes
+ * therefore end up unchanged and the actions equal those of the method.  The
+ * graph of a Standard call is also keyed by frames_written and the source
+ * pointers.  Naive keeps one set of dynamic K/V per layer in the workspace.
+ * Errors: REFLEX_EINVAL (unknown mode, missing or inconsistent sources, and as
+ * reflex_denoise_chunk), REFLEX_ESTATE, REFLEX_EHIP.
+ */
+int reflex_denoise_chunk_baseline(reflex_ctx* ctx, int32_t mode, const reflex_sources* src,
+                                  const float* state, const float* noise, int32_t num_steps,
+                                  const float* tau_schedule, float* actions_out);
+
 /* Release the host context and its captured graphs; never frees caller
  * memory.  NULL is a no-op.  Returns 0. */
 int reflex_destroy(reflex_ctx* ctx);

@@ -449,8 +449,9 @@ def denoise_chunk_partitioned(cfg, weights, cache: PartitionedCache, state_env: 
                               naive_cache: bool = False, diag: Optional[dict] = None) -> np.ndarray:
     """One env's chunk through the simulated partitioned cache.
 
-    With ``naive_cache`` the dynamic K/V of the previous Euler step are reused
-    (a cache that ignores the timestep), the negative control of Section 4.6.
+    With ``naive_cache`` the dynamic K/V of the first Euler step are reused at
+    every later step (a cache whose key leaves out the timestep is filled at
+    the first step and hit afterwards), the negative control of Section 4.6.
     """
     T = cfg.action_horizon + 1
     pos = dyn_pos0(cfg, cache.frames_written) + np.arange(T)

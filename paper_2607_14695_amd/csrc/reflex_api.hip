@@ -46,6 +46,10 @@ struct GraphEntry {
   float* out;
   int steps;
   float taus[REFLEX_MAX_STEPS + 1];
+  int mode;
+  // Standard mode bakes the window's slots and positions into the graph
+  int64_t frames_written;
+  std::vector<const void*> srcs;
   hipGraphExec_t exec;
 };
 
@@ -68,15 +72,18 @@ struct Workspace {
   void* z;
   float* rparts;
   float* frame_scratch;
+  void* naive_k;   // [L][B][T][dh] dynamic K of the first Euler step (Naive mode)
+  void* naive_vt;  // [L][B][dh][tpad] dynamic V^T of the first Euler step (Naive mode)
 };
 
-constexpr int kWsParts = 18;
+constexpr int kWsParts = 20;
 
 struct Plan {
   int T, M, S, Nqkv, C, R, rows_pad, tpad, nrb, eb;
   SplitK o, down;
   int attn_splits;
   int max_parts;
+  size_t naive_k_stride, naive_vt_stride;  // per-layer bytes of the Naive-mode dynamic K/V
   size_t cache_bytes, ws_bytes;
   size_t off[kWsParts];
 };
@@ -166,6 +173,10 @@ Plan make_plan(const reflex_config* c) {
   sz[15] = (size_t)p.M * c->mlp_dim * eb;                                 // z
   sz[16] = (size_t)p.max_parts * p.M * D * sizeof(float);                 // rparts
   sz[17] = c->frame_dim > 0 ? B * c->frame_tokens * L * 2 * dh * sizeof(float) : 0;  // frame scratch
+  p.naive_k_stride = align256(sz[9]);
+  p.naive_vt_stride = align256(sz[10]);
+  sz[18] = L * p.naive_k_stride;                                          // naive_k
+  sz[19] = L * p.naive_vt_stride;                                         // naive_vt
   size_t off = 0;
   for (int i = 0; i < kWsParts; ++i) {
     p.off[i] = off;
@@ -240,8 +251,29 @@ struct Launcher {
   } while (0)
 
 template <typename T>
+int write_static(reflex_ctx* ctx, const void* sk, const void* sv, bool publish, Launcher& L);
+template <typename T>
+int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool publish, Launcher& L);
+
+// Standard mode (full history recomputation): the static prefix and every
+// window frame are encoded into their cache rows again, with the kernels and
+// positions of their first write, so the rows receive identical bytes.
+template <typename T>
+int reencode_history(reflex_ctx* ctx, const reflex_sources* src, Launcher& L) {
+  const reflex_config& c = ctx->cfg;
+  if (c.static_len > 0) RFX_TRY(write_static<T>(ctx, src->static_k, src->static_v, false, L));
+  for (int i = 0; i < src->n_frames; ++i) {
+    reflex_ring_step stp;
+    RFX_TRY(reflex_ring_plan(ctx->frames_written - src->n_frames + i, c.window_frames, c.frame_tokens,
+                             c.static_len, &stp));
+    RFX_TRY(write_frame<T>(ctx, src->frames[i], stp, false, L));
+  }
+  return REFLEX_OK;
+}
+
+template <typename T>
 int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
-                  float* out, bool prof) {
+                  float* out, bool prof, int mode, const reflex_sources* src) {
   const reflex_config& c = ctx->cfg;
   const Plan& P = ctx->plan;
   const Workspace& W = ctx->ws;
@@ -288,6 +320,7 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
 
   for (int k = 0; k < steps; ++k) {
     const float* x_in = (k == 0) ? noise : out;
+    if (mode == REFLEX_MODE_STANDARD) RFX_TRY(reencode_history<T>(ctx, src, L));
     EmbedArgs ea{x_in, state, ctx->w.w_state, ctx->w.w_ain, mod_at(0, k), W.h, W.y,
                  B, Tn, D, c.state_dim, c.action_dim, c.embed_scale, c.rms_eps};
     RFX_TRY(L.run(PC_EMBED, [&] { return launch_embed_norm<T>(ea, st); }));
@@ -296,11 +329,20 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
       q.A = W.y; q.lda = D;
       q.B = wqkv + (size_t)l * P.Nqkv * D * eb; q.ldb = D;
       q.M = M; q.N = P.Nqkv; q.K = D; q.splits = 1; q.k_per_split = D + 128; q.batch = 1;
-      q.qkv = QkvOut{W.rope_dyn, W.q, W.kd, W.vdt, Tn, Hq, dh, P.rows_pad, P.tpad};
+      // dynamic K/V read by the attention: this step's, or in Naive mode the
+      // first step's, kept per layer
+      void* kd = W.kd;
+      void* vdt = W.vdt;
+      if (mode == REFLEX_MODE_NAIVE) {
+        kd = (char*)W.naive_k + (size_t)l * P.naive_k_stride;
+        vdt = (char*)W.naive_vt + (size_t)l * P.naive_vt_stride;
+      }
+      const bool stale = mode == REFLEX_MODE_NAIVE && k > 0;
+      q.qkv = QkvOut{W.rope_dyn, W.q, stale ? W.kd : kd, stale ? W.vdt : vdt, Tn, Hq, dh, P.rows_pad, P.tpad};
       RFX_TRY(L.run(PC_QKV, [&] { return launch_gemm<T>(q, EPI_ROPE, st); }));
 
       AttnArgs aa{};
-      aa.q = W.q; aa.kd = W.kd; aa.vdt = W.vdt; aa.tpad = P.tpad;
+      aa.q = W.q; aa.kd = kd; aa.vdt = vdt; aa.tpad = P.tpad;
       aa.cache_k = (const char*)ctx->cache_k + (size_t)l * P.R * dh * eb;
       aa.cache_vt = (const char*)ctx->cache_vt + (size_t)l * P.R * dh * eb;
       aa.ck_bstride = (int64_t)c.n_layers * P.R * dh;
@@ -352,20 +394,23 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
 }
 
 int enqueue_chunk_dispatch(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
-                           float* out, bool prof) {
+                           float* out, bool prof, int mode, const reflex_sources* src) {
   if (ctx->cfg.dtype == REFLEX_DTYPE_BF16)
-    return enqueue_chunk<bf16_t>(ctx, state, noise, steps, taus, out, prof);
-  return enqueue_chunk<float>(ctx, state, noise, steps, taus, out, prof);
+    return enqueue_chunk<bf16_t>(ctx, state, noise, steps, taus, out, prof, mode, src);
+  return enqueue_chunk<float>(ctx, state, noise, steps, taus, out, prof, mode, src);
 }
 
+// publish: also set the device tick state to "no frame written" (the first
+// write at init); a Standard-mode re-encode leaves the tick state alone.
 template <typename T>
-int write_static(reflex_ctx* ctx, const void* sk, const void* sv) {
+int write_static(reflex_ctx* ctx, const void* sk, const void* sv, bool publish, Launcher& L) {
   const reflex_config& c = ctx->cfg;
   const Plan& P = ctx->plan;
   hipError_t e;
   if (c.static_len > 0) {
-    e = launch_rope_table(ctx->ws.rope_frame, nullptr, 0, c.static_len, c.head_dim, c.rope_theta, ctx->stream);
-    if (e != hipSuccess) return hip_fail(e);
+    RFX_TRY(L.run(PC_ROPE, [&] {
+      return launch_rope_table(ctx->ws.rope_frame, nullptr, 0, c.static_len, c.head_dim, c.rope_theta, ctx->stream);
+    }));
   }
   RingWriteArgs a{};
   a.src_k = sk; a.src_v = sv;
@@ -375,8 +420,9 @@ int write_static(reflex_ctx* ctx, const void* sk, const void* sv) {
   a.rope = ctx->ws.rope_frame;
   a.cache_k = ctx->cache_k; a.cache_vt = ctx->cache_vt;
   a.row0 = 0; a.n_tok = c.static_len; a.L = c.n_layers; a.B = c.batch; a.R = P.R;
-  a.tick = ctx->ws.tick; a.frames_written = 0; a.n_valid = 0; a.dyn_pos0 = c.static_len;
+  a.tick = publish ? ctx->ws.tick : nullptr; a.frames_written = 0; a.n_valid = 0; a.dyn_pos0 = c.static_len;
   if (c.static_len == 0) {
+    if (!publish) return REFLEX_OK;
     // still publish the tick state; a one-token dummy write is not needed, so
     // set it with a tiny copy instead
     int64_t host_tick[3] = {0, 0, (int64_t)c.static_len};
@@ -384,15 +430,15 @@ int write_static(reflex_ctx* ctx, const void* sk, const void* sv) {
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     return e == hipSuccess ? REFLEX_OK : hip_fail(e);
   }
-  e = launch_ring_write<T, T>(a, c.head_dim, ctx->stream);
-  return e == hipSuccess ? REFLEX_OK : hip_fail(e);
+  return L.run(PC_RING, [&] { return launch_ring_write<T, T>(a, c.head_dim, ctx->stream); });
 }
 
+// publish: advance the device tick state to this frame (a new frame); a
+// Standard-mode re-encode of an older frame leaves the tick state alone.
 template <typename T>
-int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool prof) {
+int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool publish, Launcher& L) {
   const reflex_config& c = ctx->cfg;
   const Plan& P = ctx->plan;
-  Launcher L{ctx, prof};
   hipStream_t st = ctx->stream;
   RFX_TRY(L.run(PC_ROPE, [&] {
     return launch_rope_table(ctx->ws.rope_frame, nullptr, stp.pos0, c.frame_tokens, c.head_dim, c.rope_theta, st);
@@ -403,7 +449,7 @@ int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp,
   a.cache_k = ctx->cache_k; a.cache_vt = ctx->cache_vt;
   a.row0 = c.static_len + stp.slot * c.frame_tokens;
   a.n_tok = c.frame_tokens; a.L = c.n_layers; a.B = c.batch; a.R = P.R;
-  a.tick = ctx->ws.tick; a.frames_written = stp.frame_index + 1; a.n_valid = stp.n_valid;
+  a.tick = publish ? ctx->ws.tick : nullptr; a.frames_written = stp.frame_index + 1; a.n_valid = stp.n_valid;
   a.dyn_pos0 = stp.dyn_pos0;
   if (c.frame_dim > 0) {
     const int N = c.n_layers * 2 * dh;
@@ -520,6 +566,8 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
   W.z = base + P.off[15];
   W.rparts = reinterpret_cast<float*>(base + P.off[16]);
   W.frame_scratch = reinterpret_cast<float*>(base + P.off[17]);
+  W.naive_k = base + P.off[18];
+  W.naive_vt = base + P.off[19];
   ctx->cache_k = cache_mem;
   ctx->cache_vt = reinterpret_cast<char*>(cache_mem) + P.cache_bytes / 2;
 
@@ -532,8 +580,11 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
     delete ctx;
     return hip_fail(e);
   }
-  rc = cfg->dtype == REFLEX_DTYPE_BF16 ? write_static<bf16_t>(ctx, static_k, static_v)
-                                        : write_static<float>(ctx, static_k, static_v);
+  {
+    Launcher L{ctx, false};
+    rc = cfg->dtype == REFLEX_DTYPE_BF16 ? write_static<bf16_t>(ctx, static_k, static_v, true, L)
+                                          : write_static<float>(ctx, static_k, static_v, true, L);
+  }
   if (rc != REFLEX_OK) {
     delete ctx;
     return rc;
@@ -552,8 +603,11 @@ int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_
   if (rc != REFLEX_OK) return rc;
   const bool prof = ctx->prof_enabled != 0;
   if (prof) ctx->ev_pending.clear();
-  rc = c.dtype == REFLEX_DTYPE_BF16 ? write_frame<bf16_t>(ctx, frame, stp, prof)
-                                    : write_frame<float>(ctx, frame, stp, prof);
+  {
+    Launcher L{ctx, prof};
+    rc = c.dtype == REFLEX_DTYPE_BF16 ? write_frame<bf16_t>(ctx, frame, stp, true, L)
+                                      : write_frame<float>(ctx, frame, stp, true, L);
+  }
   if (rc == REFLEX_OK && prof) rc = collect_profile(ctx);
   if (rc != REFLEX_OK) return rc;
   ctx->frames_written += 1;
@@ -562,18 +616,38 @@ int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_
   return REFLEX_OK;
 }
 
-int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
-                         const float* tau_schedule, float* actions_out) {
+}  // extern "C"
+
+namespace {
+
+int denoise_entry(reflex_ctx* ctx, int mode, const reflex_sources* src, const float* state, const float* noise,
+                  int32_t num_steps, const float* tau_schedule, float* actions_out) {
   if (!ctx || !ctx->alive) return REFLEX_ESTATE;
   if (!state || !noise || !actions_out) return REFLEX_EINVAL;
   if (num_steps < 1 || num_steps > ctx->cfg.max_steps) return REFLEX_EINVAL;
+  if (mode != REFLEX_MODE_REFLEX && mode != REFLEX_MODE_STANDARD && mode != REFLEX_MODE_NAIVE) return REFLEX_EINVAL;
+  std::vector<const void*> srcs;
+  if (mode == REFLEX_MODE_STANDARD) {
+    const reflex_config& c = ctx->cfg;
+    const int64_t n_valid = ctx->frames_written < c.window_frames ? ctx->frames_written : c.window_frames;
+    if (!src || src->n_frames != n_valid || (n_valid > 0 && !src->frames)) return REFLEX_EINVAL;
+    if (c.static_len > 0 && (!src->static_k || !src->static_v)) return REFLEX_EINVAL;
+    srcs.push_back(src->static_k);
+    srcs.push_back(src->static_v);
+    for (int i = 0; i < src->n_frames; ++i) {
+      if (!src->frames[i]) return REFLEX_EINVAL;
+      srcs.push_back(src->frames[i]);
+    }
+  } else {
+    src = nullptr;
+  }
   float taus[REFLEX_MAX_STEPS + 1];
   for (int k = 0; k <= num_steps; ++k)
     taus[k] = tau_schedule ? tau_schedule[k] : (float)(1.0 - (double)k / (double)num_steps);
 
   if (ctx->prof_enabled) {
     ctx->ev_pending.clear();
-    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, true);
+    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, true, mode, src);
     if (rc != REFLEX_OK) return rc;
     return collect_profile(ctx);
   }
@@ -581,7 +655,8 @@ int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise
   GraphEntry* hit = nullptr;
   for (auto& g : ctx->graphs) {
     if (g.state == state && g.noise == noise && g.out == actions_out && g.steps == num_steps &&
-        memcmp(g.taus, taus, sizeof(float) * (num_steps + 1)) == 0) {
+        g.mode == mode && memcmp(g.taus, taus, sizeof(float) * (num_steps + 1)) == 0 &&
+        (mode != REFLEX_MODE_STANDARD || (g.frames_written == ctx->frames_written && g.srcs == srcs))) {
       hit = &g;
       break;
     }
@@ -590,7 +665,7 @@ int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise
     hipGraph_t graph;
     hipError_t e = hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal);
     if (e != hipSuccess) return hip_fail(e);
-    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, false);
+    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, false, mode, src);
     e = hipStreamEndCapture(ctx->stream, &graph);
     if (rc != REFLEX_OK) {
       if (e == hipSuccess) (void)hipGraphDestroy(graph);
@@ -609,12 +684,30 @@ int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise
     ge.state = state; ge.noise = noise; ge.out = actions_out; ge.steps = num_steps;
     memset(ge.taus, 0, sizeof(ge.taus));
     memcpy(ge.taus, taus, sizeof(float) * (num_steps + 1));
+    ge.mode = mode;
+    ge.frames_written = ctx->frames_written;
+    ge.srcs = std::move(srcs);
     ge.exec = exec;
-    ctx->graphs.push_back(ge);
+    ctx->graphs.push_back(std::move(ge));
     hit = &ctx->graphs.back();
   }
   hipError_t e = hipGraphLaunch(hit->exec, ctx->stream);
   return e == hipSuccess ? REFLEX_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                         const float* tau_schedule, float* actions_out) {
+  return denoise_entry(ctx, REFLEX_MODE_REFLEX, nullptr, state, noise, num_steps, tau_schedule, actions_out);
+}
+
+int reflex_denoise_chunk_baseline(reflex_ctx* ctx, int32_t mode, const reflex_sources* src, const float* state,
+                                  const float* noise, int32_t num_steps, const float* tau_schedule,
+                                  float* actions_out) {
+  return denoise_entry(ctx, mode, src, state, noise, num_steps, tau_schedule, actions_out);
 }
 
 int reflex_destroy(reflex_ctx* ctx) {

@@ -7,6 +7,7 @@ raised.
 """
 from __future__ import annotations
 
+import collections
 import ctypes
 import os
 import re
@@ -30,6 +31,10 @@ DTYPE_BF16 = 1
 MOD_FULL = 0
 MOD_SCALE_ONLY = 1
 MAX_STEPS = 64
+MODE_REFLEX = 0
+MODE_STANDARD = 1
+MODE_NAIVE = 2
+MODES = {"reflex": MODE_REFLEX, "standard": MODE_STANDARD, "naive": MODE_NAIVE}
 
 c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 
@@ -61,6 +66,13 @@ class RingStepC(ctypes.Structure):
     ]
 
 
+class SourcesC(ctypes.Structure):
+    _fields_ = [
+        ("static_k", c_vp), ("static_v", c_vp), ("frames", ctypes.POINTER(c_vp)), ("n_frames", c_i32),
+        ("reserved", c_i32),
+    ]
+
+
 class ReflexError(RuntimeError):
     def __init__(self, status: int, what: str, text: str):
         super().__init__(f"{what} failed with status {status}: {text}")
@@ -85,6 +97,7 @@ def load_library() -> ctypes.CDLL:
         "reflex_cache_init": (c_i32, [P(ConfigC), P(WeightsC), c_vp, c_vp, c_vp, c_vp, c_vp, P(c_vp)]),
         "reflex_cache_write_frame": (c_i32, [c_vp, c_vp, P(c_i64), P(c_i32)]),
         "reflex_denoise_chunk": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp]),
+        "reflex_denoise_chunk_baseline": (c_i32, [c_vp, c_i32, P(SourcesC), c_vp, c_vp, c_i32, c_vp, c_vp]),
         "reflex_destroy": (c_i32, [c_vp]),
         "reflex_strerror": (ctypes.c_char_p, [c_i32]),
         "reflex_ring_plan": (c_i32, [c_i64, c_i32, c_i32, c_i32, P(RingStepC)]),
@@ -181,6 +194,9 @@ class ReflexEngine:
                 self.w[name] = self._dev(weights[name], weight_dtype_override)
             sk = self._dev(static_k)
             sv = self._dev(static_v)
+            # kept for the Standard strategy, which encodes them again at every step
+            self._static = (sk, sv)
+            self._window = collections.deque(maxlen=cfg.window_frames)
             self.cache_bytes, self.ws_bytes = query_sizes(cfg, self.max_steps)
             self.cache = torch.empty(self.cache_bytes, dtype=torch.uint8, device=self.device)
             self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
@@ -227,7 +243,7 @@ class ReflexEngine:
             fi, ev = c_i64(0), c_i32(0)
             _check(self.lib.reflex_cache_write_frame(self.ctx, f.data_ptr(), ctypes.byref(fi), ctypes.byref(ev)),
                    "reflex_cache_write_frame")
-            self._keep_frame = f  # alive until the stream has consumed it
+            self._window.append(f)  # the window's frames, for the Standard strategy
         caller.wait_stream(self.stream)
         return fi.value, ev.value
 
@@ -248,13 +264,20 @@ class ReflexEngine:
         return buf
 
     def denoise(self, state, noise, num_steps: Optional[int] = None, taus: Optional[Sequence[float]] = None,
-                out=None):
+                out=None, mode: str = "reflex"):
         """Denoise one chunk per env; returns the fp32 action tensor (device).
 
         Without ``out`` the result lands in a buffer owned by the engine that
         the next call overwrites.  The caller's current stream is ordered
-        after the denoise, so reading the result there is safe."""
+        after the denoise, so reading the result there is safe.
+
+        ``mode`` selects the cache strategy: "reflex" (the method), or the
+        comparison baselines "standard" (the static prefix and the window's
+        frames, as last passed to ``write_frame``, are encoded again before
+        every step) and "naive" (the first step's dynamic K/V are reused)."""
         torch = self.torch
+        if mode not in MODES:
+            raise ValueError(f"unknown mode {mode!r}")
         k = num_steps if num_steps is not None else self.cfg.num_steps
         if taus is None and self.cfg.tau_schedule is not None and k == self.cfg.num_steps:
             taus = self.cfg.taus()  # the workload's own schedule
@@ -274,11 +297,28 @@ class ReflexEngine:
                     raise ValueError("tau schedule needs num_steps + 1 entries")
                 self._keep_taus = tau_np
                 tau_arr = tau_np.ctypes.data
-            _check(self.lib.reflex_denoise_chunk(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr, out.data_ptr()),
-                   "reflex_denoise_chunk")
+            if mode == "reflex":
+                _check(self.lib.reflex_denoise_chunk(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr,
+                                                     out.data_ptr()), "reflex_denoise_chunk")
+            else:
+                src = self._sources() if mode == "standard" else None
+                _check(self.lib.reflex_denoise_chunk_baseline(self.ctx, MODES[mode], src, s.data_ptr(),
+                                                              n.data_ptr(), k, tau_arr, out.data_ptr()),
+                       "reflex_denoise_chunk_baseline")
             self._keep_io = (s, n, out)
         caller.wait_stream(self.stream)
         return out
+
+    def _sources(self):
+        sk, sv = self._static
+        frames = list(self._window)[-min(self.frames_written(), self.cfg.window_frames):] \
+            if self.frames_written() else []
+        arr = (c_vp * max(len(frames), 1))(*[f.data_ptr() for f in frames])
+        src = SourcesC(static_k=sk.data_ptr() if sk.numel() else None,
+                       static_v=sv.data_ptr() if sv.numel() else None,
+                       frames=ctypes.cast(arr, ctypes.POINTER(c_vp)), n_frames=len(frames))
+        self._keep_src = (arr, src)
+        return ctypes.byref(src)
 
     def synchronize(self):
         self.stream.synchronize()
@@ -318,9 +358,10 @@ class ReflexEngine:
         finally:
             self.lib.reflex_profile_enable(self.ctx, 0)
 
-    def profile(self, state, noise, num_steps: Optional[int] = None) -> Dict[str, Tuple[float, int]]:
+    def profile(self, state, noise, num_steps: Optional[int] = None,
+                mode: str = "reflex") -> Dict[str, Tuple[float, int]]:
         """Run one denoise eagerly with per-launch events; {class: (ms, launches)}."""
-        return self._profiled(lambda: self.denoise(state, noise, num_steps))
+        return self._profiled(lambda: self.denoise(state, noise, num_steps, mode=mode))
 
     def profile_write(self, frame) -> Dict[str, Tuple[float, int]]:
         """Write one frame eagerly with per-launch events; {class: (ms, launches)}."""
