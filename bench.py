@@ -195,6 +195,48 @@ def _mode_chunks(eng, state, noise, torch, n):
     return out
 
 
+def _pipeline(cfg, w, sk, sv, frames, state, noise, torch, ticks, warmup):
+    """Tick period of frame write + chunk, on a ring with a spare slot, with
+    both on one stream (sequential) and with the write on a second stream
+    (asynchronous pipeline; each chunk reads the frames written before the
+    tick's own frame, so it overlaps that frame's write).  Also the write and
+    the chunk alone."""
+    from paper_2607_14695_amd.reflex import ReflexEngine
+
+    eng = ReflexEngine(cfg.replace(spare_slot=1), w, sk, sv)
+
+    def run(kind, n):
+        for i in range(n):
+            fr = frames[i % len(frames)]
+            if kind == "pipelined":
+                eng.pipeline_write(fr)
+                eng.denoise(state, noise, n_frames=eng.frames_written() - 1)
+            elif kind == "sequential":
+                eng.write_frame(fr)
+                eng.denoise(state, noise)
+            elif kind == "write":
+                eng.write_frame(fr)
+            else:
+                eng.denoise(state, noise)
+
+    out = {}
+    for kind in ("sequential", "pipelined", "write", "chunk"):
+        run(kind, warmup)
+        eng.synchronize()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(kind, ticks)
+        eng.synchronize()
+        torch.cuda.synchronize()
+        out[f"{kind}_ms"] = round((time.perf_counter() - t0) / ticks * 1e3, 4)
+    out["pipelined_speedup"] = round(out["sequential_ms"] / out["pipelined_ms"], 4)
+    # share of the write's time taken off the tick by running it beside the chunk
+    out["write_hidden_fraction"] = round((out["sequential_ms"] - out["pipelined_ms"]) / out["write_ms"], 3)
+    out["ticks_timed"] = ticks
+    eng.close()
+    return out
+
+
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
     10 Euler steps, one frame in the window), median of two runs."""
@@ -243,6 +285,8 @@ def main():
                     help="skip the per-chunk event-timed latency distribution (for counter-collection runs)")
     ap.add_argument("--no-baselines", action="store_true",
                     help="skip the Standard / Naive-cache strategy timings")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the two-stream (asynchronous pipeline) tick timings")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -344,10 +388,13 @@ def main():
             b32["strategies"] = _mode_chunks(e32, st32, nz32, torch, 3)
             log(f"b32 strategies: {b32['strategies']}")
         e32.close()
+        if not args.no_pipeline:
+            b32["pipeline"] = _pipeline(c32, w32, sk32, sv32, fr32, st32, nz32, torch, 8, 2)
+            log(f"b32 pipeline: {b32['pipeline']}")
         log(f"b32 tick {t32 * 1e3:.3f} ms, chunk {c32s * 1e3:.3f} ms")
 
-    stream = strategies = None
-    if not (args.no_latency and args.no_baselines):
+    stream = strategies = pipeline = None
+    if not (args.no_latency and args.no_baselines and args.no_pipeline):
         cs = WL.CONFIGS["pi0_stream_bf16"]
         ws_, sks, svs, frs, sts, nzs = _device_inputs(cs, torch, seed=2)
         es = ReflexEngine(cs, ws_, sks, svs)
@@ -368,6 +415,12 @@ def main():
             strategies["standard_class_ms"] = {k: round(v[0], 4) for k, v in pst.items() if v[1]}
             log(f"strategies: {strategies}")
         es.close()
+        if not args.no_pipeline:
+            pipeline = _pipeline(cs, ws_, sks, svs, frs, sts, nzs, torch, 30, 3)
+            pipeline["workload"] = ("pi0_stream_bf16 tick on a ring with one spare slot: 768x2048 frame through the "
+                                    "per-layer Wk/Wv projection + 10-step chunk; pipelined = write on a second "
+                                    "stream, chunk over the frames before it")
+            log(f"pipeline: {pipeline}")
         del es, ws_
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, log)
@@ -403,6 +456,7 @@ def main():
         "ring_write_us": round(rw_ms / rw_n * 1e3, 3),
         "stream_ticks": stream,
         "strategies": strategies,
+        "pipeline": pipeline,
         "kernel_avg_us": kernel_avg_us,
         "roofline": {
             "kernel": dominant,

@@ -66,7 +66,10 @@ extern "C" {
  * of layer l), 2*n_layers (final norm before the action head).
  *
  * Cache: static_len prefix tokens; window_frames ring slots of frame_tokens
- * tokens.  frame_dim > 0: frames arrive as [frame_tokens, frame_dim]
+ * tokens, plus one spare slot when spare_slot = 1 (the pipelined ring of the
+ * reflex_pipeline_* calls: frame f then goes to slot f mod (window_frames + 1),
+ * and a chunk still sees exactly window_frames frames).
+ * frame_dim > 0: frames arrive as [frame_tokens, frame_dim]
  * embeddings and K/V come from the per-layer frame projection w_kv;
  * frame_dim == 0: frames arrive as pre-RoPE per-layer K/V.  batch independent
  * environments advance in lockstep and share the weights.
@@ -106,6 +109,8 @@ typedef struct reflex_config {
   double rope_theta;
   double temb_min_period;
   double temb_max_period;
+  int32_t spare_slot;  /* 0 or 1, see "Cache" above */
+  int32_t reserved;    /* must be 0 */
 } reflex_config;
 
 /*
@@ -159,14 +164,17 @@ typedef struct reflex_ctx reflex_ctx;
  * Bytes the caller must allocate for the cache and the workspace.  Pure host
  * function (no device calls).  Both buffers need 256-byte alignment.
  *
- * Cache layout (element type `dtype`), R = static_len + window_frames*frame_tokens:
+ * Cache layout (element type `dtype`), R = static_len + (window_frames + spare_slot)*frame_tokens:
  *   K at offset 0:           [batch][n_layers][R][head_dim]   RoPE applied
  *   V at offset K bytes:     [batch][n_layers][head_dim][R]   stored transposed
  * Rows [0, static_len) hold the static prefix; ring slot s holds rows
  * [static_len + s*frame_tokens, static_len + (s+1)*frame_tokens).
- * The first 24 bytes of the workspace hold the device tick state as three
- * int64 values {frames_written, n_valid, dyn_pos0} (read-only for callers);
- * the rest of the workspace is private scratch of the library.
+ * The first 32 bytes of the workspace hold the device tick state as four
+ * int64 values {frames_written, n_valid, dyn_pos0, hole_row} (read-only for
+ * callers): the frames, window length and dynamic position the next chunk
+ * uses, and the logical cached row from which the physical rows skip the
+ * spare slot (a value past the window means no skip).  The rest of the
+ * workspace is private scratch of the library.
  * Returns REFLEX_EINVAL for an unsupported config.
  */
 int reflex_query_sizes(const reflex_config* cfg, size_t* cache_bytes, size_t* workspace_bytes);
@@ -262,6 +270,44 @@ typedef struct reflex_sources {
 int reflex_denoise_chunk_baseline(reflex_ctx* ctx, int32_t mode, const reflex_sources* src,
                                   const float* state, const float* noise, int32_t num_steps,
                                   const float* tau_schedule, float* actions_out);
+
+/*
+ * Asynchronous pipeline (Section 3.3): a producer writes frames on a stream of
+ * its own while the context's stream denoises chunks over frames whose write
+ * has completed, so the two overlap on the GPU.  Both calls need a context
+ * created with cfg.spare_slot = 1: the ring then has window_frames + 1 slots
+ * and the frame being written never lands in a slot that an in-flight chunk
+ * reads.  Ordering between the two streams is done on the device with events;
+ * neither call blocks the host.
+ *
+ * reflex_pipeline_write_frame: reflex_cache_write_frame with the device work
+ * enqueued on writer_stream (a hipStream_t; may be the context's stream).  On
+ * the device it first waits for the previous frame write and for every chunk,
+ * enqueued earlier, whose window contains the frame in the target slot.  It
+ * does not change the frames a chunk sees: each chunk picks its window.
+ * The frame buffer must stay unchanged until the write has completed.
+ *
+ * reflex_pipeline_denoise_chunk: reflex_denoise_chunk on the context's stream
+ * over the window of the first n_frames frames (frames max(0, n_frames - W) ..
+ * n_frames - 1, dynamic tokens at positions static_len + n_frames*frame_tokens
+ * + i).  With F frames written so far, n_frames must lie in [max(0, F - 1), F];
+ * the context's stream waits on the device for the write of frame
+ * n_frames - 1.  n_frames = -1 takes F if the newest write has completed when
+ * the call is made, else F - 1 (the consumer querying the latest cache state;
+ * the host never waits).  *n_frames_out (nullable) receives the value used.
+ * reflex_denoise_chunk on such a context is this call with n_frames = F.
+ *
+ * Errors: REFLEX_EINVAL (cfg.spare_slot == 0, n_frames outside the range, and
+ * as the calls they extend), REFLEX_ESTATE, REFLEX_EHIP.  The Standard
+ * strategy of reflex_denoise_chunk_baseline is not available on a context
+ * with a spare slot (it would re-encode frames on the context's stream while
+ * the writer stream uses the same scratch); the Naive strategy is.
+ */
+int reflex_pipeline_write_frame(reflex_ctx* ctx, const void* frame, void* writer_stream,
+                                int64_t* frame_index_out, int32_t* evicted_tokens_out);
+int reflex_pipeline_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise,
+                                  int32_t num_steps, const float* tau_schedule, float* actions_out,
+                                  int64_t n_frames, int64_t* n_frames_out);
 
 /* Release the host context and its captured graphs; never frees caller
  * memory.  NULL is a no-op.  Returns 0. */

@@ -6,7 +6,10 @@
 // n_valid*frame_tokens read from device memory, so the same launch serves
 // every tick.  Softmax is permutation-invariant over keys, so ring slots are
 // read in physical order; the result equals one softmax over the concatenated
-// context (Appendix A, Proposition A.1).
+// context (Appendix A, Proposition A.1).  A pipelined ring holds one spare
+// slot, the one the next frame is being written into while this launch runs;
+// the cached rows are then read around it (logical row j at physical row
+// j + frame_tokens from *hole_row on), again from device memory.
 //
 // Inputs come ready from the QKV projection's epilogue: RoPE-rotated q rows
 // and dynamic keys, and transposed dynamic values zero-padded to 64 columns,
@@ -106,6 +109,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
   const T* kdb = reinterpret_cast<const T*>(p.kd) + (int64_t)b * T_ * DH;
   const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
   const float scale = rsqrtf((float)DH) * 1.4426950408889634f;  // 1/sqrt(d) * log2(e)
+  const int hole = *p.hole_row, skip = p.frame_tokens;
 
   // global -> register staging of one tile.  Loads are unconditional from
   // clamped (in-range) addresses and the out-of-range chunks are zeroed when
@@ -127,7 +131,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
       const int r = base + kr;
       const bool ok = r < lim;
       kmask |= ok ? (1u << i) : 0u;
-      rk[i] = ld16(reinterpret_cast<const unsigned char*>(ksrc + (int64_t)(ok ? r : 0) * DH) + cc * 16);
+      int rr = ok ? r : 0;
+      rr += (!dyn && rr >= hole) ? skip : 0;
+      rk[i] = ld16(reinterpret_cast<const unsigned char*>(ksrc + (int64_t)rr * DH) + cc * 16);
     }
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
@@ -138,7 +144,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs p) {
       const bool ok = dyn || key < lim;
       vmask |= ok ? (1u << i) : 0u;
       const T* vsrc = dyn ? vdb + (int64_t)d * p.tpad : cvt + (int64_t)d * p.R;
-      rv[i] = ld16(reinterpret_cast<const unsigned char*>(vsrc + (ok ? key : 0)));
+      int kk = ok ? key : 0;
+      kk += (!dyn && kk >= hole) ? skip : 0;
+      rv[i] = ld16(reinterpret_cast<const unsigned char*>(vsrc + kk));
     }
   };
 
@@ -365,6 +373,7 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
   const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
   const float scale = rsqrtf((float)DH) * 1.4426950408889634f;
   const int tpad = p.tpad, Rrow = p.R;  // copied: a lambda must not capture the kernel argument
+  const int hole = __builtin_amdgcn_readfirstlane(*p.hole_row), skip = p.frame_tokens;
   constexpr int RPI = 64 / KCH;         // K rows per DMA instruction
 
   // DMA of tile t into stage sk.  Per-lane offsets are rebuilt from an opaque
@@ -396,15 +405,18 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
 #pragma unroll
       for (int j = 0; j < NIK; ++j) {
         const int row = RPI * (wave * NIK + j) + kr;
-        const int r = min(base + row, last);
+        int r = min(base + row, last);
+        r += r >= hole ? skip : 0;
         __builtin_amdgcn_global_load_lds(ck + (int64_t)r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8,
                                          sk + (wave * NIK + j) * 1024, 16, 0, 0);
       }
 #pragma unroll
       for (int j = 0; j < NIV; ++j) {
         const int d = (wave * NIV + j) * 8 + vd;
-        const int key = base + (vc ^ (d & 7)) * 8;
-        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + (key <= last ? key : 0),
+        int key = base + (vc ^ (d & 7)) * 8;
+        key = key <= last ? key : 0;
+        key += key >= hole ? skip : 0;
+        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + key,
                                          sv + (wave * NIV + j) * 1024, 16, 0, 0);
       }
     }

@@ -70,6 +70,11 @@ struct AttnArgs {
   const void* cache_vt;   // layer base: [B] stride ck_bstride, [dh][R]
   int64_t ck_bstride;     // elements between envs (= L*R*dh)
   const int32_t* n_valid; // device: frames visible in the ring
+  // device: cached rows are read in logical order; logical row j >= *hole_row
+  // sits one frame further in memory (the spare slot of a pipelined ring is
+  // skipped).  A value past the visible rows means no skip.  Both are
+  // multiples of 8 rows, so no 16-byte load straddles the skip.
+  const int32_t* hole_row;
   int static_len, frame_tokens, R;
   int B, T, Hq;
   int nsplit;             // key splits (blockIdx.x)
@@ -138,6 +143,12 @@ template <typename T> hipError_t launch_cond(void* cond, const float* state, con
                                              int B, int D, int ds, double min_p, double max_p,
                                              hipStream_t s);
 
+// Sets the device tick state {frames, n_valid, dyn_pos0, hole_row} that the
+// next chunk on this stream reads (one thread; the chunk's kernels follow in
+// stream order).
+hipError_t launch_tick_set(int64_t* tick, int64_t frames, int64_t n_valid, int64_t dyn_pos0, int64_t hole_row,
+                           hipStream_t s);
+
 // Ring/static write: K rows get RoPE from the table, V is stored transposed.
 struct RingWriteArgs {
   const void* src_k;     // element (b, l, j, d) at b*sb + l*sl + j*sj + d
@@ -150,7 +161,7 @@ struct RingWriteArgs {
   int n_tok, L, B, R;
   // tick state update (written by block 0 when tick != nullptr)
   int64_t* tick;
-  int64_t frames_written, dyn_pos0;
+  int64_t frames_written, dyn_pos0, hole_row;
   int32_t n_valid;
 };
 template <typename T, typename S> hipError_t launch_ring_write(const RingWriteArgs& a, int head_dim,

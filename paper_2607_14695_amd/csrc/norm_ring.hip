@@ -259,6 +259,22 @@ hipError_t launch_cond(void* cond, const float* state, const TauTable& taus, int
   return hipGetLastError();
 }
 
+__global__ void tick_set_kernel(int64_t* tick, int64_t frames, int64_t n_valid, int64_t dyn_pos0,
+                                int64_t hole_row) {
+  if (threadIdx.x == 0) {
+    tick[0] = frames;
+    tick[1] = n_valid;
+    tick[2] = dyn_pos0;
+    tick[3] = hole_row;
+  }
+}
+
+hipError_t launch_tick_set(int64_t* tick, int64_t frames, int64_t n_valid, int64_t dyn_pos0, int64_t hole_row,
+                           hipStream_t s) {
+  RFX_LAUNCH(tick_set_kernel, dim3(1), dim3(64), 0, s, tick, frames, n_valid, dyn_pos0, hole_row);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // ring / static writer.  Block = (64-token tile, layer, env).
 // K: cache_k[b][l][row0 + j][d] = rope(k_j)[d]
@@ -273,6 +289,7 @@ __global__ __launch_bounds__(256) void ring_write_kernel(RingWriteArgs p) {
     p.tick[0] = p.frames_written;
     p.tick[1] = (int64_t)p.n_valid;
     p.tick[2] = p.dyn_pos0;
+    p.tick[3] = p.hole_row;
   }
   const S* sk = reinterpret_cast<const S*>(p.src_k) + (int64_t)b * p.sb + (int64_t)l * p.sl;
   const S* sv = reinterpret_cast<const S*>(p.src_v) + (int64_t)b * p.sb + (int64_t)l * p.sl;

@@ -6,6 +6,7 @@
 // / Appendix B.2, and is mirrored into a small device "tick state" so the
 // captured denoise graph reads the current window length and dynamic positions
 // from memory and never needs re-capture when a frame arrives.
+#include <stdint.h>
 #include <string.h>
 
 #include <mutex>
@@ -79,7 +80,7 @@ struct Workspace {
 constexpr int kWsParts = 20;
 
 struct Plan {
-  int T, M, S, Nqkv, C, R, rows_pad, tpad, nrb, eb;
+  int T, M, S, Nqkv, C, R, slots, rows_pad, tpad, nrb, eb;
   SplitK o, down;
   int attn_splits;
   int max_parts;
@@ -120,13 +121,14 @@ int validate(const reflex_config* c) {
   if (c->static_len < 0 || c->static_len % 8) return REFLEX_EINVAL;
   if (c->frame_tokens < 8 || c->frame_tokens % 8) return REFLEX_EINVAL;
   if (c->window_frames < 1) return REFLEX_EINVAL;
+  if ((c->spare_slot != 0 && c->spare_slot != 1) || c->reserved != 0) return REFLEX_EINVAL;
   if (c->frame_dim < 0 || c->frame_dim % 8) return REFLEX_EINVAL;
   if (c->batch < 1 || c->batch > 4096) return REFLEX_EINVAL;
   if (c->max_steps < 1 || c->max_steps > REFLEX_MAX_STEPS) return REFLEX_EINVAL;
   if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.0) || !(c->temb_min_period > 0.0) ||
       !(c->temb_max_period > 0.0))
     return REFLEX_EINVAL;
-  const int64_t R = (int64_t)c->static_len + (int64_t)c->window_frames * c->frame_tokens;
+  const int64_t R = (int64_t)c->static_len + ((int64_t)c->window_frames + c->spare_slot) * c->frame_tokens;
   if (R > (1 << 24)) return REFLEX_EINVAL;
   return REFLEX_OK;
 }
@@ -140,7 +142,8 @@ Plan make_plan(const reflex_config* c) {
   p.S = 2 * c->n_layers + 1;
   p.Nqkv = (c->n_q_heads + 2) * c->head_dim;
   p.C = c->width + c->state_dim;
-  p.R = c->static_len + c->window_frames * c->frame_tokens;
+  p.slots = c->window_frames + c->spare_slot;
+  p.R = c->static_len + p.slots * c->frame_tokens;
   const int rows = p.T * c->n_q_heads;
   p.rows_pad = (rows + 127) / 128 * 128;
   p.nrb = p.rows_pad / 64;
@@ -205,6 +208,16 @@ struct reflex_ctx {
   int32_t prof_launches[PC_N];
   std::vector<hipEvent_t> ev_pool;
   std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> ev_pending;
+  // pipelined streaming (spare slot): completion events of the last two frame
+  // writes (n = frame index) and of recent chunks (n = frames they read, one
+  // record per distinct n, increasing), with a pool of free events
+  struct EvRec {
+    int64_t n;
+    hipEvent_t ev;
+    hipStream_t stream;
+  };
+  std::vector<EvRec> write_recs, chunk_recs;
+  std::vector<hipEvent_t> pipe_free;
 };
 
 namespace {
@@ -212,6 +225,36 @@ namespace {
 int hip_fail(hipError_t e) {
   snprintf(g_hip_err, sizeof(g_hip_err), "HIP error %d: %s", (int)e, hipGetErrorString(e));
   return REFLEX_EHIP;
+}
+
+// Ring bookkeeping of writing frame f (Section 3.1 FIFO; Appendix B.2).  A
+// ring with a spare slot places frame f in slot f mod (W + 1).
+int plan_frame(const reflex_ctx* ctx, int64_t f, reflex_ring_step* stp) {
+  const reflex_config& c = ctx->cfg;
+  const int rc = reflex_ring_plan(f, c.window_frames, c.frame_tokens, c.static_len, stp);
+  if (rc != REFLEX_OK) return rc;
+  stp->slot = (int32_t)(f % ctx->plan.slots);
+  return REFLEX_OK;
+}
+
+// Logical cached row from which the physical rows skip the spare slot, once n
+// frames are written: the spare slot is the one frame n will be written into.
+// Without a spare slot the rows are read in place (the value is past them).
+int64_t hole_row(const reflex_ctx* ctx, int64_t n) {
+  const reflex_config& c = ctx->cfg;
+  if (!c.spare_slot) return ctx->plan.R;
+  return (int64_t)c.static_len + (n % ctx->plan.slots) * c.frame_tokens;
+}
+
+hipEvent_t pipe_event(reflex_ctx* ctx) {
+  if (!ctx->pipe_free.empty()) {
+    hipEvent_t e = ctx->pipe_free.back();
+    ctx->pipe_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+  return e;
 }
 
 struct Launcher {
@@ -253,7 +296,8 @@ struct Launcher {
 template <typename T>
 int write_static(reflex_ctx* ctx, const void* sk, const void* sv, bool publish, Launcher& L);
 template <typename T>
-int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool publish, Launcher& L);
+int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool publish, Launcher& L,
+                hipStream_t st);
 
 // Standard mode (full history recomputation): the static prefix and every
 // window frame are encoded into their cache rows again, with the kernels and
@@ -264,9 +308,8 @@ int reencode_history(reflex_ctx* ctx, const reflex_sources* src, Launcher& L) {
   if (c.static_len > 0) RFX_TRY(write_static<T>(ctx, src->static_k, src->static_v, false, L));
   for (int i = 0; i < src->n_frames; ++i) {
     reflex_ring_step stp;
-    RFX_TRY(reflex_ring_plan(ctx->frames_written - src->n_frames + i, c.window_frames, c.frame_tokens,
-                             c.static_len, &stp));
-    RFX_TRY(write_frame<T>(ctx, src->frames[i], stp, false, L));
+    RFX_TRY(plan_frame(ctx, ctx->frames_written - src->n_frames + i, &stp));
+    RFX_TRY(write_frame<T>(ctx, src->frames[i], stp, false, L, ctx->stream));
   }
   return REFLEX_OK;
 }
@@ -347,6 +390,7 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
       aa.cache_vt = (const char*)ctx->cache_vt + (size_t)l * P.R * dh * eb;
       aa.ck_bstride = (int64_t)c.n_layers * P.R * dh;
       aa.n_valid = reinterpret_cast<const int32_t*>(W.tick + 1);
+      aa.hole_row = reinterpret_cast<const int32_t*>(W.tick + 3);
       aa.static_len = c.static_len; aa.frame_tokens = c.frame_tokens; aa.R = P.R;
       aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits;
       aa.part_o = W.part_o; aa.part_ml = W.part_ml;
@@ -421,11 +465,12 @@ int write_static(reflex_ctx* ctx, const void* sk, const void* sv, bool publish, 
   a.cache_k = ctx->cache_k; a.cache_vt = ctx->cache_vt;
   a.row0 = 0; a.n_tok = c.static_len; a.L = c.n_layers; a.B = c.batch; a.R = P.R;
   a.tick = publish ? ctx->ws.tick : nullptr; a.frames_written = 0; a.n_valid = 0; a.dyn_pos0 = c.static_len;
+  a.hole_row = hole_row(ctx, 0);
   if (c.static_len == 0) {
     if (!publish) return REFLEX_OK;
     // still publish the tick state; a one-token dummy write is not needed, so
     // set it with a tiny copy instead
-    int64_t host_tick[3] = {0, 0, (int64_t)c.static_len};
+    int64_t host_tick[4] = {0, 0, (int64_t)c.static_len, a.hole_row};
     e = hipMemcpyAsync(ctx->ws.tick, host_tick, sizeof(host_tick), hipMemcpyHostToDevice, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     return e == hipSuccess ? REFLEX_OK : hip_fail(e);
@@ -436,10 +481,10 @@ int write_static(reflex_ctx* ctx, const void* sk, const void* sv, bool publish, 
 // publish: advance the device tick state to this frame (a new frame); a
 // Standard-mode re-encode of an older frame leaves the tick state alone.
 template <typename T>
-int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool publish, Launcher& L) {
+int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp, bool publish, Launcher& L,
+                hipStream_t st) {
   const reflex_config& c = ctx->cfg;
   const Plan& P = ctx->plan;
-  hipStream_t st = ctx->stream;
   RFX_TRY(L.run(PC_ROPE, [&] {
     return launch_rope_table(ctx->ws.rope_frame, nullptr, stp.pos0, c.frame_tokens, c.head_dim, c.rope_theta, st);
   }));
@@ -451,6 +496,7 @@ int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp,
   a.n_tok = c.frame_tokens; a.L = c.n_layers; a.B = c.batch; a.R = P.R;
   a.tick = publish ? ctx->ws.tick : nullptr; a.frames_written = stp.frame_index + 1; a.n_valid = stp.n_valid;
   a.dyn_pos0 = stp.dyn_pos0;
+  a.hole_row = hole_row(ctx, stp.frame_index + 1);
   if (c.frame_dim > 0) {
     const int N = c.n_layers * 2 * dh;
     GemmArgs g{};
@@ -478,8 +524,8 @@ int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp,
 }
 
 // Sum the per-launch events of a profiled call into the per-class totals.
-int collect_profile(reflex_ctx* ctx) {
-  hipError_t e = hipStreamSynchronize(ctx->stream);
+int collect_profile(reflex_ctx* ctx, hipStream_t st) {
+  hipError_t e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(e);
   for (int i = 0; i < PC_N; ++i) {
     ctx->prof_ms[i] = 0.0;
@@ -492,6 +538,73 @@ int collect_profile(reflex_ctx* ctx) {
     ctx->prof_launches[pe.first] += 1;
   }
   ctx->ev_pending.clear();
+  return REFLEX_OK;
+}
+
+// One frame write on stream st.  A write on the context's stream also
+// publishes the device tick state for the next chunk there.  With a spare
+// slot, chunks set their own tick state (a write on another stream must not
+// touch the state a running chunk reads), and the write is ordered on the
+// device after the previous write and after every chunk that still reads the
+// frame in its target slot.
+int write_entry(reflex_ctx* ctx, const void* frame, hipStream_t st, int64_t* frame_index_out,
+                int32_t* evicted_tokens_out) {
+  if (!frame) return REFLEX_EINVAL;
+  const reflex_config& c = ctx->cfg;
+  const int64_t f = ctx->frames_written;
+  reflex_ring_step stp;
+  int rc = plan_frame(ctx, f, &stp);
+  if (rc != REFLEX_OK) return rc;
+  const bool spare = c.spare_slot != 0;
+  if (spare) {
+    hipError_t e = hipSuccess;
+    // the previous write shares the frame scratch and must finish first
+    if (!ctx->write_recs.empty() && ctx->write_recs.back().stream != st)
+      e = hipStreamWaitEvent(st, ctx->write_recs.back().ev, 0);
+    // slot f mod (W+1) holds frame f-W-1, which the windows of chunks over
+    // n in [f-W, f-1] frames contain; the latest chunk with n <= f-1 covers
+    // all earlier ones (one stream)
+    for (auto it = ctx->chunk_recs.rbegin(); e == hipSuccess && it != ctx->chunk_recs.rend(); ++it) {
+      if (it->n <= f - 1) {
+        if (it->stream != st) e = hipStreamWaitEvent(st, it->ev, 0);
+        break;
+      }
+    }
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  const bool prof = ctx->prof_enabled != 0;
+  if (prof) ctx->ev_pending.clear();
+  {
+    Launcher L{ctx, prof};
+    const bool publish = st == ctx->stream;
+    rc = c.dtype == REFLEX_DTYPE_BF16 ? write_frame<bf16_t>(ctx, frame, stp, publish, L, st)
+                                      : write_frame<float>(ctx, frame, stp, publish, L, st);
+  }
+  if (rc == REFLEX_OK && prof) rc = collect_profile(ctx, st);
+  if (rc != REFLEX_OK) return rc;
+  if (spare) {
+    hipEvent_t ev = pipe_event(ctx);
+    if (!ev) return hip_fail(hipErrorOutOfMemory);
+    const hipError_t e = hipEventRecord(ev, st);
+    if (e != hipSuccess) {
+      ctx->pipe_free.push_back(ev);
+      return hip_fail(e);
+    }
+    ctx->write_recs.push_back({f, ev, st});
+    if (ctx->write_recs.size() > 2) {
+      ctx->pipe_free.push_back(ctx->write_recs.front().ev);
+      ctx->write_recs.erase(ctx->write_recs.begin());
+    }
+    // every chunk so far read n <= f frames: for the next write only the
+    // latest one matters
+    while (ctx->chunk_recs.size() > 1) {
+      ctx->pipe_free.push_back(ctx->chunk_recs.front().ev);
+      ctx->chunk_recs.erase(ctx->chunk_recs.begin());
+    }
+  }
+  ctx->frames_written += 1;
+  if (frame_index_out) *frame_index_out = stp.frame_index;
+  if (evicted_tokens_out) *evicted_tokens_out = stp.evicted;
   return REFLEX_OK;
 }
 
@@ -596,36 +709,55 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
 int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_index_out,
                              int32_t* evicted_tokens_out) {
   if (!ctx || !ctx->alive) return REFLEX_ESTATE;
-  if (!frame) return REFLEX_EINVAL;
-  const reflex_config& c = ctx->cfg;
-  reflex_ring_step stp;
-  int rc = reflex_ring_plan(ctx->frames_written, c.window_frames, c.frame_tokens, c.static_len, &stp);
-  if (rc != REFLEX_OK) return rc;
-  const bool prof = ctx->prof_enabled != 0;
-  if (prof) ctx->ev_pending.clear();
-  {
-    Launcher L{ctx, prof};
-    rc = c.dtype == REFLEX_DTYPE_BF16 ? write_frame<bf16_t>(ctx, frame, stp, true, L)
-                                      : write_frame<float>(ctx, frame, stp, true, L);
-  }
-  if (rc == REFLEX_OK && prof) rc = collect_profile(ctx);
-  if (rc != REFLEX_OK) return rc;
-  ctx->frames_written += 1;
-  if (frame_index_out) *frame_index_out = stp.frame_index;
-  if (evicted_tokens_out) *evicted_tokens_out = stp.evicted;
-  return REFLEX_OK;
+  return write_entry(ctx, frame, ctx->stream, frame_index_out, evicted_tokens_out);
+}
+
+int reflex_pipeline_write_frame(reflex_ctx* ctx, const void* frame, void* writer_stream, int64_t* frame_index_out,
+                                int32_t* evicted_tokens_out) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  if (!ctx->cfg.spare_slot) return REFLEX_EINVAL;
+  return write_entry(ctx, frame, reinterpret_cast<hipStream_t>(writer_stream), frame_index_out,
+                     evicted_tokens_out);
 }
 
 }  // extern "C"
 
 namespace {
 
+constexpr int64_t kAllFrames = INT64_MIN;  // every frame written so far
+
+int denoise_launch(reflex_ctx* ctx, int mode, const reflex_sources* src, std::vector<const void*> srcs,
+                   const float* state, const float* noise, int32_t num_steps, const float* taus,
+                   float* actions_out);
+
+// n_req: the frames the chunk reads on a context with a spare slot (-1: the
+// newest completed write, kAllFrames: all); ignored without a spare slot,
+// where the tick state published by the last write is read.
 int denoise_entry(reflex_ctx* ctx, int mode, const reflex_sources* src, const float* state, const float* noise,
-                  int32_t num_steps, const float* tau_schedule, float* actions_out) {
+                  int32_t num_steps, const float* tau_schedule, float* actions_out, int64_t n_req,
+                  int64_t* n_out) {
   if (!ctx || !ctx->alive) return REFLEX_ESTATE;
   if (!state || !noise || !actions_out) return REFLEX_EINVAL;
   if (num_steps < 1 || num_steps > ctx->cfg.max_steps) return REFLEX_EINVAL;
   if (mode != REFLEX_MODE_REFLEX && mode != REFLEX_MODE_STANDARD && mode != REFLEX_MODE_NAIVE) return REFLEX_EINVAL;
+  const bool spare = ctx->cfg.spare_slot != 0;
+  if (spare && mode == REFLEX_MODE_STANDARD) return REFLEX_EINVAL;
+  const int64_t F = ctx->frames_written;
+  int64_t n = F;
+  if (spare && n_req != kAllFrames) {
+    if (n_req == -1) {
+      // the newest frame whose write has completed (at most one is in flight
+      // that a chunk may skip: the spare slot protects one)
+      if (!ctx->write_recs.empty() && ctx->write_recs.back().n == F - 1) {
+        const hipError_t q = hipEventQuery(ctx->write_recs.back().ev);
+        if (q == hipErrorNotReady) n = F - 1;
+        else if (q != hipSuccess) return hip_fail(q);
+      }
+    } else {
+      n = n_req;
+    }
+    if (n < (F > 0 ? F - 1 : 0) || n > F) return REFLEX_EINVAL;
+  }
   std::vector<const void*> srcs;
   if (mode == REFLEX_MODE_STANDARD) {
     const reflex_config& c = ctx->cfg;
@@ -645,11 +777,46 @@ int denoise_entry(reflex_ctx* ctx, int mode, const reflex_sources* src, const fl
   for (int k = 0; k <= num_steps; ++k)
     taus[k] = tau_schedule ? tau_schedule[k] : (float)(1.0 - (double)k / (double)num_steps);
 
+  if (spare) {
+    // frame n-1 (and so every earlier frame) written, then this chunk's window
+    hipError_t e = hipSuccess;
+    for (const auto& w : ctx->write_recs)
+      if (w.n == n - 1 && w.stream != ctx->stream) e = hipStreamWaitEvent(ctx->stream, w.ev, 0);
+    if (e != hipSuccess) return hip_fail(e);
+    const reflex_config& c = ctx->cfg;
+    e = launch_tick_set(ctx->ws.tick, n, n < c.window_frames ? n : c.window_frames,
+                        (int64_t)c.static_len + n * c.frame_tokens, hole_row(ctx, n), ctx->stream);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  const int rc = denoise_launch(ctx, mode, src, std::move(srcs), state, noise, num_steps, taus, actions_out);
+  if (rc != REFLEX_OK) return rc;
+  if (spare) {
+    hipError_t e;
+    if (!ctx->chunk_recs.empty() && ctx->chunk_recs.back().n == n) {
+      e = hipEventRecord(ctx->chunk_recs.back().ev, ctx->stream);
+    } else {
+      hipEvent_t ev = pipe_event(ctx);
+      if (!ev) return hip_fail(hipErrorOutOfMemory);
+      e = hipEventRecord(ev, ctx->stream);
+      if (e == hipSuccess) ctx->chunk_recs.push_back({n, ev, ctx->stream});
+      else ctx->pipe_free.push_back(ev);
+    }
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  if (n_out) *n_out = n;
+  return REFLEX_OK;
+}
+
+// The chunk's launches: eager with per-launch events when profiling, else
+// one captured graph per distinct (pointers, steps, schedule, strategy).
+int denoise_launch(reflex_ctx* ctx, int mode, const reflex_sources* src, std::vector<const void*> srcs,
+                   const float* state, const float* noise, int32_t num_steps, const float* taus,
+                   float* actions_out) {
   if (ctx->prof_enabled) {
     ctx->ev_pending.clear();
     int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, true, mode, src);
     if (rc != REFLEX_OK) return rc;
-    return collect_profile(ctx);
+    return collect_profile(ctx, ctx->stream);
   }
 
   GraphEntry* hit = nullptr;
@@ -701,13 +868,23 @@ extern "C" {
 
 int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
                          const float* tau_schedule, float* actions_out) {
-  return denoise_entry(ctx, REFLEX_MODE_REFLEX, nullptr, state, noise, num_steps, tau_schedule, actions_out);
+  return denoise_entry(ctx, REFLEX_MODE_REFLEX, nullptr, state, noise, num_steps, tau_schedule, actions_out,
+                       kAllFrames, nullptr);
 }
 
 int reflex_denoise_chunk_baseline(reflex_ctx* ctx, int32_t mode, const reflex_sources* src, const float* state,
                                   const float* noise, int32_t num_steps, const float* tau_schedule,
                                   float* actions_out) {
-  return denoise_entry(ctx, mode, src, state, noise, num_steps, tau_schedule, actions_out);
+  return denoise_entry(ctx, mode, src, state, noise, num_steps, tau_schedule, actions_out, kAllFrames, nullptr);
+}
+
+int reflex_pipeline_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                                  const float* tau_schedule, float* actions_out, int64_t n_frames,
+                                  int64_t* n_frames_out) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  if (!ctx->cfg.spare_slot || n_frames < -1) return REFLEX_EINVAL;
+  return denoise_entry(ctx, REFLEX_MODE_REFLEX, nullptr, state, noise, num_steps, tau_schedule, actions_out,
+                       n_frames, n_frames_out);
 }
 
 int reflex_destroy(reflex_ctx* ctx) {
@@ -717,6 +894,9 @@ int reflex_destroy(reflex_ctx* ctx) {
   ctx->graphs.clear();
   for (auto e : ctx->ev_pool) (void)hipEventDestroy(e);
   ctx->ev_pool.clear();
+  for (auto& r : ctx->write_recs) (void)hipEventDestroy(r.ev);
+  for (auto& r : ctx->chunk_recs) (void)hipEventDestroy(r.ev);
+  for (auto e : ctx->pipe_free) (void)hipEventDestroy(e);
   delete ctx;
   return REFLEX_OK;
 }

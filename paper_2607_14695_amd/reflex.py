@@ -47,7 +47,7 @@ class ConfigC(ctypes.Structure):
         ("frame_tokens", c_i32), ("window_frames", c_i32), ("frame_dim", c_i32), ("batch", c_i32),
         ("dtype", c_i32), ("mod_mode", c_i32), ("max_steps", c_i32), ("rms_eps", c_f32),
         ("embed_scale", c_f32), ("rope_theta", c_f64), ("temb_min_period", c_f64),
-        ("temb_max_period", c_f64),
+        ("temb_max_period", c_f64), ("spare_slot", c_i32), ("reserved", c_i32),
     ]
 
 
@@ -98,6 +98,8 @@ def load_library() -> ctypes.CDLL:
         "reflex_cache_write_frame": (c_i32, [c_vp, c_vp, P(c_i64), P(c_i32)]),
         "reflex_denoise_chunk": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp]),
         "reflex_denoise_chunk_baseline": (c_i32, [c_vp, c_i32, P(SourcesC), c_vp, c_vp, c_i32, c_vp, c_vp]),
+        "reflex_pipeline_write_frame": (c_i32, [c_vp, c_vp, c_vp, P(c_i64), P(c_i32)]),
+        "reflex_pipeline_denoise_chunk": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp, c_i64, P(c_i64)]),
         "reflex_destroy": (c_i32, [c_vp]),
         "reflex_strerror": (ctypes.c_char_p, [c_i32]),
         "reflex_ring_plan": (c_i32, [c_i64, c_i32, c_i32, c_i32, P(RingStepC)]),
@@ -139,7 +141,7 @@ def config_to_c(cfg: ReflexConfig, max_steps: Optional[int] = None) -> ConfigC:
         frame_dim=cfg.frame_dim, batch=cfg.batch, dtype=DTYPE_BF16 if cfg.bf16 else DTYPE_F32,
         mod_mode=MOD_SCALE_ONLY if cfg.mod_mode == "scale_only" else MOD_FULL, max_steps=ms,
         rms_eps=cfg.rms_eps, embed_scale=cfg.embed_scale, rope_theta=cfg.rope_theta,
-        temb_min_period=cfg.temb_min_period, temb_max_period=cfg.temb_max_period)
+        temb_min_period=cfg.temb_min_period, temb_max_period=cfg.temb_max_period, spare_slot=cfg.spare_slot)
 
 
 def query_sizes(cfg: ReflexConfig, max_steps: Optional[int] = None) -> Tuple[int, int]:
@@ -184,6 +186,8 @@ class ReflexEngine:
         self.dtype = torch.bfloat16 if cfg.bf16 else torch.float32
         self.max_steps = max_steps if max_steps is not None else max(cfg.num_steps, 1)
         self.stream = torch.cuda.Stream(device=self.device)
+        self.writer = None  # second stream of the asynchronous pipeline, made on first use
+        self.last_n_frames = None
         self.ctx = c_vp(None)
         self._bufs = {}
         with torch.cuda.stream(self.stream):
@@ -247,6 +251,26 @@ class ReflexEngine:
         caller.wait_stream(self.stream)
         return fi.value, ev.value
 
+    def pipeline_write(self, frame) -> Tuple[int, int]:
+        """Write one frame on the engine's writer stream (asynchronous
+        pipeline, needs ``cfg.spare_slot = 1``); returns (frame_index,
+        evicted_tokens).  The write overlaps chunks on the engine stream; the
+        library orders the two streams on the device.  The caller's stream is
+        not made to wait for the write."""
+        torch = self.torch
+        if self.writer is None:
+            self.writer = torch.cuda.Stream(device=self.device)
+        self.writer.wait_stream(torch.cuda.current_stream(self.device))
+        with torch.cuda.stream(self.writer):
+            f = self._dev(frame)
+            f.record_stream(self.writer)  # not reused before the writer has read it
+            fi, ev = c_i64(0), c_i32(0)
+            _check(self.lib.reflex_pipeline_write_frame(self.ctx, f.data_ptr(), self.writer.cuda_stream,
+                                                        ctypes.byref(fi), ctypes.byref(ev)),
+                   "reflex_pipeline_write_frame")
+            self._window.append(f)
+        return fi.value, ev.value
+
     def _staged(self, key, a):
         """Device fp32 view of an input; numpy inputs are copied into a
         persistent buffer so repeated calls keep the same device pointers (and
@@ -264,7 +288,7 @@ class ReflexEngine:
         return buf
 
     def denoise(self, state, noise, num_steps: Optional[int] = None, taus: Optional[Sequence[float]] = None,
-                out=None, mode: str = "reflex"):
+                out=None, mode: str = "reflex", n_frames: Optional[int] = None):
         """Denoise one chunk per env; returns the fp32 action tensor (device).
 
         Without ``out`` the result lands in a buffer owned by the engine that
@@ -274,10 +298,16 @@ class ReflexEngine:
         ``mode`` selects the cache strategy: "reflex" (the method), or the
         comparison baselines "standard" (the static prefix and the window's
         frames, as last passed to ``write_frame``, are encoded again before
-        every step) and "naive" (the first step's dynamic K/V are reused)."""
+        every step) and "naive" (the first step's dynamic K/V are reused).
+
+        ``n_frames`` (pipelined ring, ``cfg.spare_slot = 1``) selects the
+        window: the first n_frames frames, or -1 for the newest frame whose
+        write has completed; the value used is left in ``last_n_frames``."""
         torch = self.torch
         if mode not in MODES:
             raise ValueError(f"unknown mode {mode!r}")
+        if n_frames is not None and mode != "reflex":
+            raise ValueError("a pipelined window is only available to the method")
         k = num_steps if num_steps is not None else self.cfg.num_steps
         if taus is None and self.cfg.tau_schedule is not None and k == self.cfg.num_steps:
             taus = self.cfg.taus()  # the workload's own schedule
@@ -297,7 +327,13 @@ class ReflexEngine:
                     raise ValueError("tau schedule needs num_steps + 1 entries")
                 self._keep_taus = tau_np
                 tau_arr = tau_np.ctypes.data
-            if mode == "reflex":
+            if n_frames is not None:
+                used = c_i64(0)
+                _check(self.lib.reflex_pipeline_denoise_chunk(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr,
+                                                              out.data_ptr(), n_frames, ctypes.byref(used)),
+                       "reflex_pipeline_denoise_chunk")
+                self.last_n_frames = used.value
+            elif mode == "reflex":
                 _check(self.lib.reflex_denoise_chunk(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr,
                                                      out.data_ptr()), "reflex_denoise_chunk")
             else:
@@ -321,16 +357,25 @@ class ReflexEngine:
         return ctypes.byref(src)
 
     def synchronize(self):
+        if self.writer is not None:
+            self.writer.synchronize()
         self.stream.synchronize()
 
     def frames_written(self) -> int:
         return int(self.lib.reflex_frames_written(self.ctx))
 
     def tick_state(self) -> Tuple[int, int, int]:
-        """Device tick state (frames_written, n_valid, dyn_pos0), first 24 workspace bytes."""
+        """Device tick state (frames_written, n_valid, dyn_pos0), the first three
+        of the four int64 at the start of the workspace."""
         self.synchronize()
         t = self.ws[:24].view(self.torch.int64).cpu().tolist()
         return int(t[0]), int(t[1]), int(t[2])
+
+    def hole_row(self) -> int:
+        """Fourth tick-state value: the logical cached row from which the
+        physical rows skip the spare slot."""
+        self.synchronize()
+        return int(self.ws[24:32].view(self.torch.int64).cpu().item())
 
     def cache_views(self):
         """(K [B, L, R, dh], V^T [B, L, dh, R]) views of the cache, config dtype."""

@@ -68,6 +68,8 @@ class ReflexConfig:
     temb_max_period: float = 4.0
     embed_scale: float = 1.0
     mod_mode: str = "full"  # "full" (scale/shift/gate) or "scale_only" (Eq. 2)
+    # GPU cache layout only: 1 = one spare ring slot for pipelined frame writes
+    spare_slot: int = 0
     # workload driver
     ticks: int = 1
     tau_schedule: Optional[Tuple[float, ...]] = None
@@ -92,7 +94,7 @@ class ReflexConfig:
 
     @property
     def cache_rows(self) -> int:
-        return self.static_len + self.window_frames * self.frame_tokens
+        return self.static_len + (self.window_frames + self.spare_slot) * self.frame_tokens
 
     @property
     def bf16(self) -> bool:

@@ -20,6 +20,7 @@ may write filler for those):
 """
 from __future__ import annotations
 
+import ast
 import hashlib
 import os
 import sys
@@ -42,11 +43,23 @@ CASES = {
 }
 
 
+def _code_only(text: str) -> str:
+    """The module's syntax tree without docstrings (comments are not in the
+    tree): documentation edits leave the digest unchanged, code edits do not."""
+    tree = ast.parse(text)
+    for node in ast.walk(tree):
+        body = getattr(node, "body", None)
+        if isinstance(body, list) and body and isinstance(body[0], ast.Expr) \
+                and isinstance(body[0].value, ast.Constant) and isinstance(body[0].value.value, str):
+            node.body = body[1:] or [ast.Pass()]
+    return ast.dump(tree, include_attributes=False)
+
+
 def source_digest() -> str:
     h = hashlib.sha256()
     for rel in ("oracle/reflex_oracle.py", "paper_2607_14695_amd/workloads.py"):
-        with open(os.path.join(ROOT, rel), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -3,6 +3,7 @@ header declares, and its pure host functions (ring bookkeeping, size query,
 validation, status text) behave as documented.  No device calls."""
 import ctypes
 import os
+import subprocess
 
 import pytest
 
@@ -65,10 +66,23 @@ def test_query_sizes_rejects_bad_configs():
     assert R.query_sizes_status(base) == R.REFLEX_OK
     for field, bad in [("n_kv_heads", 2), ("head_dim", 96), ("action_horizon", 64), ("width", 100),
                        ("dtype", 7), ("max_steps", 0), ("max_steps", 65), ("frame_tokens", 12),
-                       ("static_len", -8), ("batch", 0), ("window_frames", 0), ("state_dim", 5)]:
+                       ("static_len", -8), ("batch", 0), ("window_frames", 0), ("state_dim", 5),
+                       ("spare_slot", 2), ("spare_slot", -1), ("reserved", 1)]:
         c = R.config_to_c(WL.CONFIGS["tiny_fp32"])
         setattr(c, field, bad)
         assert R.query_sizes_status(c) == R.REFLEX_EINVAL, field
+
+
+def test_spare_slot_adds_one_frame_of_rows():
+    """A ring with a spare slot holds window_frames + 1 frames per layer and env."""
+    for name in ("tiny_fp32", "pi0_stream_bf16"):
+        cfg = WL.CONFIGS[name]
+        c0, w0 = R.query_sizes(cfg)
+        c1, w1 = R.query_sizes(cfg.replace(spare_slot=1))
+        esz = 2 if cfg.bf16 else 4
+        extra = 2 * cfg.batch * cfg.n_layers * cfg.frame_tokens * cfg.head_dim * esz
+        assert abs((c1 - c0) - extra) <= 512, name
+        assert w1 >= w0  # the key split count may grow with the row count
 
 
 def test_null_and_state_errors_without_device():
@@ -90,6 +104,24 @@ def test_strerror_texts():
         assert isinstance(R.strerror(code), str) and R.strerror(code)
 
 
-def test_struct_sizes_match_c_layout():
-    assert ctypes.sizeof(R.ConfigC) == 18 * 4 + 2 * 4 + 3 * 8
-    assert ctypes.sizeof(R.RingStepC) == 40
+def test_struct_sizes_match_c_layout(tmp_path):
+    """Every ctypes mirror has the size and field offsets the C compiler gives
+    the header's struct (a small host program built with gcc prints them)."""
+    structs = {"reflex_config": R.ConfigC, "reflex_weights": R.WeightsC, "reflex_ring_step": R.RingStepC,
+               "reflex_sources": R.SourcesC}
+    lines = ['#include <stddef.h>', '#include <stdio.h>', f'#include "{R.HEADER_PATH}"', "int main(void) {"]
+    for cname, py in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-o", str(exe), str(src)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l.strip()}
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert got[(cname, fname)] == getattr(py, fname).offset, (cname, fname)
