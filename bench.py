@@ -237,6 +237,28 @@ def _pipeline(cfg, w, sk, sv, frames, state, noise, torch, ticks, warmup):
     return out
 
 
+def _scheduler(cfg, w, sk, sv, frames, noise, torch, chunks):
+    """Algorithm 1 in real time around the engine at batch 1: 50-action chunks
+    at a 20 ms control period, a frame every period through the pipelined
+    writer, a first-order robot; stall rate, reaction latency, inference
+    latency and hand-over state error for each schedule."""
+    import numpy as np
+
+    from paper_2607_14695_amd import overlap as OV
+    from paper_2607_14695_amd.reflex import ReflexEngine
+
+    eng = ReflexEngine(cfg.replace(spare_slot=1), w, sk, sv)
+    out = {}
+    for strategy in OV.STRATEGIES:
+        pol = OV.EnginePolicy(eng, frames, lambda i: noise)
+        sch = OV.OverlapScheduler(pol, cfg.action_horizon, 0.020, strategy=strategy, frame_period_s=0.020)
+        st = sch.run(OV.FirstOrderRobot(np.zeros(cfg.state_dim), alpha=0.5), chunks * cfg.action_horizon)
+        out[strategy] = st.summary()
+    eng.synchronize()
+    eng.close()
+    return out
+
+
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
     10 Euler steps, one frame in the window), median of two runs."""
@@ -287,6 +309,8 @@ def main():
                     help="skip the Standard / Naive-cache strategy timings")
     ap.add_argument("--no-pipeline", action="store_true",
                     help="skip the two-stream (asynchronous pipeline) tick timings")
+    ap.add_argument("--no-scheduler", action="store_true",
+                    help="skip the real-time Algorithm 1 scheduler run (about 10 s)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -393,8 +417,8 @@ def main():
             log(f"b32 pipeline: {b32['pipeline']}")
         log(f"b32 tick {t32 * 1e3:.3f} ms, chunk {c32s * 1e3:.3f} ms")
 
-    stream = strategies = pipeline = None
-    if not (args.no_latency and args.no_baselines and args.no_pipeline):
+    stream = strategies = pipeline = scheduler = None
+    if not (args.no_latency and args.no_baselines and args.no_pipeline and args.no_scheduler):
         cs = WL.CONFIGS["pi0_stream_bf16"]
         ws_, sks, svs, frs, sts, nzs = _device_inputs(cs, torch, seed=2)
         es = ReflexEngine(cs, ws_, sks, svs)
@@ -421,6 +445,12 @@ def main():
                                     "per-layer Wk/Wv projection + 10-step chunk; pipelined = write on a second "
                                     "stream, chunk over the frames before it")
             log(f"pipeline: {pipeline}")
+        if not args.no_scheduler:
+            scheduler = _scheduler(cs, ws_, sks, svs, frs, nzs, torch, 3)
+            scheduler["workload"] = ("pi0_stream_bf16 at batch 1: Algorithm 1 with 50-action chunks at a 20 ms "
+                                     "control period, a 768x2048 frame every period through the pipelined writer, "
+                                     "first-order robot (alpha 0.5); 150 control periods per schedule (the first chunk, then two hand-overs)")
+            log(f"scheduler: {scheduler}")
         del es, ws_
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, log)
@@ -457,6 +487,7 @@ def main():
         "stream_ticks": stream,
         "strategies": strategies,
         "pipeline": pipeline,
+        "scheduler": scheduler,
         "kernel_avg_us": kernel_avg_us,
         "roofline": {
             "kernel": dominant,

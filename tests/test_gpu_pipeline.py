@@ -168,3 +168,31 @@ def test_pipeline_rejects_misuse():
     eng.denoise(state, noise)
     eng.synchronize()
     eng.close()
+
+
+def test_overlap_scheduler_with_engine():
+    """Algorithm 1 in real time around the engine (tiny workload, 20 ms
+    control period, a frame every period through the pipelined writer): the
+    chunks come back with the engine's actions, the overlapped schedules never
+    stall, and the synchronous one stalls once per chunk."""
+    from paper_2607_14695_amd import overlap as OV
+
+    cfg = SPARE_CASES["tiny_fp32"]
+    w, sk, sv, frames = _setup(cfg, 4)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    noise = torch.from_numpy(WL.make_noise(cfg, 0)).cuda()
+    chunk = cfg.action_horizon
+    for strategy in ("reflex", "async_naive", "sync"):
+        pol = OV.EnginePolicy(eng, [frames[t] for t in range(4)], lambda i: noise)
+        sch = OV.OverlapScheduler(pol, chunk, 0.02, strategy=strategy, frame_period_s=0.02)
+        st = sch.run(OV.FirstOrderRobot(np.zeros(cfg.state_dim)), 3 * chunk)
+        s = st.summary()
+        print(strategy, s, flush=True)
+        assert st.chunks >= 2
+        assert s["inference_ms_mean"] < 20.0
+        if strategy == "sync":
+            assert st.stalls >= st.chunks
+        else:
+            assert st.stalls == 0 and set(st.k_used) == {1}
+    eng.synchronize()
+    eng.close()
