@@ -259,6 +259,84 @@ def _scheduler(cfg, w, sk, sv, frames, noise, torch, chunks):
     return out
 
 
+def _event_ms(eng, torch, fn, n):
+    """Mean device ms of n back-to-back calls of fn, between two events on the
+    engine's stream (after one untimed call)."""
+    fn()
+    eng.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(eng.stream)
+    for _ in range(n):
+        fn()
+    b.record(eng.stream)
+    eng.synchronize()
+    return round(a.elapsed_time(b) / n, 4)
+
+
+def sweep_window(torch, log, windows=(1, 2, 5, 10, 20, 50)):
+    """Context-window sweep (Section 4.6, context window size): batch 1,
+    768-token frames through the per-layer Wk/Wv, the ring filled with W
+    frames; chunk time of the method and of the Standard recompute, the
+    attention launch time, and a tick (write + chunk)."""
+    from paper_2607_14695_amd import workloads as WL
+    from paper_2607_14695_amd.reflex import ReflexEngine
+
+    base = WL.CONFIGS["pi0_stream_bf16"]
+    w, sk, sv, frames, state, noise = _device_inputs(base, torch, seed=3)
+    rows = []
+    for W in windows:
+        cfg = base.replace(window_frames=W)
+        eng = ReflexEngine(cfg, w, sk, sv)
+        for i in range(W):
+            eng.write_frame(frames[i % len(frames)])
+        r = {"window_frames": W, "cached_tokens": cfg.static_len + W * cfg.frame_tokens}
+        r["reflex_chunk_ms"] = _event_ms(eng, torch, lambda: eng.denoise(state, noise), 10)
+        r["standard_chunk_ms"] = _event_ms(eng, torch, lambda: eng.denoise(state, noise, mode="standard"), 3)
+        r["standard_over_reflex"] = round(r["standard_chunk_ms"] / r["reflex_chunk_ms"], 3)
+        prof = eng.profile(state, noise)
+        r["attention_us"] = round(prof["attention"][0] / prof["attention"][1] * 1e3, 3)
+        r["attn_merge_us"] = round(prof["attn_merge"][0] / max(1, prof["attn_merge"][1]) * 1e3, 3)
+        k = [0]
+
+        def tick():
+            eng.write_frame(frames[k[0] % len(frames)])
+            k[0] += 1
+            eng.denoise(state, noise)
+
+        r["tick_ms"] = _event_ms(eng, torch, tick, 10)
+        eng.close()
+        log(f"window {r}")
+        rows.append(r)
+    return rows
+
+
+def sweep_chunk(torch, log, horizons=(25, 50, 75, 100)):
+    """Action-chunk sweep: 10-step chunk time for H actions at batch 1 and 32
+    (2-frame ring of 768-token frames, 48 static tokens)."""
+    from paper_2607_14695_amd import workloads as WL
+    from paper_2607_14695_amd.reflex import ReflexEngine
+
+    rows = []
+    for name in ("pi0_stream_bf16", "pi0_batch32_bf16"):
+        base = WL.CONFIGS[name]
+        w, sk, sv, frames, state, _ = _device_inputs(base, torch, seed=4)
+        for H in horizons:
+            cfg = base.replace(action_horizon=H)
+            noise = torch.randn((cfg.batch, H, cfg.action_dim), device="cuda")
+            eng = ReflexEngine(cfg, w, sk, sv)
+            for i in range(cfg.window_frames):
+                eng.write_frame(frames[i])
+            ms = _event_ms(eng, torch, lambda: eng.denoise(state, noise), 5)
+            r = {"workload": name, "batch": cfg.batch, "action_horizon": H, "dynamic_tokens": H + 1,
+                 "chunk_ms": ms, "denoise_step_us": round(ms / cfg.num_steps * 1e3, 1),
+                 "actions_per_s": round(cfg.batch * H / (ms / 1e3), 1)}
+            eng.close()
+            log(f"chunk {r}")
+            rows.append(r)
+        del w
+    return rows
+
+
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
     10 Euler steps, one frame in the window), median of two runs."""
@@ -311,6 +389,8 @@ def main():
                     help="skip the two-stream (asynchronous pipeline) tick timings")
     ap.add_argument("--no-scheduler", action="store_true",
                     help="skip the real-time Algorithm 1 scheduler run (about 10 s)")
+    ap.add_argument("--sweep", choices=("window", "chunk", "all"),
+                    help="instead of the benchmark line, print one JSON line of the window and/or chunk sweeps")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -327,6 +407,15 @@ def main():
 
     def log(msg):
         print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    if args.sweep:
+        out = {"metric": "sweeps", "data": "synthetic", "dtype": "bf16"}
+        if args.sweep in ("window", "all"):
+            out["window"] = sweep_window(torch, log)
+        if args.sweep in ("chunk", "all"):
+            out["chunk"] = sweep_chunk(torch, log)
+        print(json.dumps(out), flush=True)
+        return
 
     if args.calibrate_copy:
         # a plain copy of known size: 256 MiB read + 256 MiB written per launch

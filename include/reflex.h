@@ -83,7 +83,7 @@ extern "C" {
  *
  * Supported by this build: n_kv_heads == 1; head_dim in {64, 128, 256};
  * width, mlp_dim, cond_hidden multiples of 64; state_dim, action_dim, frame_dim
- * multiples of 8; dynamic rows T <= 64 per env.
+ * multiples of 8; dynamic rows T <= 128 per env.
  */
 typedef struct reflex_config {
   int32_t n_layers;

@@ -117,7 +117,7 @@ int validate(const reflex_config* c) {
   if (c->dtype == REFLEX_DTYPE_F32 && c->head_dim > 128) return REFLEX_EINVAL;
   if (c->state_dim < 8 || c->state_dim > 64 || c->state_dim % 8) return REFLEX_EINVAL;
   if (c->action_dim < 1 || c->action_dim > 64) return REFLEX_EINVAL;
-  if (c->action_horizon < 1 || c->action_horizon + 1 > 64) return REFLEX_EINVAL;
+  if (c->action_horizon < 1 || c->action_horizon + 1 > 128) return REFLEX_EINVAL;
   if (c->static_len < 0 || c->static_len % 8) return REFLEX_EINVAL;
   if (c->frame_tokens < 8 || c->frame_tokens % 8) return REFLEX_EINVAL;
   if (c->window_frames < 1) return REFLEX_EINVAL;

@@ -231,6 +231,30 @@ def test_limits_t64_no_static_prefix(dtype):
     eng.close()
 
 
+@pytest.mark.parametrize("dtype,horizon", [("f32", 100), ("bf16", 100), ("bf16", 127)])
+def test_long_chunks_two_dynamic_tiles(dtype, horizon):
+    """Action chunks longer than one 64-key tile: T = 101 (a ragged second
+    dynamic tile) and T = 128 (the largest supported), so the dynamic keys
+    span two tiles and the query rows several 128-row blocks."""
+    cfg = RAGGED.replace(name=f"long_{dtype}_{horizon}", dtype=dtype, batch=2, action_horizon=horizon,
+                         n_q_heads=2, head_dim=64, width=128, mlp_dim=128, cond_hidden=64, frame_dim=0,
+                         window_frames=2, num_steps=2)
+    w, sk, sv, frames = _setup(cfg, 3)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(3):
+        eng.write_frame(frames[t])
+    state, noise = WL.make_state(cfg, 2), WL.make_noise(cfg, 2)
+    got = eng.denoise(state, noise).cpu().numpy()
+    eng.synchronize()
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 3, state, noise, cfg.taus())
+    if dtype == "f32":
+        assert np.max(np.abs(got - ref)) <= FP32_TOL
+    else:
+        rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        assert rel <= BF16_REL and float(np.max(np.abs(got - ref))) <= BF16_ABS, rel
+    eng.close()
+
+
 def test_dtype_probe_rejects_mismatch(tiny):
     cfg, w, sk, sv, frames = tiny
     with pytest.raises(R.ReflexError) as ei:
