@@ -337,6 +337,66 @@ def sweep_chunk(torch, log, horizons=(25, 50, 75, 100)):
     return rows
 
 
+def soak(torch, log, ticks):
+    """Stability stress (Section 4.6): the x64-embedding, 8-env, 8-frame workload
+    streamed for `ticks` ticks in closed loop (each chunk's last action is the
+    next tick's state), with the norm path in fp32 (the method), with a bf16
+    residual stream and fp32 statistics, and fully in bf16.  Per variant: ticks
+    with a non-finite action, the largest |action|, the chunk time, and the
+    deviation from the fp32 trajectory over time (same frames and noise)."""
+    from paper_2607_14695_amd import workloads as WL
+    from paper_2607_14695_amd.reflex import ReflexEngine
+
+    cfg = WL.CONFIGS["pi0_long_bf16"]
+    w, sk, sv, frames, state, noise = _device_inputs(cfg, torch, seed=5)
+    modes = ("fp32", "bf16_fp32_stats", "bf16")
+    engs = {m: ReflexEngine(cfg.replace(norm_precision=m), w, sk, sv) for m in modes}
+    st = {m: state.clone() for m in modes}
+    bad = {m: torch.zeros(ticks, device="cuda") for m in modes}
+    amax = {m: torch.zeros(ticks, device="cuda") for m in modes}
+    dev = {m: torch.zeros(ticks, device="cuda") for m in modes}
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7)
+    t0 = time.perf_counter()
+    for t in range(ticks):
+        nz = torch.randn(noise.shape, generator=gen, device="cuda")
+        outs = {}
+        for m in modes:
+            engs[m].write_frame(frames[t % len(frames)])
+            outs[m] = engs[m].denoise(st[m], nz).clone()
+        for m in modes:
+            o = outs[m]
+            fin = torch.isfinite(o)
+            bad[m][t] = (~fin).any().float()
+            amax[m][t] = torch.where(fin, o.abs(), torch.zeros_like(o)).max()
+            dev[m][t] = (torch.nan_to_num(o, nan=1e30, posinf=1e30, neginf=-1e30) - outs["fp32"]).abs().max()
+            # closed loop; a non-finite action leaves the state where it was
+            nxt = o[:, -1, :cfg.state_dim]
+            st[m] = torch.where(torch.isfinite(nxt), nxt, st[m])
+        if (t + 1) % 250 == 0:
+            torch.cuda.synchronize()
+            log(f"soak tick {t + 1}/{ticks}: " + ", ".join(
+                f"{m} bad={int(bad[m][:t + 1].sum())} dev={float(dev[m][t]):.3g}" for m in modes))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    out = {"workload": "pi0_long_bf16 (8 envs, 256 static + 8x768 ring, token embeddings x64, tau schedule "
+                       "concentrated near 0 and 1), closed loop: state <- last action of the previous chunk",
+           "ticks": ticks, "wall_s": round(wall, 1), "variants": {}}
+    marks = [t for t in (0, 9, 99, 999, 1999, ticks - 1) if t < ticks]
+    for m in modes:
+        b = bad[m].cpu()
+        first = int(b.nonzero()[0]) if b.any() else None
+        out["variants"][m] = {
+            "nonfinite_ticks": int(b.sum()), "first_nonfinite_tick": first,
+            "max_abs_action": round(float(amax[m].max()), 4),
+            "chunk_ms": _event_ms(engs[m], torch, lambda: engs[m].denoise(st[m], noise), 5),
+            "dev_from_fp32_at_tick": {str(t + 1): round(float(dev[m][t]), 6) for t in marks},
+            "dev_from_fp32_max": round(float(dev[m].max()), 6),
+        }
+        engs[m].close()
+    return out
+
+
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
     10 Euler steps, one frame in the window), median of two runs."""
@@ -391,6 +451,8 @@ def main():
                     help="skip the real-time Algorithm 1 scheduler run (about 10 s)")
     ap.add_argument("--sweep", choices=("window", "chunk", "all"),
                     help="instead of the benchmark line, print one JSON line of the window and/or chunk sweeps")
+    ap.add_argument("--soak", type=int, metavar="TICKS",
+                    help="instead of the benchmark line, print one JSON line of the norm-precision soak")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -407,6 +469,11 @@ def main():
 
     def log(msg):
         print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    if args.soak:
+        print(json.dumps({"metric": "soak", "data": "synthetic", "dtype": "bf16", **soak(torch, log, args.soak)}),
+              flush=True)
+        return
 
     if args.sweep:
         out = {"metric": "sweeps", "data": "synthetic", "dtype": "bf16"}

@@ -53,6 +53,16 @@ extern "C" {
 
 #define REFLEX_MAX_STEPS 64
 
+/* Precision of the residual stream and of the RMS statistics of every
+ * AdaRMSNorm.  REFLEX_NORM_FP32 is the method (fp32 statistics, Section 3.2).
+ * The other two reproduce the baselines of the stability stress test
+ * (Section 4.6): a bf16 residual stream with the statistics accumulated in
+ * bf16 (every product and partial sum rounded to bf16), and a bf16 residual
+ * stream with fp32 statistics ("FP32 norm-only"). */
+#define REFLEX_NORM_FP32 0
+#define REFLEX_NORM_BF16 1
+#define REFLEX_NORM_BF16_FP32_STATS 2
+
 /*
  * Shape of the action expert and of the cache.
  *
@@ -109,8 +119,8 @@ typedef struct reflex_config {
   double rope_theta;
   double temb_min_period;
   double temb_max_period;
-  int32_t spare_slot;  /* 0 or 1, see "Cache" above */
-  int32_t reserved;    /* must be 0 */
+  int32_t spare_slot;      /* 0 or 1, see "Cache" above */
+  int32_t norm_precision;  /* REFLEX_NORM_*: REFLEX_NORM_FP32 for the method */
 } reflex_config;
 
 /*

@@ -783,6 +783,340 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
 }
 
 // --------------------------------------------------------------------------
+// tiled, bf16, 256x256 workgroup tile for the large-M shapes (the batched
+// projections, the frame projection, the conditioning MLPs).  Eight waves in
+// 2 (M) x 4 (N), each a 128x64 block of 16x16x32 MFMAs (C^T blocks, 32
+// accumulators of four floats per lane).  The copy into LDS per K stage is
+// (256 + 256) rows x 128 bytes = 64 KB for 256x256x64x2 flops, half the bytes
+// per flop of the 128x128 tile: with every CU copying from L2 at once, the
+// copy rate and not the MFMA rate bounds the smaller tile.  Double-buffered
+// (128 KB of LDS, one workgroup per CU).  Pairs (gated GELU, rotate-half
+// RoPE) put 128 first-half and the matching 128 second-half columns in one
+// tile; a wave holds 32 + 32 of them.
+// --------------------------------------------------------------------------
+constexpr int GBM = 256, GBN = 256;
+constexpr int GSTAGE = (GBM + GBN) * DROWB;  // 64 KB
+
+template <int PAIR>
+RFX_DEV bool big_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
+  const int nx = PAIR == PAIR_NONE ? (p.N + GBN - 1) / GBN : (PAIR == PAIR_N ? p.N / 128 : p.N / 256);
+  const int ny = (p.M + GBM - 1) / GBM;
+  const int total = nx * ny * p.batch * p.splits;
+  const int per = (total + 7) / 8;
+  const int t = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (t >= total) return false;
+  by = t % ny;
+  const int rest = t / ny;
+  bx = rest % nx;
+  bz = rest / nx;
+  return true;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512) void gemm_big(GemmArgs p) {
+  using T = bf16_t;
+  constexpr int PAIR = EpiPair<EPI>::value;
+  __shared__ __attribute__((aligned(16))) unsigned char st0[GSTAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char st1[GSTAGE];
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int wm = wave >> 2, wn = wave & 3;
+  int bx, by, bz;
+  if (!big_tile<PAIR>(p, bx, by, bz)) return;
+  const int z = bz / p.splits, split = bz % p.splits;
+  const int m0 = by * GBM;
+  int n0, pair_off;
+  if constexpr (PAIR == PAIR_HEAD) {
+    const int half = p.qkv.head_dim >> 1, per_head = half / 128;
+    const int h = bx / per_head;
+    n0 = h * p.qkv.head_dim + (bx - h * per_head) * 128;
+    pair_off = half;
+  } else if constexpr (PAIR == PAIR_N) {
+    n0 = bx * 128;
+    pair_off = p.N;
+  } else {
+    n0 = bx * GBN;
+    pair_off = 0;
+  }
+  const int kbeg = split * p.k_per_split;
+  const int kend = min(p.K, kbeg + p.k_per_split);
+  const int nst = (kend - kbeg) / DST;
+
+  const T* A = reinterpret_cast<const T*>(p.A) + (int64_t)z * p.a_bstride;
+  const T* B = reinterpret_cast<const T*>(p.B) + (int64_t)z * p.b_bstride;
+
+  // DMA: wave w, instruction j covers stage rows 8*(4w + (j & 3)) + (lane >> 3)
+  // of A (j < 4) or B (j >= 4): 8 waves x 4 x 8 = 256 rows of each; physical
+  // chunk lane & 7 holds logical chunk (lane & 7) ^ swizzle(row)
+  const T* gsrc[8];
+  {
+    const int rr = lane >> 3, pc = lane & 7;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = 8 * (4 * wave + (j & 3)) + rr;
+      const int lc = pc ^ RFX_GSWZ(row);
+      if (j < 4) {
+        gsrc[j] = A + (int64_t)min(m0 + row, p.M - 1) * p.lda + kbeg + lc * 8;
+      } else {
+        int brw;
+        if (PAIR != PAIR_NONE) {
+          const int c = n0 + (row & 127);
+          brw = row >= 128 ? c + pair_off : c;
+        } else {
+          brw = min(n0 + row, p.N - 1);
+        }
+        gsrc[j] = B + (int64_t)brw * p.ldb + kbeg + lc * 8;
+      }
+    }
+  }
+  auto issue = [&](int st, unsigned char* buf) __attribute__((always_inline)) {
+    const int k0 = st * DST;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = 8 * (4 * wave + (j & 3));
+      __builtin_amdgcn_global_load_lds(gsrc[j] + k0, buf + ((j >= 4 ? GBM : 0) + row) * DROWB, 16, 0, 0);
+    }
+  };
+
+  f32x4_v acc[8][4];
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+
+  int foff[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) foff[kk] = r16 * DROWB + ((4 * kk + g) ^ RFX_GSWZ(r16)) * 16;
+  int brow_l[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    if (PAIR != PAIR_NONE)
+      brow_l[nb] = (nb < 2 ? 0 : 128) + wn * 32 + (nb & 1) * 16;
+    else
+      brow_l[nb] = wn * 64 + nb * 16;
+  }
+
+  auto step = [&](int st, const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt)
+                  __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): this wave's share of stage st
+    // every wave's share is in LDS, and every wave is done with stage st-1,
+    // whose buffer the next copy overwrites
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (st + 1 < nst) issue(st + 1, nxt);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      uint4 bf[4];
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+        bf[nb] = *reinterpret_cast<const uint4*>(cur + (GBM + brow_l[nb]) * DROWB + foff[kk]);
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+        const uint4 af = *reinterpret_cast<const uint4*>(cur + (wm * 128 + mb * 16) * DROWB + foff[kk]);
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) mfma_step(acc[mb][nb], bf[nb], af, T());  // C^T blocks
+      }
+    }
+  };
+
+  if (nst > 0) issue(0, st0);
+  for (int st = 0; st < nst; st += 2) {
+    step(st, st0, st1);
+    if (st + 1 < nst) step(st + 1, st1, st0);
+  }
+
+  // acc[mb][nb]: lane (r16, g) holds output row m0 + wm*128 + mb*16 + r16,
+  // columns 4g .. 4g+3 of column block nb
+#pragma unroll
+  for (int mb = 0; mb < 8; ++mb) {
+    const int grow = m0 + wm * 128 + mb * 16 + r16;
+    if (grow >= p.M) continue;
+    if (PAIR != PAIR_NONE) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const int gcol = n0 + wn * 32 + nb * 16 + 4 * g;
+        const float v[4] = {acc[mb][nb][0], acc[mb][nb][1], acc[mb][nb][2], acc[mb][nb][3]};
+        const float u[4] = {acc[mb][nb + 2][0], acc[mb][nb + 2][1], acc[mb][nb + 2][2], acc[mb][nb + 2][3]};
+        epilogue_store4<EPI>(p, z, split, grow, gcol, v, u);
+      }
+    } else {
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int gcol = n0 + wn * 64 + nb * 16 + 4 * g;
+        const float v[4] = {acc[mb][nb][0], acc[mb][nb][1], acc[mb][nb][2], acc[mb][nb][3]};
+        if (gcol + 3 < p.N) {
+          epilogue_store4<EPI>(p, z, split, grow, gcol, v, v);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (gcol + e < p.N) epilogue_store<EPI, T>(p, z, split, grow, gcol + e, v[e], 0.f);
+        }
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------------------
+// 256x256 tile with 32-element K stages: 32 KB per stage, five stages (the
+// whole 160 KB of LDS) and four copies in flight.  With 64-element stages
+// only one 64 KB copy is in flight per CU while a stage is computed, and the
+// copy latency, not the bandwidth, sets the pace.  A 64-byte stage row holds
+// four 16-byte chunks; chunk c of row r sits at c ^ ((r >> 2) & 3), so the 16
+// rows a fragment read touches with one chunk each fall on distinct banks.
+// NST (stages per workgroup) is a compile-time constant and the stage loop
+// fully unrolled, so the compiler knows which buffer every copy in flight
+// targets and does not wait for all copies before reading LDS.
+// --------------------------------------------------------------------------
+constexpr int HROWB = 64;                       // bytes per stage row
+constexpr int HSTAGE = (GBM + GBN) * HROWB;     // 32 KB
+#define RFX_HSWZ(r) (((r) >> 2) & 3)
+
+template <int EPI, int NST>
+__global__ __launch_bounds__(512) void gemm_big5(GemmArgs p) {
+  using T = bf16_t;
+  constexpr int PAIR = EpiPair<EPI>::value;
+  constexpr int NS = 5;
+  __shared__ __attribute__((aligned(16))) unsigned char st0[HSTAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char st1[HSTAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char st2[HSTAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char st3[HSTAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char st4[HSTAGE];
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int wm = wave >> 2, wn = wave & 3;
+  int bx, by, bz;
+  if (!big_tile<PAIR>(p, bx, by, bz)) return;
+  const int z = bz / p.splits, split = bz % p.splits;
+  const int m0 = by * GBM;
+  int n0, pair_off;
+  if constexpr (PAIR == PAIR_HEAD) {
+    const int half = p.qkv.head_dim >> 1, per_head = half / 128;
+    const int h = bx / per_head;
+    n0 = h * p.qkv.head_dim + (bx - h * per_head) * 128;
+    pair_off = half;
+  } else if constexpr (PAIR == PAIR_N) {
+    n0 = bx * 128;
+    pair_off = p.N;
+  } else {
+    n0 = bx * GBN;
+    pair_off = 0;
+  }
+  const int kbeg = split * p.k_per_split;
+
+  const T* A = reinterpret_cast<const T*>(p.A) + (int64_t)z * p.a_bstride;
+  const T* B = reinterpret_cast<const T*>(p.B) + (int64_t)z * p.b_bstride;
+
+  // DMA: wave w, instruction j covers stage rows 16*(2w + (j & 1)) + (lane >> 2)
+  // of A (j < 2) or B (j >= 2): 8 waves x 2 x 16 = 256 rows of each; physical
+  // chunk lane & 3 holds logical chunk (lane & 3) ^ swizzle(row)
+  const T* gsrc[4];
+  {
+    const int rr = lane >> 2, pc = lane & 3;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = 16 * (2 * wave + (j & 1)) + rr;
+      const int lc = pc ^ RFX_HSWZ(row);
+      if (j < 2) {
+        gsrc[j] = A + (int64_t)min(m0 + row, p.M - 1) * p.lda + kbeg + lc * 8;
+      } else {
+        int brw;
+        if (PAIR != PAIR_NONE) {
+          const int c = n0 + (row & 127);
+          brw = row >= 128 ? c + pair_off : c;
+        } else {
+          brw = min(n0 + row, p.N - 1);
+        }
+        gsrc[j] = B + (int64_t)brw * p.ldb + kbeg + lc * 8;
+      }
+    }
+  }
+  auto issue = [&](int st, unsigned char* buf) __attribute__((always_inline)) {
+    const int k0 = st * 32;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = 16 * (2 * wave + (j & 1));
+      __builtin_amdgcn_global_load_lds(gsrc[j] + k0, buf + ((j >= 2 ? GBM : 0) + row) * HROWB, 16, 0, 0);
+    }
+  };
+
+  f32x4_v acc[8][4];
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+
+  // fragment rows are 16-aligned, so the swizzle of row r16 + 16i is that of r16
+  const int foff = r16 * HROWB + (g ^ RFX_HSWZ(r16)) * 16;
+  int brow_l[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    if (PAIR != PAIR_NONE)
+      brow_l[nb] = (nb < 2 ? 0 : 128) + wn * 32 + (nb & 1) * 16;
+    else
+      brow_l[nb] = wn * 64 + nb * 16;
+  }
+
+  auto step = [&](int st, const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt)
+                  __attribute__((always_inline)) {
+    // stage st is complete once at most (stages issued after it) x 4 of this
+    // wave's copies are outstanding
+    const int after = (st + NS - 2 < NST ? st + NS - 2 : NST - 1) - st;
+    if (after >= 3)
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 12);
+    else if (after == 2)
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 8);
+    else if (after == 1)
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 4);
+    else
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+    // every wave's share of stage st is in LDS, and every wave is done with
+    // stage st-1, whose buffer the next copy overwrites
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (st + NS - 1 < NST) issue(st + NS - 1, nxt);
+    uint4 bf[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+      bf[nb] = *reinterpret_cast<const uint4*>(cur + (GBM + brow_l[nb]) * HROWB + foff);
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const uint4 af = *reinterpret_cast<const uint4*>(cur + (wm * 128 + mb * 16) * HROWB + foff);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) mfma_step(acc[mb][nb], bf[nb], af, T());  // C^T blocks
+    }
+  };
+
+  unsigned char* const bufs[NS] = {st0, st1, st2, st3, st4};
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st)
+    if (st < NST) issue(st, bufs[st]);
+#pragma unroll
+  for (int st = 0; st < NST; ++st) step(st, bufs[st % NS], bufs[(st + NS - 1) % NS]);
+
+#pragma unroll
+  for (int mb = 0; mb < 8; ++mb) {
+    const int grow = m0 + wm * 128 + mb * 16 + r16;
+    if (grow >= p.M) continue;
+    if (PAIR != PAIR_NONE) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const int gcol = n0 + wn * 32 + nb * 16 + 4 * g;
+        const float v[4] = {acc[mb][nb][0], acc[mb][nb][1], acc[mb][nb][2], acc[mb][nb][3]};
+        const float u[4] = {acc[mb][nb + 2][0], acc[mb][nb + 2][1], acc[mb][nb + 2][2], acc[mb][nb + 2][3]};
+        epilogue_store4<EPI>(p, z, split, grow, gcol, v, u);
+      }
+    } else {
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int gcol = n0 + wn * 64 + nb * 16 + 4 * g;
+        const float v[4] = {acc[mb][nb][0], acc[mb][nb][1], acc[mb][nb][2], acc[mb][nb][3]};
+        epilogue_store4<EPI>(p, z, split, grow, gcol, v, v);
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------------------
 // host side
 // --------------------------------------------------------------------------
 static int skinny_mb(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
@@ -882,6 +1216,23 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
   // (vector epilogue stores: output rows start 16-byte aligned)
   if (sizeof(T) == 2 && a.K % DST == 0 && a.k_per_split % DST == 0 && a.N % 4 == 0 && a.ldo % 4 == 0) {
     const int total = grid.x * grid.y * grid.z;
+    // 256x256 tiles when there are at least 512 rows and the large tiles
+    // alone give at least half a wave of workgroups
+    const bool pair_ok = (PAIR == PAIR_NONE && a.N % GBN == 0) || (PAIR == PAIR_N && a.N % 128 == 0) ||
+                         (PAIR == PAIR_HEAD && (a.qkv.head_dim / 2) % 128 == 0);
+    const int bx = PAIR == PAIR_NONE ? (a.N + GBN - 1) / GBN : (PAIR == PAIR_N ? a.N / 128 : a.N / 256);
+    const int btotal = bx * ((a.M + GBM - 1) / GBM) * a.batch * a.splits;
+    if (pair_ok && a.M >= 512 && btotal >= 128 && a.k_per_split / DST >= 8) {
+      const dim3 g((btotal + 7) / 8 * 8);
+      const bool whole = a.K == a.k_per_split * a.splits;  // every split a full K range
+      if (whole && a.k_per_split == 1024)
+        RFX_LAUNCH((gemm_big5<EPI, 32>), g, dim3(512), 0, s, a);
+      else if (whole && a.k_per_split == 2048)
+        RFX_LAUNCH((gemm_big5<EPI, 64>), g, dim3(512), 0, s, a);
+      else
+        RFX_LAUNCH((gemm_big<EPI>), g, dim3(512), 0, s, a);
+      return;
+    }
     // four-stage unrolled pipeline (one workgroup per CU) when one wave of
     // workgroups covers the grid; else the two-stage one (two per CU)
     const int nst = a.k_per_split / DST;

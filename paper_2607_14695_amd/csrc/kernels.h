@@ -88,6 +88,13 @@ template <typename T> hipError_t launch_attn_merge(const AttnArgs& a, int head_d
 int attention_pick_splits(int B, int rows, int max_keys, int elem_bytes);
 int attention_rows_per_block(int elem_bytes);
 
+// Precision of the residual stream and of the RMS statistics.  NORM_FP32 is
+// the method (fp32 statistics, Section 3.2); the other two reproduce the
+// baselines of the stability ablation: a bf16 residual stream with the
+// statistics accumulated in bf16 (every product and partial sum rounded), or
+// with fp32 statistics ("fp32 norm-only").
+enum NormMode : int { NORM_FP32 = 0, NORM_BF16 = 1, NORM_BF16_FP32_STATS = 2 };
+
 // Token embedding + first AdaRMSNorm: h = embed_scale*[s W_s^T ; x W_ain^T], y = ada(h).
 struct EmbedArgs {
   const float* x;        // [B][H][da]
@@ -99,6 +106,7 @@ struct EmbedArgs {
   void* y;               // [B*T][D]
   int B, T, D, ds, da;
   float embed_scale, eps;
+  int norm_mode;         // NormMode
 };
 template <typename T> hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s);
 
@@ -113,6 +121,7 @@ struct ResidArgs {
   void* y;                // [M][D]
   int M, T, D;
   float eps;
+  int norm_mode;          // NormMode
 };
 template <typename T> hipError_t launch_resid_norm(const ResidArgs& a, hipStream_t s);
 
@@ -129,6 +138,7 @@ struct FinalArgs {
   float* x_out;           // [B][H][da]
   int B, T, D, da;
   float dt, eps;
+  int norm_mode;          // NormMode
 };
 template <typename T> hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s);
 

@@ -45,6 +45,35 @@ RFX_DEV float4 sum_parts(const float* pp, int64_t stride, int nparts) {
   return acc;
 }
 
+// bf16 rounding of an fp32 value (round to nearest even), kept in fp32
+RFX_DEV float rbf(float x) { return bf2f(f2bf(x)); }
+RFX_DEV float4 rbf4(float4 v) { return make_float4(rbf(v.x), rbf(v.y), rbf(v.z), rbf(v.w)); }
+
+// sum of squares of 4 values added to ss: fp32, or bf16 arithmetic with every
+// product and every partial sum rounded
+RFX_DEV float add_ssq(float ss, float4 v, bool bf) {
+  if (!bf) return ss + v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  ss = rbf(ss + rbf(v.x * v.x));
+  ss = rbf(ss + rbf(v.y * v.y));
+  ss = rbf(ss + rbf(v.z * v.z));
+  return rbf(ss + rbf(v.w * v.w));
+}
+
+// Block sum of the 256 per-thread partials and the inverse RMS 1/sqrt(ss/D +
+// eps).  In bf16 arithmetic every partial sum, the mean and the result are
+// rounded.
+RFX_DEV float inv_rms(float ss, int D, float eps, bool bf, float* red) {
+  if (!bf) return rsqrtf(block_sum_256(ss, red) / (float)D + eps);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss = rbf(ss + __shfl_xor(ss, off, 64));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  const float tot = rbf(rbf(red[0] + red[1]) + rbf(red[2] + red[3]));
+  return rbf(rsqrtf(rbf(rbf(tot / (float)D) + eps)));
+}
+
 // y = v * r * (1 + scale) + shift for 4 columns
 RFX_DEV float4 ada4(float4 v, float r, float4 sc, float4 sh) {
   return make_float4(v.x * r * (1.f + sc.x) + sh.x, v.y * r * (1.f + sc.y) + sh.y, v.z * r * (1.f + sc.z) + sh.z,
@@ -79,15 +108,16 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(EmbedArgs p) {
     }
     for (; e < n_in; ++e) acc += to_f(w[e]) * in[e];
     acc *= p.embed_scale;
+    if (p.norm_mode != NORM_FP32) acc = rbf(acc);  // bf16 residual stream
     hs[c] = acc;
-    ss += acc * acc;
+    ss = add_ssq(ss, make_float4(acc, 0.f, 0.f, 0.f), p.norm_mode == NORM_BF16);
   }
-  const float tot = block_sum_256(ss, red);
-  const float r = rsqrtf(tot / (float)p.D + p.eps);
+  const float r = inv_rms(ss, p.D, p.eps, p.norm_mode == NORM_BF16, red);
   const float* mod = p.mod + (int64_t)b * 3 * p.D;
   for (int c = threadIdx.x; c < p.D; c += 256) {
     p.h[(int64_t)m * p.D + c] = hs[c];
-    const float y = hs[c] * r * (1.f + mod[c]) + mod[p.D + c];
+    const float xr = p.norm_mode == NORM_BF16 ? rbf(hs[c] * r) : hs[c] * r;
+    const float y = xr * (1.f + mod[c]) + mod[p.D + c];
     reinterpret_cast<T*>(p.y)[(int64_t)m * p.D + c] = from_f<T>(y);
   }
 }
@@ -116,17 +146,20 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(ResidArgs p) {
     const float4 acc = sum_parts(p.parts + (int64_t)m * p.D + c, p.part_stride, p.nparts);
     const float4 h = ld4f(p.h + (int64_t)m * p.D + c);
     const float4 gt = ld4f(gmod + c);
-    const float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+    float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+    if (p.norm_mode != NORM_FP32) v = rbf4(v);  // bf16 residual stream
     hs[c4] = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    ss = add_ssq(ss, v, p.norm_mode == NORM_BF16);
   }
-  const float tot = block_sum_256(ss, red);
-  const float r = rsqrtf(tot / (float)p.D + p.eps);
+  const float r = inv_rms(ss, p.D, p.eps, p.norm_mode == NORM_BF16, red);
   for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
     const int c = c4 * 4;
     const float4 v = hs[c4];
     st4(p.h + (int64_t)m * p.D + c, v);
-    st4(reinterpret_cast<T*>(p.y) + (int64_t)m * p.D + c, ada4(v, r, ld4f(nmod + c), ld4f(nmod + p.D + c)));
+    const float4 sc = ld4f(nmod + c), sh = ld4f(nmod + p.D + c);
+    const float4 y = p.norm_mode == NORM_BF16 ? ada4(rbf4(make_float4(v.x * r, v.y * r, v.z * r, v.w * r)), 1.f, sc, sh)
+                                              : ada4(v, r, sc, sh);
+    st4(reinterpret_cast<T*>(p.y) + (int64_t)m * p.D + c, y);
   }
 }
 
@@ -157,15 +190,18 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
     const float4 acc = sum_parts(p.parts + m * p.D + c, p.part_stride, p.nparts);
     const float4 h = ld4f(p.h + m * p.D + c);
     const float4 gt = ld4f(gmod + c);
-    const float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+    float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+    if (p.norm_mode != NORM_FP32) v = rbf4(v);  // bf16 residual stream
     ys[c4] = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    ss = add_ssq(ss, v, p.norm_mode == NORM_BF16);
   }
-  const float tot = block_sum_256(ss, red);
-  const float r = rsqrtf(tot / (float)p.D + p.eps);
+  const float r = inv_rms(ss, p.D, p.eps, p.norm_mode == NORM_BF16, red);
   for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
     const int c = c4 * 4;
-    ys[c4] = ada4(ys[c4], r, ld4f(fmod + c), ld4f(fmod + p.D + c));
+    const float4 v = ys[c4];
+    const float4 sc = ld4f(fmod + c), sh = ld4f(fmod + p.D + c);
+    ys[c4] = p.norm_mode == NORM_BF16 ? ada4(rbf4(make_float4(v.x * r, v.y * r, v.z * r, v.w * r)), 1.f, sc, sh)
+                                      : ada4(v, r, sc, sh);
   }
   __syncthreads();
   // v[a] = sum_c y[c] W[a][c]: eight threads per output, each a strided

@@ -121,7 +121,8 @@ int validate(const reflex_config* c) {
   if (c->static_len < 0 || c->static_len % 8) return REFLEX_EINVAL;
   if (c->frame_tokens < 8 || c->frame_tokens % 8) return REFLEX_EINVAL;
   if (c->window_frames < 1) return REFLEX_EINVAL;
-  if ((c->spare_slot != 0 && c->spare_slot != 1) || c->reserved != 0) return REFLEX_EINVAL;
+  if (c->spare_slot != 0 && c->spare_slot != 1) return REFLEX_EINVAL;
+  if (c->norm_precision < REFLEX_NORM_FP32 || c->norm_precision > REFLEX_NORM_BF16_FP32_STATS) return REFLEX_EINVAL;
   if (c->frame_dim < 0 || c->frame_dim % 8) return REFLEX_EINVAL;
   if (c->batch < 1 || c->batch > 4096) return REFLEX_EINVAL;
   if (c->max_steps < 1 || c->max_steps > REFLEX_MAX_STEPS) return REFLEX_EINVAL;
@@ -365,7 +366,7 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
     const float* x_in = (k == 0) ? noise : out;
     if (mode == REFLEX_MODE_STANDARD) RFX_TRY(reencode_history<T>(ctx, src, L));
     EmbedArgs ea{x_in, state, ctx->w.w_state, ctx->w.w_ain, mod_at(0, k), W.h, W.y,
-                 B, Tn, D, c.state_dim, c.action_dim, c.embed_scale, c.rms_eps};
+                 B, Tn, D, c.state_dim, c.action_dim, c.embed_scale, c.rms_eps, c.norm_precision};
     RFX_TRY(L.run(PC_EMBED, [&] { return launch_embed_norm<T>(ea, st); }));
     for (int l = 0; l < c.n_layers; ++l) {
       GemmArgs q{};
@@ -406,7 +407,7 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
       RFX_TRY(L.run(PC_O, [&] { return launch_gemm<T>(og, EPI_F32, st); }));
 
       ResidArgs r1{W.h, W.rparts, rpart_stride, P.o.splits, mod_at(2 * l, k), mod_at(2 * l + 1, k), W.y,
-                   M, Tn, D, c.rms_eps};
+                   M, Tn, D, c.rms_eps, c.norm_precision};
       RFX_TRY(L.run(PC_RESID, [&] { return launch_resid_norm<T>(r1, st); }));
 
       GemmArgs gu{};
@@ -425,13 +426,14 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
 
       if (l + 1 < c.n_layers) {
         ResidArgs r2{W.h, W.rparts, rpart_stride, P.down.splits, mod_at(2 * l + 1, k), mod_at(2 * l + 2, k),
-                     W.y, M, Tn, D, c.rms_eps};
+                     W.y, M, Tn, D, c.rms_eps, c.norm_precision};
         RFX_TRY(L.run(PC_RESID, [&] { return launch_resid_norm<T>(r2, st); }));
       }
     }
     const float dt = (float)((double)taus[k + 1] - (double)taus[k]);
     FinalArgs fa{W.h, W.rparts, rpart_stride, P.down.splits, mod_at(2 * c.n_layers - 1, k),
-                 mod_at(2 * c.n_layers, k), ctx->w.w_aout, x_in, out, B, Tn, D, c.action_dim, dt, c.rms_eps};
+                 mod_at(2 * c.n_layers, k), ctx->w.w_aout, x_in, out, B, Tn, D, c.action_dim, dt, c.rms_eps,
+                 c.norm_precision};
     RFX_TRY(L.run(PC_FINAL, [&] { return launch_final_euler<T>(fa, st); }));
   }
   return REFLEX_OK;

@@ -35,6 +35,7 @@ MODE_REFLEX = 0
 MODE_STANDARD = 1
 MODE_NAIVE = 2
 MODES = {"reflex": MODE_REFLEX, "standard": MODE_STANDARD, "naive": MODE_NAIVE}
+NORM_PRECISIONS = {"fp32": 0, "bf16": 1, "bf16_fp32_stats": 2}
 
 c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 
@@ -47,7 +48,7 @@ class ConfigC(ctypes.Structure):
         ("frame_tokens", c_i32), ("window_frames", c_i32), ("frame_dim", c_i32), ("batch", c_i32),
         ("dtype", c_i32), ("mod_mode", c_i32), ("max_steps", c_i32), ("rms_eps", c_f32),
         ("embed_scale", c_f32), ("rope_theta", c_f64), ("temb_min_period", c_f64),
-        ("temb_max_period", c_f64), ("spare_slot", c_i32), ("reserved", c_i32),
+        ("temb_max_period", c_f64), ("spare_slot", c_i32), ("norm_precision", c_i32),
     ]
 
 
@@ -141,7 +142,8 @@ def config_to_c(cfg: ReflexConfig, max_steps: Optional[int] = None) -> ConfigC:
         frame_dim=cfg.frame_dim, batch=cfg.batch, dtype=DTYPE_BF16 if cfg.bf16 else DTYPE_F32,
         mod_mode=MOD_SCALE_ONLY if cfg.mod_mode == "scale_only" else MOD_FULL, max_steps=ms,
         rms_eps=cfg.rms_eps, embed_scale=cfg.embed_scale, rope_theta=cfg.rope_theta,
-        temb_min_period=cfg.temb_min_period, temb_max_period=cfg.temb_max_period, spare_slot=cfg.spare_slot)
+        temb_min_period=cfg.temb_min_period, temb_max_period=cfg.temb_max_period, spare_slot=cfg.spare_slot,
+        norm_precision=NORM_PRECISIONS[cfg.norm_precision])
 
 
 def query_sizes(cfg: ReflexConfig, max_steps: Optional[int] = None) -> Tuple[int, int]:

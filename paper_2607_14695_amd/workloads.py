@@ -70,6 +70,8 @@ class ReflexConfig:
     mod_mode: str = "full"  # "full" (scale/shift/gate) or "scale_only" (Eq. 2)
     # GPU cache layout only: 1 = one spare ring slot for pipelined frame writes
     spare_slot: int = 0
+    # GPU numerics ablation only: "fp32" (the method), "bf16", "bf16_fp32_stats"
+    norm_precision: str = "fp32"
     # workload driver
     ticks: int = 1
     tau_schedule: Optional[Tuple[float, ...]] = None

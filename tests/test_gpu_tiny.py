@@ -255,6 +255,30 @@ def test_long_chunks_two_dynamic_tiles(dtype, horizon):
     eng.close()
 
 
+def test_norm_precision_variants():
+    """The two baselines of the stability stress test (a bf16 residual stream
+    with bf16 or fp32 RMS statistics) stay finite and close to the oracle on a
+    short chunk, differ from the method, and the method is unchanged by the
+    option's existence (checked by every other test)."""
+    cfg = RAGGED.replace(name="normprec", dtype="bf16", head_dim=128, frame_dim=0)
+    w, sk, sv, frames = _setup(cfg, 3)
+    state, noise = WL.make_state(cfg, 2), WL.make_noise(cfg, 2)
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 3, state, noise, cfg.taus())
+    got = {}
+    for prec in ("fp32", "bf16_fp32_stats", "bf16"):
+        eng = R.ReflexEngine(cfg.replace(norm_precision=prec), w, sk, sv)
+        for t in range(3):
+            eng.write_frame(frames[t])
+        got[prec] = eng.denoise(state, noise).cpu().numpy()
+        eng.close()
+        rel = float(np.linalg.norm(got[prec] - ref) / np.linalg.norm(ref))
+        print(prec, f"rel-L2 vs oracle {rel:.2e}", flush=True)
+        assert np.isfinite(got[prec]).all()
+        assert rel <= (BF16_REL if prec == "fp32" else 5e-2), (prec, rel)
+    for prec in ("bf16_fp32_stats", "bf16"):
+        assert np.max(np.abs(got[prec] - got["fp32"])) > 0.0, prec
+
+
 def test_dtype_probe_rejects_mismatch(tiny):
     cfg, w, sk, sv, frames = tiny
     with pytest.raises(R.ReflexError) as ei:
