@@ -175,7 +175,7 @@ def _mode_chunks(eng, state, noise, torch, n):
     events on the engine's stream) under each cache strategy, once the ring is
     full, plus how far the naive strategy's actions land from the method's."""
     out, acts = {}, {}
-    for mode in ("reflex", "standard", "naive"):
+    for mode in ("reflex", "standard", "naive", "unfused"):
         acts[mode] = eng.denoise(state, noise, mode=mode).clone()  # captures the graph
         eng.denoise(state, noise, mode=mode)
         eng.synchronize()
@@ -187,6 +187,8 @@ def _mode_chunks(eng, state, noise, torch, n):
         eng.synchronize()
         out[f"{mode}_chunk_ms"] = round(a.elapsed_time(b) / n, 4)
     out["standard_over_reflex"] = round(out["standard_chunk_ms"] / out["reflex_chunk_ms"], 3)
+    # the fusion ablation: the same chunk with every fusion undone
+    out["unfused_over_reflex"] = round(out["unfused_chunk_ms"] / out["reflex_chunk_ms"], 3)
     out["standard_equals_reflex"] = bool(torch.equal(acts["reflex"], acts["standard"]))
     d = (acts["naive"] - acts["reflex"]).double()
     out["naive_vs_reflex_mse"] = float((d * d).mean())

@@ -247,6 +247,9 @@ int reflex_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise
                                   prefix and every window frame are encoded into the cache again */
 #define REFLEX_MODE_NAIVE 2    /* a K/V cache that ignores the timestep: the dynamic K/V computed at
                                   the first Euler step are reused at every later step */
+#define REFLEX_MODE_UNFUSED 3  /* the method without operator fusion (the fusion ablation of Section
+                                  4.6): conditioning MLPs at every step, RoPE, gated GELU, residual add,
+                                  norm, action head and Euler update as separate launches */
 
 /* Sources the Standard strategy re-encodes at every step. */
 typedef struct reflex_sources {
@@ -264,7 +267,7 @@ typedef struct reflex_sources {
  * Section 4: the full-recomputation "Standard" baseline and the "Naive Cache"
  * negative control.  Arguments as reflex_denoise_chunk, plus:
  *   mode: REFLEX_MODE_REFLEX (identical to reflex_denoise_chunk),
- *         REFLEX_MODE_STANDARD or REFLEX_MODE_NAIVE;
+ *         REFLEX_MODE_STANDARD, REFLEX_MODE_NAIVE or REFLEX_MODE_UNFUSED;
  *   src:  required for REFLEX_MODE_STANDARD, ignored otherwise (may be NULL).
  *         The frame and static buffers are read by the device work of this
  *         call and must stay unchanged until it completes.

@@ -153,6 +153,46 @@ template <typename T> hipError_t launch_cond(void* cond, const float* state, con
                                              int B, int D, int ds, double min_p, double max_p,
                                              hipStream_t s);
 
+// Separate passes used by the unfused schedule of the fusion ablation: the
+// work the fused kernels do in GEMM epilogues and in the residual/norm kernel.
+struct ResidAddArgs {        // h += gate (.) sum_s parts[s]
+  float* h;
+  const float* parts;
+  int64_t part_stride;
+  int nparts;
+  const float* gate_mod;     // [B][3D], gate at +2D
+  int M, T, D;
+};
+hipError_t launch_resid_add(const ResidAddArgs& a, hipStream_t s);
+struct NormArgs {            // y = h / rms(h) * (1 + scale) + shift
+  const float* h;
+  const float* norm_mod;     // [B][3D]
+  void* y;
+  int M, T, D;
+  float eps;
+};
+template <typename T> hipError_t launch_norm(const NormArgs& a, hipStream_t s);
+struct RopeScatterArgs {     // RoPE on the q and k heads of fp32 [M][(Hq+2)*dh] rows, scattered like EPI_ROPE
+  const float* qkv;
+  QkvOut out;
+  int M;
+};
+template <typename T> hipError_t launch_rope_scatter(const RopeScatterArgs& a, hipStream_t s);
+struct GeluMulArgs {         // z[m][c] = gelu_tanh(u[m][c]) * u[m][F + c]
+  const float* u;
+  void* z;
+  int M, F;
+};
+template <typename T> hipError_t launch_gelu_mul(const GeluMulArgs& a, hipStream_t s);
+struct EulerArgs {           // x_out = x_in + dt * v (action rows 1..T-1 of v [B*T][da])
+  const float* v;
+  const float* x_in;
+  float* x_out;
+  int B, T, da;
+  float dt;
+};
+hipError_t launch_euler(const EulerArgs& a, hipStream_t s);
+
 // Sets the device tick state {frames, n_valid, dyn_pos0, hole_row} that the
 // next chunk on this stream reads (one thread; the chunk's kernels follow in
 // stream order).

@@ -75,9 +75,11 @@ struct Workspace {
   float* frame_scratch;
   void* naive_k;   // [L][B][T][dh] dynamic K of the first Euler step (Naive mode)
   void* naive_vt;  // [L][B][dh][tpad] dynamic V^T of the first Euler step (Naive mode)
+  float* uf_wide;  // [M][max(Nqkv, 2*mlp)] fp32 projection outputs (unfused schedule)
+  float* uf_v;     // [M][da] fp32 action-head output (unfused schedule)
 };
 
-constexpr int kWsParts = 20;
+constexpr int kWsParts = 22;
 
 struct Plan {
   int T, M, S, Nqkv, C, R, slots, rows_pad, tpad, nrb, eb;
@@ -181,6 +183,8 @@ Plan make_plan(const reflex_config* c) {
   p.naive_vt_stride = align256(sz[10]);
   sz[18] = L * p.naive_k_stride;                                          // naive_k
   sz[19] = L * p.naive_vt_stride;                                         // naive_vt
+  sz[20] = (size_t)p.M * (p.Nqkv > 2 * c->mlp_dim ? p.Nqkv : 2 * c->mlp_dim) * sizeof(float);  // uf_wide
+  sz[21] = (size_t)p.M * c->action_dim * sizeof(float);                   // uf_v
   size_t off = 0;
   for (int i = 0; i < kWsParts; ++i) {
     p.off[i] = off;
@@ -439,8 +443,130 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
   return REFLEX_OK;
 }
 
+// The unfused schedule of the operator-fusion ablation (Section 4.6): the
+// same chunk with the conditioning MLPs evaluated at every step instead of
+// once per chunk, RoPE and the gated GELU applied by their own kernels to fp32
+// projection outputs, the residual add, the norm, the action head and the
+// Euler update as separate launches.  Attention and the token embedding are
+// the fused path's.
+template <typename T>
+int enqueue_chunk_unfused(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
+                          float* out, bool prof) {
+  const reflex_config& c = ctx->cfg;
+  const Plan& P = ctx->plan;
+  const Workspace& W = ctx->ws;
+  hipStream_t st = ctx->stream;
+  Launcher L{ctx, prof};
+  const int B = c.batch, Tn = P.T, M = P.M, D = c.width, dh = c.head_dim, Hq = c.n_q_heads, F = c.mlp_dim;
+  const int64_t site_stride = (int64_t)c.max_steps * B * 3 * D;
+  auto mod_at = [&](int site, int k) { return W.mod + site * site_stride + (int64_t)k * B * 3 * D; };
+  const size_t eb = sizeof(T);
+  const int64_t rpart_stride = (int64_t)M * D;
+
+  RFX_TRY(L.run(PC_ROPE, [&] { return launch_rope_table(W.rope_dyn, W.tick + 2, 0, Tn, dh, c.rope_theta, st); }));
+  for (int k = 0; k < steps; ++k) {
+    // conditioning MLPs of this step only
+    TauTable tt;
+    memset(&tt, 0, sizeof(tt));
+    tt.tau[0] = taus[k];
+    RFX_TRY(L.run(PC_MOD, [&] {
+      return launch_cond<T>(W.cond, state, tt, 1, B, D, c.state_dim, c.temb_min_period, c.temb_max_period, st);
+    }));
+    GemmArgs g1{};
+    g1.A = W.cond; g1.lda = P.C;
+    g1.B = ctx->w.w_mod1; g1.ldb = P.C;
+    g1.out = W.hid; g1.ldo = (int64_t)P.S * c.cond_hidden;
+    g1.M = B; g1.N = P.S * c.cond_hidden; g1.K = P.C;
+    g1.splits = 1; g1.k_per_split = P.C + 64; g1.batch = 1;
+    RFX_TRY(L.run(PC_MOD, [&] { return launch_gemm<T>(g1, EPI_SILU, st); }));
+    GemmArgs g2{};
+    g2.A = W.hid; g2.lda = (int64_t)P.S * c.cond_hidden; g2.a_bstride = c.cond_hidden;
+    g2.B = ctx->w.w_mod2; g2.ldb = c.cond_hidden; g2.b_bstride = (int64_t)3 * D * c.cond_hidden;
+    g2.out = mod_at(0, k); g2.ldo = 3 * D; g2.o_bstride = site_stride;
+    g2.M = B; g2.N = 3 * D; g2.K = c.cond_hidden;
+    g2.splits = 1; g2.k_per_split = c.cond_hidden + 64; g2.batch = P.S;
+    g2.mod_width = c.mod_mode == REFLEX_MOD_SCALE_ONLY ? D : 0;
+    RFX_TRY(L.run(PC_MOD, [&] { return launch_gemm<T>(g2, EPI_MOD, st); }));
+
+    const float* x_in = (k == 0) ? noise : out;
+    EmbedArgs ea{x_in, state, ctx->w.w_state, ctx->w.w_ain, mod_at(0, k), W.h, W.y,
+                 B, Tn, D, c.state_dim, c.action_dim, c.embed_scale, c.rms_eps, c.norm_precision};
+    RFX_TRY(L.run(PC_EMBED, [&] { return launch_embed_norm<T>(ea, st); }));
+    for (int l = 0; l < c.n_layers; ++l) {
+      GemmArgs q{};
+      q.A = W.y; q.lda = D;
+      q.B = (const char*)ctx->w.w_qkv + (size_t)l * P.Nqkv * D * eb; q.ldb = D;
+      q.out = W.uf_wide; q.ldo = P.Nqkv;
+      q.M = M; q.N = P.Nqkv; q.K = D; q.splits = 1; q.k_per_split = D + 128; q.batch = 1;
+      RFX_TRY(L.run(PC_QKV, [&] { return launch_gemm<T>(q, EPI_F32, st); }));
+      RopeScatterArgs rs{W.uf_wide, QkvOut{W.rope_dyn, W.q, W.kd, W.vdt, Tn, Hq, dh, P.rows_pad, P.tpad}, M};
+      RFX_TRY(L.run(PC_ROPE, [&] { return launch_rope_scatter<T>(rs, st); }));
+
+      AttnArgs aa{};
+      aa.q = W.q; aa.kd = W.kd; aa.vdt = W.vdt; aa.tpad = P.tpad;
+      aa.cache_k = (const char*)ctx->cache_k + (size_t)l * P.R * dh * eb;
+      aa.cache_vt = (const char*)ctx->cache_vt + (size_t)l * P.R * dh * eb;
+      aa.ck_bstride = (int64_t)c.n_layers * P.R * dh;
+      aa.n_valid = reinterpret_cast<const int32_t*>(W.tick + 1);
+      aa.hole_row = reinterpret_cast<const int32_t*>(W.tick + 3);
+      aa.static_len = c.static_len; aa.frame_tokens = c.frame_tokens; aa.R = P.R;
+      aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits;
+      aa.part_o = W.part_o; aa.part_ml = W.part_ml;
+      aa.rows_pad = P.rows_pad; aa.out = W.o;
+      RFX_TRY(L.run(PC_ATTN, [&] { return launch_attention<T>(aa, dh, st); }));
+      if (P.attn_splits > 1) RFX_TRY(L.run(PC_MERGE, [&] { return launch_attn_merge<T>(aa, dh, st); }));
+
+      GemmArgs og{};
+      og.A = W.o; og.lda = (int64_t)Hq * dh;
+      og.B = (const char*)ctx->w.w_o + (size_t)l * D * Hq * dh * eb; og.ldb = (int64_t)Hq * dh;
+      og.out = W.rparts; og.ldo = D; og.o_split_stride = rpart_stride;
+      og.M = M; og.N = D; og.K = Hq * dh; og.splits = P.o.splits; og.k_per_split = P.o.kps; og.batch = 1;
+      RFX_TRY(L.run(PC_O, [&] { return launch_gemm<T>(og, EPI_F32, st); }));
+      ResidAddArgs ra1{W.h, W.rparts, rpart_stride, P.o.splits, mod_at(2 * l, k), M, Tn, D};
+      RFX_TRY(L.run(PC_RESID, [&] { return launch_resid_add(ra1, st); }));
+      NormArgs n1{W.h, mod_at(2 * l + 1, k), W.y, M, Tn, D, c.rms_eps};
+      RFX_TRY(L.run(PC_RESID, [&] { return launch_norm<T>(n1, st); }));
+
+      GemmArgs gu{};
+      gu.A = W.y; gu.lda = D;
+      gu.B = (const char*)ctx->w.w_gu + (size_t)l * 2 * F * D * eb; gu.ldb = D;
+      gu.out = W.uf_wide; gu.ldo = 2 * F;
+      gu.M = M; gu.N = 2 * F; gu.K = D; gu.splits = 1; gu.k_per_split = D + 128; gu.batch = 1;
+      RFX_TRY(L.run(PC_GU, [&] { return launch_gemm<T>(gu, EPI_F32, st); }));
+      GeluMulArgs gm{W.uf_wide, W.z, M, F};
+      RFX_TRY(L.run(PC_GU, [&] { return launch_gelu_mul<T>(gm, st); }));
+
+      GemmArgs dg{};
+      dg.A = W.z; dg.lda = F;
+      dg.B = (const char*)ctx->w.w_down + (size_t)l * D * F * eb; dg.ldb = F;
+      dg.out = W.rparts; dg.ldo = D; dg.o_split_stride = rpart_stride;
+      dg.M = M; dg.N = D; dg.K = F; dg.splits = P.down.splits; dg.k_per_split = P.down.kps; dg.batch = 1;
+      RFX_TRY(L.run(PC_DOWN, [&] { return launch_gemm<T>(dg, EPI_F32, st); }));
+      ResidAddArgs ra2{W.h, W.rparts, rpart_stride, P.down.splits, mod_at(2 * l + 1, k), M, Tn, D};
+      RFX_TRY(L.run(PC_RESID, [&] { return launch_resid_add(ra2, st); }));
+      // the next site's norm: the next layer's attention norm, or the final one
+      NormArgs n2{W.h, mod_at(2 * l + 2, k), W.y, M, Tn, D, c.rms_eps};
+      RFX_TRY(L.run(PC_RESID, [&] { return launch_norm<T>(n2, st); }));
+    }
+    GemmArgs hg{};
+    hg.A = W.y; hg.lda = D;
+    hg.B = ctx->w.w_aout; hg.ldb = D;
+    hg.out = W.uf_v; hg.ldo = c.action_dim;
+    hg.M = M; hg.N = c.action_dim; hg.K = D; hg.splits = 1; hg.k_per_split = D + 128; hg.batch = 1;
+    RFX_TRY(L.run(PC_FINAL, [&] { return launch_gemm<T>(hg, EPI_F32, st); }));
+    EulerArgs eu{W.uf_v, x_in, out, B, Tn, c.action_dim, (float)((double)taus[k + 1] - (double)taus[k])};
+    RFX_TRY(L.run(PC_FINAL, [&] { return launch_euler(eu, st); }));
+  }
+  return REFLEX_OK;
+}
+
 int enqueue_chunk_dispatch(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
                            float* out, bool prof, int mode, const reflex_sources* src) {
+  if (mode == REFLEX_MODE_UNFUSED) {
+    if (ctx->cfg.dtype == REFLEX_DTYPE_BF16)
+      return enqueue_chunk_unfused<bf16_t>(ctx, state, noise, steps, taus, out, prof);
+    return enqueue_chunk_unfused<float>(ctx, state, noise, steps, taus, out, prof);
+  }
   if (ctx->cfg.dtype == REFLEX_DTYPE_BF16)
     return enqueue_chunk<bf16_t>(ctx, state, noise, steps, taus, out, prof, mode, src);
   return enqueue_chunk<float>(ctx, state, noise, steps, taus, out, prof, mode, src);
@@ -683,6 +809,8 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
   W.frame_scratch = reinterpret_cast<float*>(base + P.off[17]);
   W.naive_k = base + P.off[18];
   W.naive_vt = base + P.off[19];
+  W.uf_wide = reinterpret_cast<float*>(base + P.off[20]);
+  W.uf_v = reinterpret_cast<float*>(base + P.off[21]);
   ctx->cache_k = cache_mem;
   ctx->cache_vt = reinterpret_cast<char*>(cache_mem) + P.cache_bytes / 2;
 
@@ -741,7 +869,9 @@ int denoise_entry(reflex_ctx* ctx, int mode, const reflex_sources* src, const fl
   if (!ctx || !ctx->alive) return REFLEX_ESTATE;
   if (!state || !noise || !actions_out) return REFLEX_EINVAL;
   if (num_steps < 1 || num_steps > ctx->cfg.max_steps) return REFLEX_EINVAL;
-  if (mode != REFLEX_MODE_REFLEX && mode != REFLEX_MODE_STANDARD && mode != REFLEX_MODE_NAIVE) return REFLEX_EINVAL;
+  if (mode != REFLEX_MODE_REFLEX && mode != REFLEX_MODE_STANDARD && mode != REFLEX_MODE_NAIVE &&
+      mode != REFLEX_MODE_UNFUSED)
+    return REFLEX_EINVAL;
   const bool spare = ctx->cfg.spare_slot != 0;
   if (spare && mode == REFLEX_MODE_STANDARD) return REFLEX_EINVAL;
   const int64_t F = ctx->frames_written;

@@ -158,3 +158,27 @@ def test_baseline_rejects_bad_arguments():
                                            cfg.num_steps, None, out.data_ptr())
     assert st == R.REFLEX_EINVAL
     eng.close()
+
+
+@pytest.mark.parametrize("case", ["tiny_fp32", "ragged_bf16_dh256_embed", "ragged_bf16_dh128_direct"])
+def test_unfused_schedule_matches_oracle(case):
+    """The fusion ablation's unfused schedule computes the same chunk: within
+    the parity bar of the oracle, and close to the fused result."""
+    cfg = STANDARD_CASES[case]
+    w, sk, sv, frames = _setup(cfg, 3)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(3):
+        eng.write_frame(frames[t])
+    state, noise = WL.make_state(cfg, 3), WL.make_noise(cfg, 3)
+    fused = eng.denoise(state, noise).cpu().numpy()
+    unfused = eng.denoise(state, noise, mode="unfused").cpu().numpy()
+    again = eng.denoise(state, noise, mode="unfused").cpu().numpy()  # graph replay
+    eng.close()
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 3, state, noise, cfg.taus())
+    assert np.array_equal(unfused, again)
+    if cfg.bf16:
+        rel = float(np.linalg.norm(unfused - ref) / np.linalg.norm(ref))
+        assert rel <= BF16_REL and float(np.max(np.abs(unfused - ref))) <= BF16_ABS, rel
+    else:
+        assert float(np.max(np.abs(unfused - ref))) <= FP32_TOL
+        assert float(np.max(np.abs(unfused - fused))) <= 1e-5
