@@ -35,6 +35,8 @@
 //
 // With more than one key split each block writes (O unnormalised, m, l) and a
 // merge kernel combines the splits with log-sum-exp weights in a fixed order.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -552,16 +554,20 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
           make_uint2(pack_bf16x2(o[db][0] * inv, o[db][1] * inv), pack_bf16x2(o[db][2] * inv, o[db][3] * inv));
     return;
   }
+  // bf16 partials: half the bytes of this kernel's largest write and of the
+  // merge's reads; the merged output is bf16 too
   const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq;
-  float* dst = p.part_o + prow * DH + 4 * g;
+  T* dst = reinterpret_cast<T*>(p.part_o) + prow * DH + 4 * g;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
-    *reinterpret_cast<float4*>(dst + db * 16) = make_float4(o[db][0], o[db][1], o[db][2], o[db][3]);
+    *reinterpret_cast<uint2*>(dst + db * 16) =
+        make_uint2(pack_bf16x2(o[db][0], o[db][1]), pack_bf16x2(o[db][2], o[db][3]));
   if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
 }
 
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
 // splits combined in index order.  One thread per (query row, 4 consecutive d).
+// The partial O_s are fp32 on the fp32 path and bf16 on the bf16 path.
 constexpr int kMaxSplits = 16;
 
 template <typename T, int DH>
@@ -575,14 +581,27 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   if (rq >= nrows) return;
   const int64_t base = (int64_t)b * p.nsplit * p.rows_pad + rq;
   // all loads of this thread are independent: one memory round trip
+  // (the raw partials are converted only after every load is issued)
   float2 ml[kMaxSplits];
-  float4 ov[kMaxSplits];
+  using Raw = typename std::conditional<sizeof(T) == 2, uint2, float4>::type;
+  Raw raw[kMaxSplits];
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s) {
     if (s < p.nsplit) {
       const int64_t prow = base + (int64_t)s * p.rows_pad;
       ml[s] = *reinterpret_cast<const float2*>(p.part_ml + prow * 2);
-      ov[s] = *reinterpret_cast<const float4*>(p.part_o + prow * DH + d);
+      raw[s] = *reinterpret_cast<const Raw*>(reinterpret_cast<const T*>(p.part_o) + prow * DH + d);
+    }
+  }
+  float4 ov[kMaxSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) {
+    if constexpr (sizeof(T) == 2) {
+      const uint2 w = *reinterpret_cast<const uint2*>(&raw[s]);
+      ov[s] = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                          __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+    } else {
+      ov[s] = *reinterpret_cast<const float4*>(&raw[s]);
     }
   }
   float M = -INFINITY;

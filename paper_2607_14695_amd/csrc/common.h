@@ -113,9 +113,15 @@ RFX_DEV float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
+// GELU, tanh approximation: 0.5 u (1 + tanh(y)), y = sqrt(2/pi) (u + 0.044715 u^3).
+// Evaluated in the equivalent logistic form u / (1 + exp(-2y)) (tanh(y) =
+// 2 sigma(2y) - 1) with the hardware exp2 and reciprocal: relative error a few
+// ulp; large |y| gives u or -0 without overflow trouble (1 + inf -> rcp 0).
 RFX_DEV float gelu_tanh(float u) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  return 0.5f * u * (1.0f + tanhf(k0 * (u + 0.044715f * u * u * u)));
+  const float y = k0 * (u + 0.044715f * u * u * u);
+  const float e = __builtin_amdgcn_exp2f(-2.0f * 1.4426950408889634f * y);  // exp(-2y)
+  return u * __builtin_amdgcn_rcpf(1.0f + e);
 }
 RFX_DEV float silu(float u) { return u / (1.0f + __expf(-u)); }
 

@@ -78,7 +78,7 @@ struct AttnArgs {
   int static_len, frame_tokens, R;
   int B, T, Hq;
   int nsplit;             // key splits (blockIdx.x)
-  float* part_o;          // [B][nsplit][rows_pad][dh]
+  float* part_o;          // [B][nsplit][rows_pad][dh], fp32 (fp32 path) or bf16 (bf16 path)
   float* part_ml;         // [B][nsplit][rows_pad][2]
   int rows_pad;
   void* out;              // [B*T][Hq*dh]
