@@ -1224,10 +1224,11 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
     const int btotal = bx * ((a.M + GBM - 1) / GBM) * a.batch * a.splits;
     if (pair_ok && a.M >= 512 && btotal >= 128 && a.k_per_split / DST >= 8) {
       const dim3 g((btotal + 7) / 8 * 8);
-      const bool whole = a.K == a.k_per_split * a.splits;  // every split a full K range
-      if (whole && a.k_per_split == 1024)
+      // K range of every split (one split may be given a range past K)
+      const int kr = a.splits == 1 ? a.K : (a.K == a.k_per_split * a.splits ? a.k_per_split : 0);
+      if (kr == 1024)
         RFX_LAUNCH((gemm_big5<EPI, 32>), g, dim3(512), 0, s, a);
-      else if (whole && a.k_per_split == 2048)
+      else if (kr == 2048)
         RFX_LAUNCH((gemm_big5<EPI, 64>), g, dim3(512), 0, s, a);
       else
         RFX_LAUNCH((gemm_big<EPI>), g, dim3(512), 0, s, a);
