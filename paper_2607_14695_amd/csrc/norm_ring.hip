@@ -134,32 +134,43 @@ hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void resid_norm_kernel(ResidArgs p) {
+  constexpr int MAXC = 4;  // D <= 4096: at most four 4-column chunks per thread
   __shared__ float red[4];
-  __shared__ float4 hs[4 * 256];
   const int m = blockIdx.x, b = m / p.T;
   const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
   const float* nmod = p.norm_mod + (int64_t)b * 3 * p.D;
   const int D4 = p.D >> 2;
+  // everything this thread needs, the next site's scale and shift included,
+  // is loaded before the row reduction: one memory round trip per row
+  float4 v[MAXC], sc[MAXC], sh[MAXC];
   float ss = 0.f;
-  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
-    const int c = c4 * 4;
-    const float4 acc = sum_parts(p.parts + (int64_t)m * p.D + c, p.part_stride, p.nparts);
-    const float4 h = ld4f(p.h + (int64_t)m * p.D + c);
-    const float4 gt = ld4f(gmod + c);
-    float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
-    if (p.norm_mode != NORM_FP32) v = rbf4(v);  // bf16 residual stream
-    hs[c4] = v;
-    ss = add_ssq(ss, v, p.norm_mode == NORM_BF16);
+#pragma unroll
+  for (int u = 0; u < MAXC; ++u) {
+    const int c4 = threadIdx.x + 256 * u;
+    if (c4 < D4) {
+      const int c = c4 * 4;
+      sc[u] = ld4f(nmod + c);
+      sh[u] = ld4f(nmod + p.D + c);
+      const float4 acc = sum_parts(p.parts + (int64_t)m * p.D + c, p.part_stride, p.nparts);
+      const float4 h = ld4f(p.h + (int64_t)m * p.D + c);
+      const float4 gt = ld4f(gmod + c);
+      v[u] = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+      if (p.norm_mode != NORM_FP32) v[u] = rbf4(v[u]);  // bf16 residual stream
+      ss = add_ssq(ss, v[u], p.norm_mode == NORM_BF16);
+      st4(p.h + (int64_t)m * p.D + c, v[u]);
+    }
   }
   const float r = inv_rms(ss, p.D, p.eps, p.norm_mode == NORM_BF16, red);
-  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
-    const int c = c4 * 4;
-    const float4 v = hs[c4];
-    st4(p.h + (int64_t)m * p.D + c, v);
-    const float4 sc = ld4f(nmod + c), sh = ld4f(nmod + p.D + c);
-    const float4 y = p.norm_mode == NORM_BF16 ? ada4(rbf4(make_float4(v.x * r, v.y * r, v.z * r, v.w * r)), 1.f, sc, sh)
-                                              : ada4(v, r, sc, sh);
-    st4(reinterpret_cast<T*>(p.y) + (int64_t)m * p.D + c, y);
+#pragma unroll
+  for (int u = 0; u < MAXC; ++u) {
+    const int c4 = threadIdx.x + 256 * u;
+    if (c4 < D4) {
+      const float4 x = v[u];
+      const float4 y = p.norm_mode == NORM_BF16
+                           ? ada4(rbf4(make_float4(x.x * r, x.y * r, x.z * r, x.w * r)), 1.f, sc[u], sh[u])
+                           : ada4(x, r, sc[u], sh[u]);
+      st4(reinterpret_cast<T*>(p.y) + (int64_t)m * p.D + c4 * 4, y);
+    }
   }
 }
 
@@ -184,24 +195,35 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
   const float* fmod = p.final_mod + (int64_t)b * 3 * p.D;
   const int D4 = p.D >> 2;
+  constexpr int MAXC = 4;  // D <= 4096
+  float4 sc[MAXC], sh[MAXC];
   float ss = 0.f;
-  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
-    const int c = c4 * 4;
-    const float4 acc = sum_parts(p.parts + m * p.D + c, p.part_stride, p.nparts);
-    const float4 h = ld4f(p.h + m * p.D + c);
-    const float4 gt = ld4f(gmod + c);
-    float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
-    if (p.norm_mode != NORM_FP32) v = rbf4(v);  // bf16 residual stream
-    ys[c4] = v;
-    ss = add_ssq(ss, v, p.norm_mode == NORM_BF16);
+#pragma unroll
+  for (int u = 0; u < MAXC; ++u) {
+    const int c4 = threadIdx.x + 256 * u;
+    if (c4 < D4) {
+      const int c = c4 * 4;
+      sc[u] = ld4f(fmod + c);  // loaded with the residual inputs: one round trip
+      sh[u] = ld4f(fmod + p.D + c);
+      const float4 acc = sum_parts(p.parts + m * p.D + c, p.part_stride, p.nparts);
+      const float4 h = ld4f(p.h + m * p.D + c);
+      const float4 gt = ld4f(gmod + c);
+      float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
+      if (p.norm_mode != NORM_FP32) v = rbf4(v);  // bf16 residual stream
+      ys[c4] = v;
+      ss = add_ssq(ss, v, p.norm_mode == NORM_BF16);
+    }
   }
   const float r = inv_rms(ss, p.D, p.eps, p.norm_mode == NORM_BF16, red);
-  for (int c4 = threadIdx.x; c4 < D4; c4 += 256) {
-    const int c = c4 * 4;
-    const float4 v = ys[c4];
-    const float4 sc = ld4f(fmod + c), sh = ld4f(fmod + p.D + c);
-    ys[c4] = p.norm_mode == NORM_BF16 ? ada4(rbf4(make_float4(v.x * r, v.y * r, v.z * r, v.w * r)), 1.f, sc, sh)
-                                      : ada4(v, r, sc, sh);
+#pragma unroll
+  for (int u = 0; u < MAXC; ++u) {
+    const int c4 = threadIdx.x + 256 * u;
+    if (c4 < D4) {
+      const float4 v = ys[c4];
+      ys[c4] = p.norm_mode == NORM_BF16
+                   ? ada4(rbf4(make_float4(v.x * r, v.y * r, v.z * r, v.w * r)), 1.f, sc[u], sh[u])
+                   : ada4(v, r, sc[u], sh[u]);
+    }
   }
   __syncthreads();
   // v[a] = sum_c y[c] W[a][c]: eight threads per output, each a strided
