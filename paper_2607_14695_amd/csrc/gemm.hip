@@ -288,24 +288,30 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_lds(GemmArgs p) {
   const int kbeg = split * p.k_per_split;
   const int kend = min(p.K, kbeg + p.k_per_split);
   const int nsteps = (kend - kbeg) / KS;  // K and k_per_split are multiples of 32
-  const int rs = p.k_per_split * 2;       // LDS bytes per activation row
-  const int cpr = rs >> 4;                // 16-byte chunks per row
+  // LDS bytes per activation row: this split's K range, rounded up to whole
+  // groups of 8 chunks so the chunk swizzle (an XOR of the low 3 bits) stays
+  // inside the row
+  const int rs = (((kend - kbeg) * 2) + 127) & ~127;
+  const int cpr = rs >> 4;  // 16-byte chunks per row
 
   const T* A = reinterpret_cast<const T*>(p.A) + (int64_t)z * p.a_bstride;
   const T* B = reinterpret_cast<const T*>(p.B) + (int64_t)z * p.b_bstride;
 
-  // 1. activation rows m0 .. m0+16*MB-1 (rows past M repeat row M-1), chunks
-  //    kbeg/8 .. ; chunk position q of row r holds logical chunk q ^ (r & 7)
+  // 1. activation rows m0 .. min(M, m0+16*MB)-1, chunks kbeg/8 .. ; chunk
+  //    position q of row r holds logical chunk q ^ (r & 7).  Rows past M are
+  //    not copied: an MFMA output row depends only on its own A row, and those
+  //    rows are never stored.
   {
-    const int total = 16 * MB * cpr;  // chunks
+    const int rows = min(16 * MB, p.M - m0);
+    const int total = rows * cpr;  // chunks
     const int kchunks = (kend - kbeg) >> 3;
     for (int i0 = wave * 64; i0 < total; i0 += NW * 64) {
       const int q = i0 + lane;
       const int r = q / cpr, pos = q - r * cpr;
       int lc = pos ^ (r & 7);
-      lc = lc < kchunks ? lc : 0;  // past the end of a short last split: any valid chunk
+      lc = lc < kchunks ? lc : 0;  // a K range that is not a multiple of 64: any valid chunk
       const T* src = A + (int64_t)min(m0 + r, p.M - 1) * p.lda + kbeg + lc * 8;
-      __builtin_amdgcn_global_load_lds(src, smem + i0 * 16, 16, 0, 0);
+      if (q < total) __builtin_amdgcn_global_load_lds(src, smem + i0 * 16, 16, 0, 0);
     }
   }
 
@@ -411,7 +417,8 @@ static void launch_skinny_lds_cfg(const GemmArgs& a, hipStream_t s, int nw) {
     nx = (a.N + 16 * NB - 1) / (16 * NB);
   const int mch = (a.M + 16 * MB - 1) / (16 * MB);
   dim3 grid(nx, mch * a.splits, a.batch);
-  const size_t tile = (size_t)16 * MB * a.k_per_split * 2;
+  const size_t klen = (size_t)(a.k_per_split < a.K ? a.k_per_split : a.K);
+  const size_t tile = (size_t)16 * MB * ((klen * 2 + 127) & ~(size_t)127);
   const size_t red = (size_t)nw * MB * 16 * (16 * NBT + 1) * 4;
   const size_t shm = tile > red ? tile : red;
   if (nw == 8)
@@ -1193,7 +1200,9 @@ static void launch_skinny_lds_pick(const GemmArgs& a, hipStream_t s) {
 template <typename T, int EPI>
 static void launch_skinny(const GemmArgs& a, hipStream_t s) {
   // bf16 with the activation K range fitting in LDS: stage it there
-  if (sizeof(T) == 2 && (size_t)16 * skinny_mb(a.M) * a.k_per_split * 2 <= 160 * 1024 && a.k_per_split % 32 == 0 &&
+  const int klen = a.k_per_split < a.K ? a.k_per_split : a.K;  // LDS holds one split's K range
+  if (sizeof(T) == 2 && (size_t)16 * skinny_mb(a.M) * ((klen * 2 + 127) & ~127) <= 160 * 1024 &&
+      a.k_per_split % 32 == 0 &&
       a.K % 32 == 0) {
     switch (skinny_mb(a.M)) {
       case 1: launch_skinny_lds_pick<1, EPI>(a, s); return;
