@@ -193,6 +193,9 @@ class ReflexEngine:
         self.last_n_frames = None
         self.ctx = c_vp(None)
         self._bufs = {}
+        # the weights and the static K/V may still be in production on the
+        # caller's stream: the library reads them on the engine stream
+        self.stream.wait_stream(torch.cuda.current_stream(self.device))
         with torch.cuda.stream(self.stream):
             self.w = {}
             for name in self.WEIGHT_ORDER:

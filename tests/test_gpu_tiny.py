@@ -293,3 +293,26 @@ def test_denoise_rejects_bad_steps(tiny):
         eng.denoise(WL.make_state(cfg, 0), WL.make_noise(cfg, 0), num_steps=cfg.num_steps + 1)
     assert ei.value.status == R.REFLEX_EINVAL
     eng.close()
+
+
+def test_engine_waits_for_inputs_made_on_the_callers_stream():
+    """The static K/V handed to the engine may still be being computed on the
+    caller's stream (here behind a ~50 ms busy kernel); the prefix written at
+    init must still be the finished values."""
+    cfg = WL.CONFIGS["tiny_fp32"]
+    w, sk, sv, frames = _setup(cfg, 1)
+    sk_ref = torch.from_numpy(sk).cuda()
+    sv_ref = torch.from_numpy(sv).cuda()
+    torch.cuda.synchronize()
+    sk_d = torch.zeros_like(sk_ref)
+    sv_d = torch.zeros_like(sv_ref)
+    torch.cuda._sleep(100_000_000)  # keeps the caller's stream busy
+    sk_d.copy_(sk_ref)
+    sv_d.copy_(sv_ref)
+    eng = R.ReflexEngine(cfg, w, sk_d, sv_d)
+    K, Vt = eng.cache_views()
+    K, Vt = K.cpu().numpy(), Vt.cpu().numpy()
+    ks, vs = O.static_kv(cfg, sk, sv, 0, 0)
+    np.testing.assert_allclose(K[0, 0, :cfg.static_len], ks[:, 0], rtol=1e-5, atol=1e-5)
+    np.testing.assert_allclose(Vt[0, 0, :, :cfg.static_len], vs[:, 0].T, rtol=0, atol=0)
+    eng.close()
