@@ -512,6 +512,9 @@ def main():
     if not args.no_latency:
         lat = _chunk_latencies(eng, state, noise, max(20, args.steps), torch)
         log(f"chunk latency p50 {lat['p50']:.3f} ms, p99 {lat['p99']:.3f} ms")
+    finite = bool(torch.isfinite(eng.denoise(state, noise)).all())
+    if not finite:
+        raise RuntimeError("non-finite actions from the timed batch-1 configuration")
     prof = eng.profile(state, noise)
     log("profile: " + ", ".join(f"{k}={v[0]:.3f}ms/{v[1]}" for k, v in prof.items() if v[1]))
     bf = _class_bytes_flops(cfg)
@@ -538,6 +541,8 @@ def main():
         steps32 = max(3, args.steps // 3)
         t32 = _time_ticks(e32, fr32, st32, nz32, steps32, 2, torch)
         c32s = _time_ticks(e32, fr32, st32, nz32, steps32, 1, torch, denoise_only=True)
+        if not bool(torch.isfinite(e32.denoise(st32, nz32)).all()):
+            raise RuntimeError("non-finite actions from the timed batch-32 configuration")
         p32 = e32.profile(st32, nz32)
         pw32 = e32.profile_write(fr32[0])
         rb32 = _ring_bytes(c32, pw32)
