@@ -63,6 +63,17 @@ extern "C" {
 #define REFLEX_NORM_BF16 1
 #define REFLEX_NORM_BF16_FP32_STATS 2
 
+/* Attention kernel of the bf16 path.  Both compute the same masked softmax
+ * over [static; ring window; dynamic] (Eq. 1) and agree to rounding.
+ * REFLEX_ATTN_AUTO picks by the launch geometry: 16-row waves sharing each
+ * key tile over 128 query rows, or one wave pair per 32 query rows when the
+ * launch would reach one key tile per split (a few envs and a short context).
+ * The other two values force one kernel (tests, tuning); the fp32 path has
+ * one kernel and ignores the field. */
+#define REFLEX_ATTN_AUTO 0
+#define REFLEX_ATTN_ROWS16 1
+#define REFLEX_ATTN_PAIR 2
+
 /*
  * Shape of the action expert and of the cache.
  *
@@ -121,6 +132,7 @@ typedef struct reflex_config {
   double temb_max_period;
   int32_t spare_slot;      /* 0 or 1, see "Cache" above */
   int32_t norm_precision;  /* REFLEX_NORM_*: REFLEX_NORM_FP32 for the method */
+  int32_t attn_kernel;     /* REFLEX_ATTN_*: REFLEX_ATTN_AUTO unless forcing one */
 } reflex_config;
 
 /*

@@ -565,6 +565,324 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
   if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
 }
 
+// ---------------------------------------------------------------------------
+// bf16 variant with wave pairs.  Two waves share 32 query rows (two 16-row
+// blocks): for S^T = K Q^T wave h takes keys [32h, 32h + 32) of the tile, for
+// O^T = V^T P^T it takes head dims [h*DH/2, (h+1)*DH/2) over all 64 keys.
+// Every K row and V^T row fragment a wave reads from LDS thus feeds two
+// MFMAs (one per row block), half the LDS bytes per query row of a 16-row
+// wave, while a wave still holds only its Q fragments (2 x DH/32 x 4 VGPRs),
+// its half of O^T (DH/32 x 2 x 4) and 16 scores, so two waves fit per SIMD.
+//
+// Per tile the pair exchanges, through LDS, (1) its per-row score maxima, so
+// both waves use the same running max and make the same lazy-rescale
+// decision, and (2) its probabilities, already in the B-operand layout of the
+// P.V MFMA (the key permutation of the 16-row variant: over its two score
+// blocks a lane holds 8 consecutive keys of the wave's 32).  The running
+// row sums cover each wave's own keys and are added once at the end; the
+// running max is identical in both waves, so the two halves share one scale.
+// A workgroup is one pair.  This variant serves the latency-bound regime (a
+// few envs, down to one key tile per split): 32-row blocks waste fewer
+// padded rows than 128-row ones (416 against 512 for 408 rows), so more
+// workgroups each finish one tile sooner.  With four pairs sharing a tile at
+// 32 envs the two extra barriers per tile made it slower than the 16-row
+// variant, which therefore keeps the large batches.
+// ---------------------------------------------------------------------------
+template <int DH>
+__global__ __launch_bounds__(128) void attn_pair_kernel(AttnArgs p) {
+  using T = bf16_t;
+  constexpr int NW = 2;
+  constexpr int NKS = DH / 32;            // 32-wide d steps of S^T
+  constexpr int NDH = DH / 32;            // 16-wide d blocks in half a head
+  constexpr int KRB = DH * 2;             // bytes per K row in LDS
+  constexpr int KCH = DH / 8;             // 16-byte chunks per K row
+  constexpr int NKO = KCH >= 16 ? 4 : 2;  // distinct per-lane K chunk offsets per parity
+  constexpr int VRB = AKT * 2;            // bytes per V^T row (128)
+  constexpr int KBYTES = AKT * KRB;
+  constexpr int VBYTES = DH * VRB;
+  constexpr int STAGE = KBYTES + VBYTES;
+  constexpr int NIK = KBYTES / 1024 / NW;  // 1-KB DMA instructions per wave, K
+  constexpr int NIV = VBYTES / 1024 / NW;  // same for V^T
+  static_assert(NIK >= 1 && NIV >= 1, "tile smaller than one DMA round");
+  __shared__ __attribute__((aligned(16))) unsigned char stage0[STAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char stage1[STAGE];
+  __shared__ __attribute__((aligned(16))) uint4 pbuf[2][2][64];  // [half][row block][lane]
+  __shared__ float xbuf[2][2][16];                               // [half][row block][row]
+
+  const int T_ = p.T, Hq = p.Hq;
+  const int nrows = T_ * Hq;
+  const int nrb = (nrows + 31) / 32;
+  int group, rb;
+  if (!attn_decode(blockIdx.x, p.B * p.nsplit, nrb, group, rb)) return;
+  const int b = group / p.nsplit, split = group - b * p.nsplit;
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int h = wave;
+  const int r16 = lane & 15, g = lane >> 4;
+  int rq[2], iq[2], jq[2];
+  bool qvalid[2];
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr) {
+    rq[rr] = rb * 32 + rr * 16 + r16;
+    qvalid[rr] = rq[rr] < nrows;
+    iq[rr] = qvalid[rr] ? rq[rr] / Hq : 0;
+    jq[rr] = qvalid[rr] ? rq[rr] % Hq : 0;
+  }
+
+  uint4 qf[2][NKS];
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr) {
+    // rows past the valid range compute on row 0's data and are never stored
+    const T* qrow =
+        reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + (qvalid[rr] ? rq[rr] : 0)) * DH + g * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[rr][ks] = ld16(qrow + ks * 32);
+  }
+
+  const int Lc = p.static_len + (*p.n_valid) * p.frame_tokens;
+  const int n_ct = (Lc + AKT - 1) / AKT;
+  const int n_dt = (T_ + AKT - 1) / AKT;
+  const int total = n_ct + n_dt;
+  const int per = (total + p.nsplit - 1) / p.nsplit;
+  const int t_beg = split * per;
+  const int t_end = min(total, t_beg + per);
+
+  const T* ck = reinterpret_cast<const T*>(p.cache_k) + (int64_t)b * p.ck_bstride;
+  const T* cvt = reinterpret_cast<const T*>(p.cache_vt) + (int64_t)b * p.ck_bstride;
+  const T* kdb = reinterpret_cast<const T*>(p.kd) + (int64_t)b * T_ * DH;
+  const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
+  const float scale = rsqrtf((float)DH) * 1.4426950408889634f;
+  const int tpad = p.tpad, Rrow = p.R;
+  const int hole = __builtin_amdgcn_readfirstlane(*p.hole_row), skip = p.frame_tokens;
+  constexpr int RPI = 64 / KCH;  // K rows per DMA instruction
+
+  // DMA of tile t into stage sk, shared by the two waves (same layout and
+  // swizzles as the 16-row variant)
+  auto issue = [&](int t, unsigned char* sk) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const bool dyn = t >= n_ct;
+    const int base = dyn ? (t - n_ct) * AKT : t * AKT;
+    const int last = (dyn ? T_ : Lc) - 1;
+    unsigned char* sv = sk + KBYTES;
+    const int kl = ln % KCH, kr = ln / KCH;
+    const int vd = ln >> 3, vc = ln & 7;
+    if (dyn) {
+#pragma unroll
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        const int r = min(base + row, last);
+        __builtin_amdgcn_global_load_lds(kdb + r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8, sk + (wave * NIK + j) * 1024, 16,
+                                         0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        __builtin_amdgcn_global_load_lds(vdb + d * tpad + base + (vc ^ (d & 7)) * 8, sv + (wave * NIV + j) * 1024, 16,
+                                         0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        int r = min(base + row, last);
+        r += r >= hole ? skip : 0;
+        __builtin_amdgcn_global_load_lds(ck + (int64_t)r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8,
+                                         sk + (wave * NIK + j) * 1024, 16, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        int key = base + (vc ^ (d & 7)) * 8;
+        key = key <= last ? key : 0;
+        key += key >= hole ? skip : 0;
+        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + key, sv + (wave * NIV + j) * 1024, 16, 0, 0);
+      }
+    }
+  };
+
+  f32x4_v o[NDH][2];
+#pragma unroll
+  for (int db = 0; db < NDH; ++db)
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) o[db][rr] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+
+  // per-lane LDS read offsets (bytes).  K: row rho = 32h + 8*(r16 >> 2) + 4e +
+  // (r16 & 3), d-chunk 4*ks + g, the low bits of ks in x.  V^T: row r16 of a
+  // d block, key chunk 4j + g of the wave's own (j = h) and the partner's
+  // (j = 1 - h) 32 keys.
+  int koff[2][NKO];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int rho = 32 * h + 8 * (r16 >> 2) + 4 * e + (r16 & 3);
+#pragma unroll
+    for (int x = 0; x < NKO; ++x) koff[e][x] = rho * KRB + ((4 * x + g) ^ RFX_KSWZ(rho, KCH)) * 16;
+  }
+  const int voff_own = h * NDH * 16 * VRB + r16 * VRB + ((4 * h + g) ^ (r16 & 7)) * 16;
+  const int voff_oth = h * NDH * 16 * VRB + r16 * VRB + ((4 * (1 - h) + g) ^ (r16 & 7)) * 16;
+
+  auto step = [&](int t, const unsigned char* cur, unsigned char* nxt) __attribute__((always_inline)) {
+    const bool dyn = t >= n_ct;
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): this wave's share of tile t
+    lds_barrier();
+    if (t + 1 < t_end) issue(t + 1, nxt);
+    const unsigned char* sk = cur;
+    const unsigned char* sv = cur + KBYTES;
+
+    // S^T for the wave's 32 keys x 32 rows: s[e][rr]
+    f32x4_v s[2][2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int rr = 0; rr < 2; ++rr) s[e][rr] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k0 = 0; k0 < NKS; k0 += 2) {
+      uint4 a[2][2];
+#pragma unroll
+      for (int u = 0; u < 2 && k0 + u < NKS; ++u)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int ks = k0 + u;
+          a[u][e] = *reinterpret_cast<const uint4*>(sk + (ks / NKO) * NKO * 64 + koff[e][ks % NKO]);
+        }
+#pragma unroll
+      for (int u = 0; u < 2 && k0 + u < NKS; ++u)
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+          for (int rr = 0; rr < 2; ++rr) mfma_step(s[e][rr], a[u][e], qf[rr][k0 + u], T());
+    }
+
+    // lane (r16, g) holds keys 32h + 8g + 4e + i of row r16 in block rr;
+    // visible iff below lim (cached rows below Lc; the state row sees only
+    // dynamic key 0)
+    float mt[2];
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) {
+      const int lim = (dyn ? (iq[rr] > 0 ? T_ : 1) - (t - n_ct) * AKT : Lc - t * AKT) - 32 * h - 8 * g;
+      float m = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float v = 4 * e + i < lim ? s[e][rr][i] * scale : -INFINITY;
+          s[e][rr][i] = v;
+          m = fmaxf(m, v);
+        }
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      mt[rr] = m;
+    }
+    // (1) row maxima of the two key halves
+    if (g == 0) {
+      xbuf[h][0][r16] = mt[0];
+      xbuf[h][1][r16] = mt[1];
+    }
+    lds_barrier();
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) mt[rr] = fmaxf(mt[rr], xbuf[1 - h][rr][r16]);
+
+    // lazy rescaling, identical in both waves of the pair (same maxima, same
+    // running max): the running max moves only when a row's tile max exceeds
+    // it by more than 8 (log2 units)
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) {
+      if (__any(mt[rr] > m_run[rr] + 8.f)) {
+        const float m_new = fmaxf(m_run[rr], mt[rr]);
+        const float corr = m_new == -INFINITY ? 1.f : exp2f(m_run[rr] - m_new);
+        l_run[rr] *= corr;
+        m_run[rr] = m_new;
+#pragma unroll
+        for (int db = 0; db < NDH; ++db) o[db][rr] *= corr;
+      }
+    }
+    uint4 pf[2];
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) {
+      const float m_use = (m_run[rr] == -INFINITY) ? 0.f : m_run[rr];
+      float psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float x = __builtin_amdgcn_exp2f(s[e][rr][i] - m_use);
+          s[e][rr][i] = x;
+          psum += x;
+        }
+      psum += __shfl_xor(psum, 16, 64);
+      psum += __shfl_xor(psum, 32, 64);
+      l_run[rr] += psum;
+      pf[rr] = make_uint4(pack_bf16x2(s[0][rr][0], s[0][rr][1]), pack_bf16x2(s[0][rr][2], s[0][rr][3]),
+                          pack_bf16x2(s[1][rr][0], s[1][rr][1]), pack_bf16x2(s[1][rr][2], s[1][rr][3]));
+    }
+    // (2) probabilities of the two key halves, as P.V B operands
+    pbuf[h][0][lane] = pf[0];
+    pbuf[h][1][lane] = pf[1];
+    lds_barrier();
+    uint4 po[2];
+    po[0] = pbuf[1 - h][0][lane];
+    po[1] = pbuf[1 - h][1][lane];
+
+    // O^T (the wave's half of the head) += V^T P^T over the own and the
+    // partner's 32 keys
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int voff = c == 0 ? voff_own : voff_oth;
+#pragma unroll
+      for (int d0 = 0; d0 < NDH; d0 += 4) {
+        uint4 vf[4];
+#pragma unroll
+        for (int u = 0; u < 4 && d0 + u < NDH; ++u)
+          vf[u] = *reinterpret_cast<const uint4*>(sv + (d0 + u) * 16 * VRB + voff);
+#pragma unroll
+        for (int u = 0; u < 4 && d0 + u < NDH; ++u)
+#pragma unroll
+          for (int rr = 0; rr < 2; ++rr) mfma_step(o[d0 + u][rr], vf[u], c == 0 ? pf[rr] : po[rr], T());
+      }
+    }
+  };
+
+  if (t_beg < t_end) issue(t_beg, stage0);
+  for (int t = t_beg; t < t_end; t += 2) {
+    step(t, stage0, stage1);
+    if (t + 1 < t_end) step(t + 1, stage1, stage0);
+  }
+
+  // row sums over all keys: own half + the partner's half
+  if (g == 0) {
+    xbuf[h][0][r16] = l_run[0];
+    xbuf[h][1][r16] = l_run[1];
+  }
+  lds_barrier();
+  float l_tot[2];
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr) l_tot[rr] = l_run[rr] + xbuf[1 - h][rr][r16];
+
+  const int dbase = h * (DH / 2) + 4 * g;
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr) {
+    if (!qvalid[rr]) continue;
+    if (p.nsplit == 1) {
+      const float inv = l_tot[rr] > 0.f ? 1.f / l_tot[rr] : 0.f;
+      T* dst = reinterpret_cast<T*>(p.out) + ((int64_t)b * T_ + iq[rr]) * (int64_t)(Hq * DH) + jq[rr] * DH + dbase;
+#pragma unroll
+      for (int db = 0; db < NDH; ++db)
+        *reinterpret_cast<uint2*>(dst + db * 16) =
+            make_uint2(pack_bf16x2(o[db][rr][0] * inv, o[db][rr][1] * inv),
+                       pack_bf16x2(o[db][rr][2] * inv, o[db][rr][3] * inv));
+    } else {
+      const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq[rr];
+      T* dst = reinterpret_cast<T*>(p.part_o) + prow * DH + dbase;
+#pragma unroll
+      for (int db = 0; db < NDH; ++db)
+        *reinterpret_cast<uint2*>(dst + db * 16) =
+            make_uint2(pack_bf16x2(o[db][rr][0], o[db][rr][1]), pack_bf16x2(o[db][rr][2], o[db][rr][3]));
+      if (h == 0 && g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run[rr], l_tot[rr]);
+    }
+  }
+}
+
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
 // splits combined in index order.  One thread per (query row, 4 consecutive d).
 // The partial O_s are fp32 on the fp32 path and bf16 on the bf16 path.
@@ -636,26 +954,43 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
 // Query rows per attention workgroup: 128 on the bf16 path, 64 on fp32.
 int attention_rows_per_block(int elem_bytes) { return elem_bytes == 2 ? 128 : 64; }
 
-int attention_pick_splits(int B, int rows, int max_keys, int elem_bytes) {
-  const int rpb = attention_rows_per_block(elem_bytes);
-  const int rbs = (rows + rpb - 1) / rpb;
-  const int base = B * rbs;
+// Kernel and key-split count for (B envs, rows query rows, up to max_keys
+// cached keys).  One workgroup per CU is resident (LDS bound), so both aim
+// for about one wave of workgroups over the 256 CUs.  The 16-row variant
+// covers 128 rows per workgroup; when that grid would reach one key tile per
+// split (a few envs, short context) the launch is latency-bound and the
+// wave-pair variant (32 rows per workgroup, one tile per split) is used.
+// `force` (ATTN_AUTO, ATTN_ROWS16 or ATTN_PAIR) overrides the choice.
+AttnPlan attention_plan(int B, int rows, int max_keys, int elem_bytes, int force) {
   const int tiles = (max_keys + AKT - 1) / AKT + 1;
-  // one workgroup per CU is resident (LDS bound): aim for ~1 wave of
-  // workgroups over 256 CUs.  Down to one tile per split: at a few envs the
-  // latency of a tile's copy and math outweighs the larger merge.
+  AttnPlan pl;
+  pl.kernel = ATTN_ROWS16;
+  const int rpb = attention_rows_per_block(elem_bytes);
+  int base = B * ((rows + rpb - 1) / rpb);
+  if (elem_bytes == 2) {
+    const bool latency = 256 / base >= tiles;
+    if (force == ATTN_PAIR || (force == ATTN_AUTO && latency)) {
+      pl.kernel = ATTN_PAIR;
+      base = B * ((rows + 31) / 32);
+    }
+  }
   int s = 256 / base;
   if (s > tiles) s = tiles;
   if (s > kMaxSplits) s = kMaxSplits;
-  return s < 1 ? 1 : s;
+  pl.splits = s < 1 ? 1 : s;
+  return pl;
 }
 
 template <typename T, int DH>
 static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
   const int groups = a.B * a.nsplit;
   if constexpr (sizeof(T) == 2) {
-    const int nwg = ((groups + 7) / 8) * 8 * (a.rows_pad / 128);
-    RFX_LAUNCH((attn16_kernel<DH>), dim3(nwg), dim3(512), 0, s, a);
+    const int rows = a.T * a.Hq;
+    const int g8 = ((groups + 7) / 8) * 8;
+    if (a.kernel == ATTN_PAIR)
+      RFX_LAUNCH((attn_pair_kernel<DH>), dim3(g8 * ((rows + 31) / 32)), dim3(128), 0, s, a);
+    else
+      RFX_LAUNCH((attn16_kernel<DH>), dim3(g8 * (a.rows_pad / 128)), dim3(512), 0, s, a);
   } else {
     const int nwg = ((groups + 7) / 8) * 8 * (a.rows_pad / 64);
     RFX_LAUNCH((attn_kernel<T, DH>), dim3(nwg), dim3(256), 0, s, a);
@@ -672,6 +1007,7 @@ static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
 template <typename T>
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
   if (a.nsplit < 1 || a.nsplit > kMaxSplits || a.rows_pad % 128) return hipErrorInvalidValue;
+  if (a.kernel != ATTN_ROWS16 && a.kernel != ATTN_PAIR) return hipErrorInvalidValue;
   switch (head_dim) {
     case 64: launch_attn_dh<T, 64>(a, s); break;
     case 128: launch_attn_dh<T, 128>(a, s); break;

@@ -84,7 +84,7 @@ constexpr int kWsParts = 22;
 struct Plan {
   int T, M, S, Nqkv, C, R, slots, rows_pad, tpad, nrb, eb;
   SplitK o, down;
-  int attn_splits;
+  int attn_splits, attn_kernel;
   int max_parts;
   size_t naive_k_stride, naive_vt_stride;  // per-layer bytes of the Naive-mode dynamic K/V
   size_t cache_bytes, ws_bytes;
@@ -125,6 +125,7 @@ int validate(const reflex_config* c) {
   if (c->window_frames < 1) return REFLEX_EINVAL;
   if (c->spare_slot != 0 && c->spare_slot != 1) return REFLEX_EINVAL;
   if (c->norm_precision < REFLEX_NORM_FP32 || c->norm_precision > REFLEX_NORM_BF16_FP32_STATS) return REFLEX_EINVAL;
+  if (c->attn_kernel < REFLEX_ATTN_AUTO || c->attn_kernel > REFLEX_ATTN_PAIR) return REFLEX_EINVAL;
   if (c->frame_dim < 0 || c->frame_dim % 8) return REFLEX_EINVAL;
   if (c->batch < 1 || c->batch > 4096) return REFLEX_EINVAL;
   if (c->max_steps < 1 || c->max_steps > REFLEX_MAX_STEPS) return REFLEX_EINVAL;
@@ -154,7 +155,9 @@ Plan make_plan(const reflex_config* c) {
   p.o = make_split(p.M, c->n_q_heads * c->head_dim,
                    gemm_pick_splits(p.M, c->width, c->n_q_heads * c->head_dim, eb), eb);
   p.down = make_split(p.M, c->mlp_dim, gemm_pick_splits(p.M, c->width, c->mlp_dim, eb), eb);
-  p.attn_splits = attention_pick_splits(c->batch, rows, p.R, eb);
+  const AttnPlan ap = attention_plan(c->batch, rows, p.R, eb, c->attn_kernel);
+  p.attn_splits = ap.splits;
+  p.attn_kernel = ap.kernel;
   p.max_parts = p.o.splits > p.down.splits ? p.o.splits : p.down.splits;
 
   const size_t B = c->batch, L = c->n_layers, dh = c->head_dim, D = c->width, K = c->max_steps;
@@ -397,7 +400,7 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
       aa.n_valid = reinterpret_cast<const int32_t*>(W.tick + 1);
       aa.hole_row = reinterpret_cast<const int32_t*>(W.tick + 3);
       aa.static_len = c.static_len; aa.frame_tokens = c.frame_tokens; aa.R = P.R;
-      aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits;
+      aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits; aa.kernel = P.attn_kernel;
       aa.part_o = W.part_o; aa.part_ml = W.part_ml;
       aa.rows_pad = P.rows_pad; aa.out = W.o;
       RFX_TRY(L.run(PC_ATTN, [&] { return launch_attention<T>(aa, dh, st); }));
@@ -510,7 +513,7 @@ int enqueue_chunk_unfused(reflex_ctx* ctx, const float* state, const float* nois
       aa.n_valid = reinterpret_cast<const int32_t*>(W.tick + 1);
       aa.hole_row = reinterpret_cast<const int32_t*>(W.tick + 3);
       aa.static_len = c.static_len; aa.frame_tokens = c.frame_tokens; aa.R = P.R;
-      aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits;
+      aa.B = B; aa.T = Tn; aa.Hq = Hq; aa.nsplit = P.attn_splits; aa.kernel = P.attn_kernel;
       aa.part_o = W.part_o; aa.part_ml = W.part_ml;
       aa.rows_pad = P.rows_pad; aa.out = W.o;
       RFX_TRY(L.run(PC_ATTN, [&] { return launch_attention<T>(aa, dh, st); }));

@@ -37,6 +37,7 @@ MODE_NAIVE = 2
 MODE_UNFUSED = 3
 MODES = {"reflex": MODE_REFLEX, "standard": MODE_STANDARD, "naive": MODE_NAIVE, "unfused": MODE_UNFUSED}
 NORM_PRECISIONS = {"fp32": 0, "bf16": 1, "bf16_fp32_stats": 2}
+ATTN_KERNELS = {"auto": 0, "rows16": 1, "pair": 2}
 
 c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 
@@ -50,6 +51,7 @@ class ConfigC(ctypes.Structure):
         ("dtype", c_i32), ("mod_mode", c_i32), ("max_steps", c_i32), ("rms_eps", c_f32),
         ("embed_scale", c_f32), ("rope_theta", c_f64), ("temb_min_period", c_f64),
         ("temb_max_period", c_f64), ("spare_slot", c_i32), ("norm_precision", c_i32),
+        ("attn_kernel", c_i32),
     ]
 
 
@@ -144,7 +146,7 @@ def config_to_c(cfg: ReflexConfig, max_steps: Optional[int] = None) -> ConfigC:
         mod_mode=MOD_SCALE_ONLY if cfg.mod_mode == "scale_only" else MOD_FULL, max_steps=ms,
         rms_eps=cfg.rms_eps, embed_scale=cfg.embed_scale, rope_theta=cfg.rope_theta,
         temb_min_period=cfg.temb_min_period, temb_max_period=cfg.temb_max_period, spare_slot=cfg.spare_slot,
-        norm_precision=NORM_PRECISIONS[cfg.norm_precision])
+        norm_precision=NORM_PRECISIONS[cfg.norm_precision], attn_kernel=ATTN_KERNELS[cfg.attn_kernel])
 
 
 def query_sizes(cfg: ReflexConfig, max_steps: Optional[int] = None) -> Tuple[int, int]:

@@ -72,6 +72,8 @@ class ReflexConfig:
     spare_slot: int = 0
     # GPU numerics ablation only: "fp32" (the method), "bf16", "bf16_fp32_stats"
     norm_precision: str = "fp32"
+    # GPU kernel choice only: "auto", or force "rows16" / "pair" (bf16 attention)
+    attn_kernel: str = "auto"
     # workload driver
     ticks: int = 1
     tau_schedule: Optional[Tuple[float, ...]] = None

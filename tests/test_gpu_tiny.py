@@ -182,14 +182,17 @@ def test_ragged_multi_env(frame_dim):
 BF16_REL, BF16_ABS = 1e-2, 5e-2
 
 
+@pytest.mark.parametrize("attn", ["rows16", "pair"])
 @pytest.mark.parametrize("head_dim,frame_dim", [(64, 72), (128, 0), (256, 48)])
-def test_ragged_bf16(head_dim, frame_dim):
+def test_ragged_bf16(head_dim, frame_dim, attn):
     """The bf16 path (bf16 attention tiles, bf16 GEMM operands) at every head
-    width it supports, with ragged tiles and blocks: Ls = 40 and F = 24 leave
-    partial 64-key tiles, T*Hq = 18 a partial 128-row query block; three envs;
-    a 3-slot ring wrapped twice.  Tolerance: relative-L2 1e-2 and max-abs 5e-2
-    on the action chunk (bf16 operands, fp32 accumulation)."""
-    cfg = RAGGED.replace(name=f"ragged_bf16_{head_dim}", dtype="bf16", head_dim=head_dim, frame_dim=frame_dim)
+    width it supports, with both attention kernels, ragged tiles and blocks:
+    Ls = 40 and F = 24 leave partial 64-key tiles, T*Hq = 18 a partial query
+    block; three envs; a 3-slot ring wrapped twice.  Tolerance: relative-L2
+    1e-2 and max-abs 5e-2 on the action chunk (bf16 operands, fp32
+    accumulation)."""
+    cfg = RAGGED.replace(name=f"ragged_bf16_{head_dim}", dtype="bf16", head_dim=head_dim, frame_dim=frame_dim,
+                         attn_kernel=attn)
     w, sk, sv, frames = _setup(cfg, 7)
     eng = R.ReflexEngine(cfg, w, sk, sv)
     for t in range(7):
@@ -201,7 +204,7 @@ def test_ragged_bf16(head_dim, frame_dim):
             ref = O.denoise_chunk(cfg, w, sk, sv, frames, t + 1, state, noise, cfg.taus())
             rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
             mx = float(np.max(np.abs(got - ref)))
-            print(f"bf16 dh={head_dim} tick {t}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+            print(f"bf16 dh={head_dim} {attn} tick {t}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
             assert rel <= BF16_REL and mx <= BF16_ABS, (t, rel, mx)
     eng.close()
 
@@ -231,14 +234,16 @@ def test_limits_t64_no_static_prefix(dtype):
     eng.close()
 
 
-@pytest.mark.parametrize("dtype,horizon", [("f32", 100), ("bf16", 100), ("bf16", 127)])
-def test_long_chunks_two_dynamic_tiles(dtype, horizon):
+@pytest.mark.parametrize("dtype,horizon,attn", [("f32", 100, "auto"), ("bf16", 100, "rows16"),
+                                                ("bf16", 127, "rows16"), ("bf16", 100, "pair"),
+                                                ("bf16", 127, "pair")])
+def test_long_chunks_two_dynamic_tiles(dtype, horizon, attn):
     """Action chunks longer than one 64-key tile: T = 101 (a ragged second
     dynamic tile) and T = 128 (the largest supported), so the dynamic keys
-    span two tiles and the query rows several 128-row blocks."""
+    span two tiles and the query rows several query blocks."""
     cfg = RAGGED.replace(name=f"long_{dtype}_{horizon}", dtype=dtype, batch=2, action_horizon=horizon,
                          n_q_heads=2, head_dim=64, width=128, mlp_dim=128, cond_hidden=64, frame_dim=0,
-                         window_frames=2, num_steps=2)
+                         window_frames=2, num_steps=2, attn_kernel=attn)
     w, sk, sv, frames = _setup(cfg, 3)
     eng = R.ReflexEngine(cfg, w, sk, sv)
     for t in range(3):
