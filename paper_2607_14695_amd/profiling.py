@@ -22,10 +22,12 @@ Usage::
 
     python -m paper_2607_14695_amd.profiling --stats KT_kernel_stats.csv \\
         --fetch FETCH_counter_collection.csv --write WRITE_counter_collection.csv \\
-        --kernel "attn16_kernel<256>" --kernel-class attention --workload pi0_chunk_bf16 \\
+        --kernel "attn_pair_kernel<256>" --kernel-class attention --workload pi0_chunk_bf16 \\
         --command-kt "..." --command-fetch "..." --command-write "..." \\
         --out-md profiles/attention_pi0_chunk_bf16.md \\
         --out-json profiles/traffic_pi0_chunk_bf16.json
+
+The JSON file holds one record per kernel class of the workload.
 """
 from __future__ import annotations
 
@@ -206,20 +208,31 @@ def main(argv: Optional[List[str]] = None) -> None:
     with open(args.out_md, "w") as f:
         f.write("\n".join(md))
     if rec is not None and args.out_json:
+        # one file per workload, one record per kernel class (a rerun for a
+        # class replaces that class's record only)
+        try:
+            with open(args.out_json) as f:
+                doc = json.load(f)
+        except (OSError, ValueError):
+            doc = {}
+        records = doc.get("records", {})
+        records[args.kernel_class] = rec
         with open(args.out_json, "w") as f:
-            json.dump(rec, f, indent=1)
+            json.dump({"workload": args.workload, "records": records}, f, indent=1)
             f.write("\n")
 
 
 def load_traffic(path: str, kernel_class: str) -> Optional[int]:
-    """HBM bytes per launch from a traffic record, or None when the record is
-    missing, is for another kernel class, or the kernel's sources changed."""
+    """HBM bytes per launch of one kernel class from a workload's traffic
+    file, or None when there is no record for the class or the class's
+    sources changed since the counters were taken."""
     try:
         with open(path) as f:
-            rec = json.load(f)
+            doc = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_class") != kernel_class or rec.get("digest") != source_digest(kernel_class):
+    rec = doc.get("records", {}).get(kernel_class)
+    if rec is None or rec.get("digest") != source_digest(kernel_class):
         return None
     return int(rec["hbm_bytes_per_launch"])
 
