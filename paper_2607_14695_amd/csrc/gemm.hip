@@ -593,10 +593,10 @@ constexpr int DSTAGE = (TBM + TBN) * DROWB;  // bytes per stage (32 KB)
 // [x*per, (x+1)*per) of the tile sequence in which the M tile varies fastest,
 // so the workgroups sharing an L2 also share B (weight) tiles and a band of
 // A tiles instead of touching every tile of both operands.
-template <int PAIR>
+template <int PAIR, int BM>
 RFX_DEV bool dma_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
   const int nx = PAIR == PAIR_NONE ? (p.N + TBN - 1) / TBN : p.N / (PAIR == PAIR_N ? 64 : 128);
-  const int ny = (p.M + TBM - 1) / TBM;
+  const int ny = (p.M + BM - 1) / BM;
   const int total = nx * ny * p.batch * p.splits;
   const int per = (total + 7) / 8;
   const int t = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
@@ -608,11 +608,20 @@ RFX_DEV bool dma_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
   return true;
 }
 
-template <int EPI, int NS, int NSTC>
+// BM (128 or 96) rows per tile: two waves along M hold BM/2 rows each
+// (MB = BM/32 blocks of 16).  96-row tiles serve grids whose 128-row count
+// just exceeds one wave of workgroups (two tiles on a few CUs would set the
+// kernel time): 340 tiles of 96 at two per CU cost 3/4 of that.
+template <int EPI, int NS, int NSTC, int BM = TBM>
 __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   using T = bf16_t;
   constexpr int PAIR = EpiPair<EPI>::value;
+  // BM / 32: 16-row blocks per wave, and A copies (8 rows each) per wave per
+  // stage
   static_assert(NS == 2 || NS == 4, "two or four stages");
+  static_assert(BM == 128 || BM == 96, "128- or 96-row tiles");
+  static_assert(BM == 128 || NS == 2, "the four-stage wait counts assume 8 copies per stage");
+  // stages sized for 128 rows (a 96-row tile uses 28 of the 32 KB)
   __shared__ __attribute__((aligned(16))) unsigned char st0[DSTAGE];
   __shared__ __attribute__((aligned(16))) unsigned char st1[DSTAGE];
   __shared__ __attribute__((aligned(16))) unsigned char st2[NS == 4 ? DSTAGE : 16];
@@ -622,9 +631,9 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   const int r16 = lane & 15, g = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
   int bx, by, bz;
-  if (!dma_tile<PAIR>(p, bx, by, bz)) return;
+  if (!dma_tile<PAIR, BM>(p, bx, by, bz)) return;
   const int z = bz / p.splits, split = bz % p.splits;
-  const int m0 = by * TBM;
+  const int m0 = by * BM;
   int n0, pair_off;
   if constexpr (PAIR == PAIR_HEAD) {
     const int half = p.qkv.head_dim >> 1, per_head = half / 64;
@@ -649,16 +658,18 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   const T* A = reinterpret_cast<const T*>(p.A) + (int64_t)z * p.a_bstride;
   const T* B = reinterpret_cast<const T*>(p.B) + (int64_t)z * p.b_bstride;
 
-  // DMA: wave w, instruction j covers stage rows 8*(4w + j) + (lane >> 3) of A
-  // (j < 4) or B (j >= 4), physical chunk lane & 7 = logical (lane & 7) ^ (row & 7)
-  const T* gsrc[8];
+  // DMA, with NA = BM/32: wave w, instruction j covers stage rows
+  // 8*(NA*w + j) + (lane >> 3) of A (j < NA) or 8*(4w + j - NA) + (lane >> 3)
+  // of B (j >= NA); physical chunk lane & 7 holds logical chunk
+  // (lane & 7) ^ swizzle(row)
+  const T* gsrc[8];  // the first BM/32 + 4 are used (a bound that depends on BM breaks the lambda capture)
   {
     const int rr = lane >> 3, pc = lane & 7;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int row = 8 * (4 * wave + (j & 3)) + rr + (j >= 4 ? 0 : 0);
+    for (int j = 0; j < (BM / 32) + 4; ++j) {
+      const int row = (j < (BM / 32) ? 8 * ((BM / 32) * wave + j) : 8 * (4 * wave + j - (BM / 32))) + rr;
       const int lc = pc ^ RFX_GSWZ(row);
-      if (j < 4) {
+      if (j < (BM / 32)) {
         gsrc[j] = A + (int64_t)min(m0 + row, p.M - 1) * p.lda + kbeg + lc * 8;
       } else {
         int brw;
@@ -672,19 +683,19 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
       }
     }
   }
-  // stage layout: A rows 0..127 then B rows 0..127, 128 bytes each
+  // stage layout: A rows 0..BM-1 then B rows 0..127, 128 bytes each
   auto issue = [&](int st, unsigned char* buf) __attribute__((always_inline)) {
     const int k0 = st * DST;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int row = 8 * (4 * wave + (j & 3));
-      __builtin_amdgcn_global_load_lds(gsrc[j] + k0, buf + ((j >= 4 ? TBM : 0) + row) * DROWB, 16, 0, 0);
+    for (int j = 0; j < (BM / 32) + 4; ++j) {
+      const int row = j < (BM / 32) ? 8 * ((BM / 32) * wave + j) : BM + 8 * (4 * wave + j - (BM / 32));
+      __builtin_amdgcn_global_load_lds(gsrc[j] + k0, buf + row * DROWB, 16, 0, 0);
     }
   };
 
-  f32x4_v acc[4][4];
+  f32x4_v acc[(BM / 32)][4];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < (BM / 32); ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b) acc[a][b] = f32x4_v{0.f, 0.f, 0.f, 0.f};
 
@@ -718,15 +729,15 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
     if (st + NS - 1 < nst) issue(st + NS - 1, nxt);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      uint4 af[4], bf[4];
+      uint4 af[(BM / 32)], bf[4];
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-        af[mb] = *reinterpret_cast<const uint4*>(cur + (wm * 64 + mb * 16) * DROWB + foff[kk]);
+      for (int mb = 0; mb < (BM / 32); ++mb)
+        af[mb] = *reinterpret_cast<const uint4*>(cur + (wm * (BM / 2) + mb * 16) * DROWB + foff[kk]);
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb)
-        bf[nb] = *reinterpret_cast<const uint4*>(cur + (TBM + brow_l[nb]) * DROWB + foff[kk]);
+        bf[nb] = *reinterpret_cast<const uint4*>(cur + (BM + brow_l[nb]) * DROWB + foff[kk]);
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
+      for (int mb = 0; mb < (BM / 32); ++mb)
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb) mfma_step(acc[mb][nb], bf[nb], af[mb], T());  // C^T blocks
     }
@@ -761,8 +772,8 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   // acc[mb][nb] holds the transposed 16x16 block: lane (r16, g) has output
   // row m0 + wm*64 + mb*16 + r16, columns 4g .. 4g+3 of column block nb
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) {
-    const int grow = m0 + wm * 64 + mb * 16 + r16;
+  for (int mb = 0; mb < (BM / 32); ++mb) {
+    const int grow = m0 + wm * (BM / 2) + mb * 16 + r16;
     if (grow >= p.M) continue;
     if (PAIR != PAIR_NONE) {
 #pragma unroll
@@ -1247,7 +1258,14 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
     // workgroups covers the grid; else the two-stage one (two per CU)
     const int nst = a.k_per_split / DST;
     if (total > 256) {
-      RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+      // just over one wave of 128-row tiles: 96-row tiles, two per CU, when
+      // they fit in two waves' worth (the busiest CU then holds 2 x 96 rows
+      // instead of 2 x 128)
+      const int total96 = nx * ((a.M + 95) / 96) * a.batch * a.splits;
+      if (total <= 512 && total96 <= 512)
+        RFX_LAUNCH((gemm_dma<EPI, 2, 0, 96>), dim3((total96 + 7) / 8 * 8), dim3(256), 0, s, a);
+      else
+        RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
     } else if (a.K == a.k_per_split * a.splits && nst == 8) {
       RFX_LAUNCH((gemm_dma<EPI, 4, 8>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
     } else if (a.K == a.k_per_split * a.splits && nst == 16)
