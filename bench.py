@@ -443,6 +443,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-b32", action="store_true")
+    ap.add_argument("--no-long", action="store_true",
+                    help="skip the long-context stress chunk (batch 8, 8-frame ring, 6,400 cached tokens)")
     ap.add_argument("--no-latency", action="store_true",
                     help="skip the per-chunk event-timed latency distribution (for counter-collection runs)")
     ap.add_argument("--no-baselines", action="store_true",
@@ -556,6 +558,7 @@ def main():
             "chunk_ms": round(c32s * 1e3, 3),
             "denoise_step_us": round(c32s / c32.num_steps * 1e6, 1),
             "attn_hbm_gbs": round(bf32["attention"][0] / (a_ms / a_n / 1e3) / 1e9, 1),
+            "attn_mfma_tflops": round(bf32["attention"][1] / (a_ms / a_n / 1e3) / 1e12, 1),
             "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in p32.items() if v[1]},
         }
         for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
@@ -579,6 +582,35 @@ def main():
             b32["pipeline"] = _pipeline(c32, w32, sk32, sv32, fr32, st32, nz32, torch, 8, 2)
             log(f"b32 pipeline: {b32['pipeline']}")
         log(f"b32 tick {t32 * 1e3:.3f} ms, chunk {c32s * 1e3:.3f} ms")
+
+    long_ctx = None
+    if not args.no_long:
+        # the stress workload where the attention dominates: 8 envs, 256 static
+        # + 8 x 768 ring tokens, x64 embeddings, its own tau schedule
+        cl = WL.CONFIGS["pi0_long_bf16"]
+        wl, skl, svl, frl, stl, nzl = _device_inputs(cl, torch, seed=3)
+        el = ReflexEngine(cl, wl, skl, svl)
+        for f in range(cl.window_frames):
+            el.write_frame(frl[f % len(frl)])
+        cls_ = _time_ticks(el, frl, stl, nzl, max(3, args.steps // 3), 1, torch, denoise_only=True)
+        if not bool(torch.isfinite(el.denoise(stl, nzl)).all()):
+            raise RuntimeError("non-finite actions from the timed long-context configuration")
+        pl = el.profile(stl, nzl)
+        bfl = _class_bytes_flops(cl)
+        al_ms, al_n = pl["attention"]
+        long_ctx = {
+            "workload": "pi0_long_bf16 chunk: 8 envs, 256 static + 8 x 768 ring + 51 dynamic tokens, x64 "
+                        "embeddings, tau schedule near 0 and 1, 10 Euler steps",
+            "chunks_per_s": round(cl.batch / cls_, 2),
+            "chunk_ms": round(cls_ * 1e3, 3),
+            "attn_us": round(al_ms / al_n * 1e3, 2),
+            "attn_hbm_gbs": round(bfl["attention"][0] / (al_ms / al_n / 1e3) / 1e9, 1),
+            "attn_mfma_tflops": round(bfl["attention"][1] / (al_ms / al_n / 1e3) / 1e12, 1),
+            "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in pl.items() if v[1]},
+        }
+        el.close()
+        del el, wl
+        log(f"long context: {long_ctx}")
 
     stream = strategies = pipeline = scheduler = None
     if not (args.no_latency and args.no_baselines and args.no_pipeline and args.no_scheduler):
@@ -662,6 +694,7 @@ def main():
             "traffic": traffic,
         },
         "b32": b32,
+        "long_ctx": long_ctx,
         "cpu_baseline": cpu,
     }
     print(json.dumps(result), flush=True)
