@@ -56,7 +56,12 @@ KERNEL_SOURCES: Dict[str, Tuple[str, ...]] = {
 }
 
 COPY_BYTES = 256 << 20  # bytes read, and bytes written, by one calibration copy
+# The copy is torch.mul over 64 Mi fp32 elements; torch's vectorized
+# elementwise kernel runs one thread per 4 elements.  Other multiplies in the
+# same run (weight initialisation) share the kernel name, so a dispatch is
+# the copy only when its grid matches as well.
 COPY_PATTERN = re.compile(r"MulFunctor")
+COPY_GRID = (COPY_BYTES // 4) // 4
 
 
 def source_digest(kernel_class: str) -> str:
@@ -81,15 +86,17 @@ def counter_per_dispatch(path: str, counter: str, kernel_pattern: str) -> Tuple[
     dispatch are summed first."""
     per_dispatch: Dict[Tuple[str, str], float] = {}
     names: Dict[Tuple[str, str], str] = {}
+    grids: Dict[Tuple[str, str], int] = {}
     for r in _rows(path):
         if r["Counter_Name"] != counter:
             continue
         key = (r["Dispatch_Id"], r.get("Agent_Id", ""))
         per_dispatch[key] = per_dispatch.get(key, 0.0) + float(r["Counter_Value"])
         names[key] = r["Kernel_Name"]
+        grids[key] = int(r["Grid_Size"])
     pat = re.compile(kernel_pattern)
     vals = [v for k, v in per_dispatch.items() if pat.search(names[k])]
-    copies = [v for k, v in per_dispatch.items() if COPY_PATTERN.search(names[k])]
+    copies = [v for k, v in per_dispatch.items() if COPY_PATTERN.search(names[k]) and grids[k] == COPY_GRID]
     if not vals:
         raise ValueError(f"no dispatch of {kernel_pattern!r} with counter {counter} in {path}")
     if not copies:

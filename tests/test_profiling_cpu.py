@@ -23,15 +23,32 @@ def test_traffic_record_is_used_only_while_its_sources_match(tmp_path):
 
 def test_counter_per_dispatch_sums_instances_and_reads_the_copy(tmp_path):
     # two counter instances of one dispatch are summed; the calibration copy
-    # (MulFunctor) is reported separately
+    # (a multiply over 64 Mi fp32 elements) is reported separately, and other
+    # multiplies of the same kernel name (weight initialisation) are not
+    # taken for it, however many there are
+    mul = '"at::native::vectorized_elementwise_kernel<4, MulFunctor<float>>"'
     rows = [
-        "Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value",
-        "1,reflex::k<1>(args),FETCH_SIZE,10",
-        "1,reflex::k<1>(args),FETCH_SIZE,5",
-        "2,reflex::k<1>(args),FETCH_SIZE,30",
-        '3,"at::native::vectorized_elementwise_kernel<4, MulFunctor<float>>",FETCH_SIZE,400',
-    ]
+        "Dispatch_Id,Grid_Size,Kernel_Name,Counter_Name,Counter_Value",
+        "1,4096,reflex::k<1>(args),FETCH_SIZE,10",
+        "1,4096,reflex::k<1>(args),FETCH_SIZE,5",
+        "2,4096,reflex::k<1>(args),FETCH_SIZE,30",
+        f"3,{P.COPY_GRID},{mul},FETCH_SIZE,400",
+    ] + [f"{4 + i},11796480,{mul},FETCH_SIZE,300" for i in range(5)]
     path = tmp_path / "c.csv"
     path.write_text("\n".join(rows) + "\n")
     avg, n, copy = P.counter_per_dispatch(str(path), "FETCH_SIZE", r"reflex::k<1>")
     assert n == 2 and avg == 22.5 and copy == 400
+
+
+def test_counter_per_dispatch_requires_the_copy(tmp_path):
+    rows = ["Dispatch_Id,Grid_Size,Kernel_Name,Counter_Name,Counter_Value",
+            "1,4096,reflex::k<1>(args),FETCH_SIZE,10",
+            '2,11796480,"at::native::vectorized_elementwise_kernel<4, MulFunctor<float>>",FETCH_SIZE,300']
+    path = tmp_path / "c.csv"
+    path.write_text("\n".join(rows) + "\n")
+    try:
+        P.counter_per_dispatch(str(path), "FETCH_SIZE", r"reflex::k<1>")
+    except ValueError as e:
+        assert "calibration copy" in str(e)
+    else:
+        raise AssertionError("a run without the calibration copy must not yield a factor")
