@@ -63,16 +63,20 @@ extern "C" {
 #define REFLEX_NORM_BF16 1
 #define REFLEX_NORM_BF16_FP32_STATS 2
 
-/* Attention kernel of the bf16 path.  Both compute the same masked softmax
+/* Attention kernel of the bf16 path.  All compute the same masked softmax
  * over [static; ring window; dynamic] (Eq. 1) and agree to rounding.
- * REFLEX_ATTN_AUTO picks by the launch geometry: 16-row waves sharing each
- * key tile over 128 query rows, or one wave pair per 32 query rows when the
- * launch would reach one key tile per split (a few envs and a short context).
- * The other two values force one kernel (tests, tuning); the fp32 path has
- * one kernel and ignores the field. */
+ * REFLEX_ATTN_AUTO picks by the launch geometry: one wave pair per 32 query
+ * rows when the launch would reach one key tile per split (a few envs and a
+ * short context), otherwise 16-row waves sharing each key tile over 128
+ * query rows, software-pipelined (a tile's scores and softmax run under the
+ * previous tile's P.V MFMAs).  REFLEX_ATTN_ROWS16 forces the 16-row kernel
+ * without that pipelining (the same results bit for bit); the other values
+ * force one kernel (tests, tuning).  The fp32 path has one kernel and
+ * ignores the field. */
 #define REFLEX_ATTN_AUTO 0
 #define REFLEX_ATTN_ROWS16 1
 #define REFLEX_ATTN_PAIR 2
+#define REFLEX_ATTN_ROWS16_PIPE 3
 
 /*
  * Shape of the action expert and of the cache.

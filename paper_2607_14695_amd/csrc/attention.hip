@@ -566,6 +566,321 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
 }
 
 // ---------------------------------------------------------------------------
+// Software-pipelined 16-row variant: the decomposition, layouts, key order
+// and arithmetic of attn16_kernel, with the per-tile work reordered so that a
+// wave's softmax runs under its own MFMAs.  Iteration i computes S^T of tile
+// i+1, then O^T += V^T P^T of tile i interleaved with the softmax of tile
+// i+1.  That softmax takes the running max as it stands; when some row's tile
+// max exceeds it by more than 8 (the lazy-rescale test), O is rescaled after
+// the P.V step and the tile's exponentials are recomputed with the new max.
+// The operations and their order per row are those of attn16_kernel, so the
+// results are the same bit for bit.
+//
+// K and V^T have separate double buffers: at the start of iteration i the
+// copies of K(i+2) and V^T(i+1) go into the buffers K(i) and V^T(i-1) left,
+// and both land before iteration i+1 (one copy round in flight, 128 KB of
+// LDS as before).  Row max and row sum cross the four lane groups with the
+// gfx950 lane swaps (VALU), not LDS permutes, so they interleave with the
+// V^T fragment reads.
+// ---------------------------------------------------------------------------
+RFX_DEV float xmax16_32(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+RFX_DEV float xsum16_32(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+template <int DH>
+__global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
+  using T = bf16_t;
+  constexpr int NW = 8;
+  constexpr int NKS = DH / 32;            // 32-wide d steps of S^T
+  constexpr int NDB = DH / 16;            // 16-wide d blocks of O^T
+  constexpr int KRB = DH * 2;             // bytes per K row in LDS
+  constexpr int KCH = DH / 8;             // 16-byte chunks per K row
+  constexpr int NKO = KCH >= 16 ? 4 : 2;  // distinct per-lane K chunk offsets per parity
+  constexpr int VRB = AKT * 2;            // bytes per V^T row (128)
+  constexpr int KBYTES = AKT * KRB;
+  constexpr int VBYTES = DH * VRB;
+  constexpr int NIK = KBYTES / 1024 / NW;  // 1-KB DMA instructions per wave, K
+  constexpr int NIV = VBYTES / 1024 / NW;  // same for V^T
+  static_assert(NIK >= 1 && NIV >= 1, "tile smaller than one DMA round");
+  __shared__ __attribute__((aligned(16))) unsigned char kbuf0[KBYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char kbuf1[KBYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char vbuf0[VBYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char vbuf1[VBYTES];
+
+  int group, rb;
+  if (!attn_decode(blockIdx.x, p.B * p.nsplit, p.rows_pad / 128, group, rb)) return;
+  const int b = group / p.nsplit, split = group - b * p.nsplit;
+
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int T_ = p.T, Hq = p.Hq;
+  const int nrows = T_ * Hq;
+  const int rq = rb * 128 + wave * 16 + r16;
+  const bool qvalid = rq < nrows;
+  const int iq = qvalid ? rq / Hq : 0;
+  const int jq = qvalid ? rq % Hq : 0;
+
+  uint4 qf[NKS];
+  {
+    // rows past the valid range compute on row 0's data and are never stored
+    const T* qrow = reinterpret_cast<const T*>(p.q) + ((int64_t)b * p.rows_pad + (qvalid ? rq : 0)) * DH + g * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = ld16(qrow + ks * 32);
+  }
+
+  const int Lc = p.static_len + (*p.n_valid) * p.frame_tokens;
+  const int n_ct = (Lc + AKT - 1) / AKT;
+  const int n_dt = (T_ + AKT - 1) / AKT;
+  const int total = n_ct + n_dt;
+  const int per = (total + p.nsplit - 1) / p.nsplit;
+  const int t_beg = split * per;
+  const int t_end = min(total, t_beg + per);
+  const int n = t_end - t_beg;
+
+  const T* ck = reinterpret_cast<const T*>(p.cache_k) + (int64_t)b * p.ck_bstride;
+  const T* cvt = reinterpret_cast<const T*>(p.cache_vt) + (int64_t)b * p.ck_bstride;
+  const T* kdb = reinterpret_cast<const T*>(p.kd) + (int64_t)b * T_ * DH;
+  const T* vdb = reinterpret_cast<const T*>(p.vdt) + (int64_t)b * DH * p.tpad;
+  const float scale = rsqrtf((float)DH) * 1.4426950408889634f;
+  const int tpad = p.tpad, Rrow = p.R;  // copied: a lambda must not capture the kernel argument
+  const int hole = __builtin_amdgcn_readfirstlane(*p.hole_row), skip = p.frame_tokens;
+  constexpr int RPI = 64 / KCH;         // K rows per DMA instruction
+
+  // DMA of tile t's K rows / V^T columns.  Per-lane offsets are rebuilt from
+  // an opaque copy of the lane id on every call so they are not hoisted into
+  // registers.
+  auto issue_k = [&](int t, unsigned char* sk) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const bool dyn = t >= n_ct;
+    const int base = dyn ? (t - n_ct) * AKT : t * AKT;
+    const int last = (dyn ? T_ : Lc) - 1;
+    const int kl = ln % KCH, kr = ln / KCH;
+    if (dyn) {
+#pragma unroll
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        const int r = min(base + row, last);
+        __builtin_amdgcn_global_load_lds(kdb + r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8, sk + (wave * NIK + j) * 1024, 16,
+                                         0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NIK; ++j) {
+        const int row = RPI * (wave * NIK + j) + kr;
+        int r = min(base + row, last);
+        r += r >= hole ? skip : 0;
+        __builtin_amdgcn_global_load_lds(ck + (int64_t)r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8,
+                                         sk + (wave * NIK + j) * 1024, 16, 0, 0);
+      }
+    }
+  };
+  auto issue_v = [&](int t, unsigned char* sv) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const bool dyn = t >= n_ct;
+    const int base = dyn ? (t - n_ct) * AKT : t * AKT;
+    const int last = (dyn ? T_ : Lc) - 1;
+    const int vd = ln >> 3, vc = ln & 7;
+    if (dyn) {
+#pragma unroll
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        __builtin_amdgcn_global_load_lds(vdb + d * tpad + base + (vc ^ (d & 7)) * 8, sv + (wave * NIV + j) * 1024, 16,
+                                         0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NIV; ++j) {
+        const int d = (wave * NIV + j) * 8 + vd;
+        int key = base + (vc ^ (d & 7)) * 8;
+        key = key <= last ? key : 0;
+        key += key >= hole ? skip : 0;
+        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + key,
+                                         sv + (wave * NIV + j) * 1024, 16, 0, 0);
+      }
+    }
+  };
+
+  f32x4_v o[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) o[db] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // per-lane LDS read offsets (bytes), as in attn16_kernel
+  int koff[2][NKO], voff[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int rho = 8 * (r16 >> 2) + 4 * e + (r16 & 3);
+#pragma unroll
+    for (int x = 0; x < NKO; ++x) koff[e][x] = rho * KRB + ((4 * x + g) ^ RFX_KSWZ(rho, KCH)) * 16;
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) voff[j] = r16 * VRB + ((4 * j + g) ^ (r16 & 7)) * 16;
+
+  // S^T = K Q^T of the tile in sk: four 16-key blocks, chains interleaved
+  auto scores = [&](const unsigned char* sk, f32x4_v* s) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) s[kb] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k0 = 0; k0 < NKS; k0 += 2) {
+      uint4 a[2][4];
+#pragma unroll
+      for (int u = 0; u < 2 && k0 + u < NKS; ++u)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          const int ks = k0 + u;
+          a[u][kb] = *reinterpret_cast<const uint4*>(sk + (kb >> 1) * 32 * KRB + (ks / NKO) * NKO * 64 +
+                                                     koff[kb & 1][ks % NKO]);
+        }
+#pragma unroll
+      for (int u = 0; u < 2 && k0 + u < NKS; ++u)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) mfma_step(s[kb], a[u][kb], qf[k0 + u], T());
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+  };
+  // mask and scale tile t's scores in place; returns the row max over the tile
+  auto mask_max = [&](int t, f32x4_v* s) __attribute__((always_inline)) {
+    const bool dyn = t >= n_ct;
+    const int lim = (dyn ? (iq > 0 ? T_ : 1) - (t - n_ct) * AKT : Lc - t * AKT) - 8 * g;
+    float mt = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = (kb >> 1) * 32 + 4 * (kb & 1) + i < lim ? s[kb][i] * scale : -INFINITY;
+        s[kb][i] = v;
+        mt = fmaxf(mt, v);
+      }
+    return xmax16_32(mt);
+  };
+  // exponentials against m_use, packed as the two P^T operands; returns the
+  // row sum
+  auto expo = [&](const f32x4_v* s, float m_use, uint4* pf) __attribute__((always_inline)) {
+    float e[4][4];
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        e[kb][i] = __builtin_amdgcn_exp2f(s[kb][i] - m_use);
+        psum += e[kb][i];
+      }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      pf[j] = make_uint4(pack_bf16x2(e[2 * j][0], e[2 * j][1]), pack_bf16x2(e[2 * j][2], e[2 * j][3]),
+                         pack_bf16x2(e[2 * j + 1][0], e[2 * j + 1][1]),
+                         pack_bf16x2(e[2 * j + 1][2], e[2 * j + 1][3]));
+    return xsum16_32(psum);
+  };
+  // lazy rescale test for a tile whose exponentials were taken against the
+  // running max; on a rescale they are taken again against the new one
+  auto commit = [&](float mt, const f32x4_v* s, uint4* pf, float psum) __attribute__((always_inline)) {
+    if (__any(mt > m_run + 8.f)) {
+      const float m_new = fmaxf(m_run, mt);
+      const float corr = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+      l_run *= corr;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db] *= corr;
+      psum = expo(s, m_run == -INFINITY ? 0.f : m_run, pf);
+    }
+    l_run += psum;
+  };
+  // O^T += V^T P^T of the tile in sv; slot 8g + 4e + i <-> key 32j + 8g + 4e + i
+  auto pv = [&](const unsigned char* sv, const uint4* pf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int d0 = 0; d0 < NDB; d0 += 8) {
+        uint4 vf[8];
+#pragma unroll
+        for (int u = 0; u < 8 && d0 + u < NDB; ++u)
+          vf[u] = *reinterpret_cast<const uint4*>(sv + (d0 + u) * 16 * VRB + voff[j]);
+#pragma unroll
+        for (int u = 0; u < 8 && d0 + u < NDB; ++u) mfma_step(o[d0 + u], vf[u], pf[j], T());
+      }
+  };
+
+  uint4 pcur[2], pnext[2];
+  // iteration i: S^T of tile i+1 (K in kn), then P.V of tile i (V^T in vc)
+  // under tile i+1's softmax; K(i+2) goes to kf, V^T(i+1) to vn
+  auto iter = [&](int i, const unsigned char* kn, unsigned char* kf, const unsigned char* vc, unsigned char* vn)
+                  __attribute__((always_inline)) {
+    // K(i+1) and V^T(i) complete; every wave is done with K(i) and V^T(i-1)
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    lds_barrier();
+    if (i + 2 < n) issue_k(t_beg + i + 2, kf);
+    issue_v(t_beg + i + 1, vn);
+    f32x4_v s[4];
+    scores(kn, s);
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    const float mt = mask_max(t_beg + i + 1, s);
+    const float psum = expo(s, m_use, pnext);
+    pv(vc, pcur);
+    commit(mt, s, pnext, psum);
+    pcur[0] = pnext[0];
+    pcur[1] = pnext[1];
+  };
+
+  if (n > 0) {
+    issue_k(t_beg, kbuf0);
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    lds_barrier();
+    if (n > 1) issue_k(t_beg + 1, kbuf1);
+    issue_v(t_beg, vbuf0);
+    f32x4_v s[4];
+    scores(kbuf0, s);
+    const float mt = mask_max(t_beg, s);
+    const float psum = expo(s, 0.f, pcur);
+    commit(mt, s, pcur, psum);
+    // tile i's K sits in kbuf[i & 1] and its V^T in vbuf[i & 1]
+    int i = 0;
+    for (; i + 2 < n; i += 2) {
+      iter(i, kbuf1, kbuf0, vbuf0, vbuf1);
+      iter(i + 1, kbuf0, kbuf1, vbuf1, vbuf0);
+    }
+    if (i + 1 < n) {
+      iter(i, kbuf1, kbuf0, vbuf0, vbuf1);
+      ++i;
+    }
+    // last tile: its P.V only
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+    lds_barrier();
+    pv((i & 1) ? vbuf1 : vbuf0, pcur);
+  }
+
+  if (!qvalid) return;
+  if (p.nsplit == 1) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    T* dst = reinterpret_cast<T*>(p.out) + ((int64_t)b * T_ + iq) * (int64_t)(Hq * DH) + jq * DH + 4 * g;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      *reinterpret_cast<uint2*>(dst + db * 16) =
+          make_uint2(pack_bf16x2(o[db][0] * inv, o[db][1] * inv), pack_bf16x2(o[db][2] * inv, o[db][3] * inv));
+    return;
+  }
+  const int64_t prow = ((int64_t)b * p.nsplit + split) * p.rows_pad + rq;
+  T* dst = reinterpret_cast<T*>(p.part_o) + prow * DH + 4 * g;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+    *reinterpret_cast<uint2*>(dst + db * 16) =
+        make_uint2(pack_bf16x2(o[db][0], o[db][1]), pack_bf16x2(o[db][2], o[db][3]));
+  if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
+}
+
+// ---------------------------------------------------------------------------
 // bf16 variant with wave pairs.  Two waves share 32 query rows (two 16-row
 // blocks): for S^T = K Q^T wave h takes keys [32h, 32h + 32) of the tile, for
 // O^T = V^T P^T it takes head dims [h*DH/2, (h+1)*DH/2) over all 64 keys.
@@ -956,11 +1271,12 @@ int attention_rows_per_block(int elem_bytes) { return elem_bytes == 2 ? 128 : 64
 
 // Kernel and key-split count for (B envs, rows query rows, up to max_keys
 // cached keys).  One workgroup per CU is resident (LDS bound), so both aim
-// for about one wave of workgroups over the 256 CUs.  The 16-row variant
-// covers 128 rows per workgroup; when that grid would reach one key tile per
+// for about one wave of workgroups over the 256 CUs.  The 16-row variants
+// cover 128 rows per workgroup; when that grid would reach one key tile per
 // split (a few envs, short context) the launch is latency-bound and the
-// wave-pair variant (32 rows per workgroup, one tile per split) is used.
-// `force` (ATTN_AUTO, ATTN_ROWS16 or ATTN_PAIR) overrides the choice.
+// wave-pair variant (32 rows per workgroup, one tile per split) is used,
+// otherwise the software-pipelined 16-row kernel.  `force` (ATTN_AUTO,
+// ATTN_ROWS16, ATTN_PAIR or ATTN_ROWS16_PIPE) overrides the choice.
 AttnPlan attention_plan(int B, int rows, int max_keys, int elem_bytes, int force) {
   const int tiles = (max_keys + AKT - 1) / AKT + 1;
   AttnPlan pl;
@@ -972,6 +1288,8 @@ AttnPlan attention_plan(int B, int rows, int max_keys, int elem_bytes, int force
     if (force == ATTN_PAIR || (force == ATTN_AUTO && latency)) {
       pl.kernel = ATTN_PAIR;
       base = B * ((rows + 31) / 32);
+    } else if (force != ATTN_ROWS16) {
+      pl.kernel = ATTN_ROWS16_PIPE;
     }
   }
   int s = 256 / base;
@@ -989,6 +1307,8 @@ static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
     const int g8 = ((groups + 7) / 8) * 8;
     if (a.kernel == ATTN_PAIR)
       RFX_LAUNCH((attn_pair_kernel<DH>), dim3(g8 * ((rows + 31) / 32)), dim3(128), 0, s, a);
+    else if (a.kernel == ATTN_ROWS16_PIPE)
+      RFX_LAUNCH((attn16p_kernel<DH>), dim3(g8 * (a.rows_pad / 128)), dim3(512), 0, s, a);
     else
       RFX_LAUNCH((attn16_kernel<DH>), dim3(g8 * (a.rows_pad / 128)), dim3(512), 0, s, a);
   } else {
@@ -1007,7 +1327,7 @@ static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
 template <typename T>
 hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s) {
   if (a.nsplit < 1 || a.nsplit > kMaxSplits || a.rows_pad % 128) return hipErrorInvalidValue;
-  if (a.kernel != ATTN_ROWS16 && a.kernel != ATTN_PAIR) return hipErrorInvalidValue;
+  if (a.kernel != ATTN_ROWS16 && a.kernel != ATTN_PAIR && a.kernel != ATTN_ROWS16_PIPE) return hipErrorInvalidValue;
   switch (head_dim) {
     case 64: launch_attn_dh<T, 64>(a, s); break;
     case 128: launch_attn_dh<T, 128>(a, s); break;

@@ -82,14 +82,15 @@ struct AttnArgs {
   float* part_ml;         // [B][nsplit][rows_pad][2]
   int rows_pad;
   void* out;              // [B*T][Hq*dh]
-  int kernel;             // bf16 path: ATTN_ROWS16 or ATTN_PAIR
+  int kernel;             // bf16 path: ATTN_ROWS16, ATTN_PAIR or ATTN_ROWS16_PIPE
 };
 template <typename T> hipError_t launch_attention(const AttnArgs& a, int head_dim, hipStream_t s);
 template <typename T> hipError_t launch_attn_merge(const AttnArgs& a, int head_dim, hipStream_t s);
 int attention_rows_per_block(int elem_bytes);
-// bf16 attention kernels: 16-row waves (128 rows per workgroup) or one wave
-// pair per workgroup (32 rows); ATTN_AUTO picks by the launch geometry
-enum AttnKernel : int { ATTN_AUTO = 0, ATTN_ROWS16 = 1, ATTN_PAIR = 2 };
+// bf16 attention kernels: 16-row waves (128 rows per workgroup; plain or
+// software-pipelined, equal bit for bit) or one wave pair per workgroup (32
+// rows); ATTN_AUTO picks by the launch geometry
+enum AttnKernel : int { ATTN_AUTO = 0, ATTN_ROWS16 = 1, ATTN_PAIR = 2, ATTN_ROWS16_PIPE = 3 };
 struct AttnPlan {
   int kernel;
   int splits;

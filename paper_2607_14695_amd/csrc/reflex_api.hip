@@ -125,7 +125,7 @@ int validate(const reflex_config* c) {
   if (c->window_frames < 1) return REFLEX_EINVAL;
   if (c->spare_slot != 0 && c->spare_slot != 1) return REFLEX_EINVAL;
   if (c->norm_precision < REFLEX_NORM_FP32 || c->norm_precision > REFLEX_NORM_BF16_FP32_STATS) return REFLEX_EINVAL;
-  if (c->attn_kernel < REFLEX_ATTN_AUTO || c->attn_kernel > REFLEX_ATTN_PAIR) return REFLEX_EINVAL;
+  if (c->attn_kernel < REFLEX_ATTN_AUTO || c->attn_kernel > REFLEX_ATTN_ROWS16_PIPE) return REFLEX_EINVAL;
   if (c->frame_dim < 0 || c->frame_dim % 8) return REFLEX_EINVAL;
   if (c->batch < 1 || c->batch > 4096) return REFLEX_EINVAL;
   if (c->max_steps < 1 || c->max_steps > REFLEX_MAX_STEPS) return REFLEX_EINVAL;

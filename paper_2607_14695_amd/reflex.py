@@ -37,7 +37,7 @@ MODE_NAIVE = 2
 MODE_UNFUSED = 3
 MODES = {"reflex": MODE_REFLEX, "standard": MODE_STANDARD, "naive": MODE_NAIVE, "unfused": MODE_UNFUSED}
 NORM_PRECISIONS = {"fp32": 0, "bf16": 1, "bf16_fp32_stats": 2}
-ATTN_KERNELS = {"auto": 0, "rows16": 1, "pair": 2}
+ATTN_KERNELS = {"auto": 0, "rows16": 1, "pair": 2, "rows16p": 3}
 
 c_i32, c_i64, c_f32, c_f64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_void_p
 

@@ -68,7 +68,7 @@ def test_query_sizes_rejects_bad_configs():
                        ("dtype", 7), ("max_steps", 0), ("max_steps", 65), ("frame_tokens", 12),
                        ("static_len", -8), ("batch", 0), ("window_frames", 0), ("state_dim", 5),
                        ("spare_slot", 2), ("spare_slot", -1), ("norm_precision", 3), ("norm_precision", -1),
-                       ("attn_kernel", 3), ("attn_kernel", -1)]:
+                       ("attn_kernel", 4), ("attn_kernel", -1)]:
         c = R.config_to_c(WL.CONFIGS["tiny_fp32"])
         setattr(c, field, bad)
         assert R.query_sizes_status(c) == R.REFLEX_EINVAL, field

@@ -182,7 +182,7 @@ def test_ragged_multi_env(frame_dim):
 BF16_REL, BF16_ABS = 1e-2, 5e-2
 
 
-@pytest.mark.parametrize("attn", ["rows16", "pair"])
+@pytest.mark.parametrize("attn", ["rows16", "rows16p", "pair"])
 @pytest.mark.parametrize("head_dim,frame_dim", [(64, 72), (128, 0), (256, 48)])
 def test_ragged_bf16(head_dim, frame_dim, attn):
     """The bf16 path (bf16 attention tiles, bf16 GEMM operands) at every head
@@ -207,6 +207,39 @@ def test_ragged_bf16(head_dim, frame_dim, attn):
             print(f"bf16 dh={head_dim} {attn} tick {t}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
             assert rel <= BF16_REL and mx <= BF16_ABS, (t, rel, mx)
     eng.close()
+
+
+@pytest.mark.parametrize("head_dim", [64, 256])
+def test_multi_tile_splits_pipelined_equals_rows16(head_dim):
+    """Key splits of several tiles each: two envs and a 20-frame ring of
+    200-token frames give 21 to 65 key tiles over 16 splits, so a split runs
+    2, 3, 4 or 5 tiles (odd and even counts, the pipelined kernel's loop and
+    its tail).  Frame keys are scaled by 1, 2 and 4 for frames 0-6, 7-13 and
+    14-19 (exact in bf16), so tile maxima grow by more than the lazy-rescale
+    threshold inside a split.  The pipelined 16-row kernel must equal the
+    plain one bit for bit (same operations in the same order per row), and
+    both must match the oracle within the bf16 tolerance."""
+    cfg = RAGGED.replace(name=f"multi_tile_{head_dim}", dtype="bf16", batch=2, static_len=40, frame_tokens=200,
+                         window_frames=20, action_horizon=7, n_q_heads=2, head_dim=head_dim, frame_dim=0,
+                         num_steps=2)
+    w, sk, sv, frames = _setup(cfg, 20)
+    for f in frames:
+        frames[f][:, :, 0] *= float(2 ** (f // 7))
+    engs = {a: R.ReflexEngine(cfg.replace(attn_kernel=a), w, sk, sv) for a in ("rows16", "rows16p")}
+    for t in range(20):
+        for e in engs.values():
+            e.write_frame(frames[t])
+        if t + 1 in (6, 11, 16, 20):
+            state, noise = WL.make_state(cfg, t), WL.make_noise(cfg, t)
+            got = {a: e.denoise(state, noise).cpu().numpy().copy() for a, e in engs.items()}
+            assert np.array_equal(got["rows16"], got["rows16p"]), t
+            ref = O.denoise_chunk(cfg, w, sk, sv, frames, t + 1, state, noise, cfg.taus())
+            rel = float(np.linalg.norm(got["rows16p"] - ref) / np.linalg.norm(ref))
+            mx = float(np.max(np.abs(got["rows16p"] - ref)))
+            print(f"multi-tile dh={head_dim} frames {t + 1}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+            assert rel <= BF16_REL and mx <= BF16_ABS, (t, rel, mx)
+    for e in engs.values():
+        e.close()
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -236,7 +269,8 @@ def test_limits_t64_no_static_prefix(dtype):
 
 @pytest.mark.parametrize("dtype,horizon,attn", [("f32", 100, "auto"), ("bf16", 100, "rows16"),
                                                 ("bf16", 127, "rows16"), ("bf16", 100, "pair"),
-                                                ("bf16", 127, "pair")])
+                                                ("bf16", 127, "pair"), ("bf16", 100, "rows16p"),
+                                                ("bf16", 127, "rows16p")])
 def test_long_chunks_two_dynamic_tiles(dtype, horizon, attn):
     """Action chunks longer than one 64-key tile: T = 101 (a ragged second
     dynamic tile) and T = 128 (the largest supported), so the dynamic keys
