@@ -596,6 +596,23 @@ RFX_DEV float xsum16_32(float v) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Copy of 16 bytes per lane from global memory into LDS (global_load_lds,
+// LDS destination from M0), issued through inline assembly: the compiler
+// then does not track these LDS writes and waits for its own LDS reads with
+// partial counts instead of draining every outstanding read first.  Every
+// kernel that uses it orders the copies itself: a vmcnt(0) wait and a
+// barrier come before any read of a stage, and no stage is overwritten
+// before a barrier that follows its last read.  Outstanding copies it does
+// not know of only make the compiler's own vmcnt waits stricter (loads
+// complete in order).  M0 is a reserved register the compiler sets right
+// before each instruction of its own that reads it, so it is not declared
+// clobbered (it cannot be); the kernels using this helper contain no other
+// M0 reader.
+RFX_DEV void lds_dma16(const void* g, void* lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"((unsigned)(size_t)lds) : "memory");
+}
+
 template <int DH>
 __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
   using T = bf16_t;
@@ -670,8 +687,7 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
       for (int j = 0; j < NIK; ++j) {
         const int row = RPI * (wave * NIK + j) + kr;
         const int r = min(base + row, last);
-        __builtin_amdgcn_global_load_lds(kdb + r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8, sk + (wave * NIK + j) * 1024, 16,
-                                         0, 0);
+        lds_dma16(kdb + r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8, sk + (wave * NIK + j) * 1024);
       }
     } else {
 #pragma unroll
@@ -679,8 +695,7 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
         const int row = RPI * (wave * NIK + j) + kr;
         int r = min(base + row, last);
         r += r >= hole ? skip : 0;
-        __builtin_amdgcn_global_load_lds(ck + (int64_t)r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8,
-                                         sk + (wave * NIK + j) * 1024, 16, 0, 0);
+        lds_dma16(ck + (int64_t)r * DH + (kl ^ RFX_KSWZ(row, KCH)) * 8, sk + (wave * NIK + j) * 1024);
       }
     }
   };
@@ -695,8 +710,7 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
 #pragma unroll
       for (int j = 0; j < NIV; ++j) {
         const int d = (wave * NIV + j) * 8 + vd;
-        __builtin_amdgcn_global_load_lds(vdb + d * tpad + base + (vc ^ (d & 7)) * 8, sv + (wave * NIV + j) * 1024, 16,
-                                         0, 0);
+        lds_dma16(vdb + d * tpad + base + (vc ^ (d & 7)) * 8, sv + (wave * NIV + j) * 1024);
       }
     } else {
 #pragma unroll
@@ -705,8 +719,7 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
         int key = base + (vc ^ (d & 7)) * 8;
         key = key <= last ? key : 0;
         key += key >= hole ? skip : 0;
-        __builtin_amdgcn_global_load_lds(cvt + (int64_t)d * Rrow + key,
-                                         sv + (wave * NIV + j) * 1024, 16, 0, 0);
+        lds_dma16(cvt + (int64_t)d * Rrow + key, sv + (wave * NIV + j) * 1024);
       }
     }
   };
