@@ -1212,16 +1212,21 @@ __global__ __launch_bounds__(128) void attn_pair_kernel(AttnArgs p) {
 }
 
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
-// splits combined in index order.  One thread per (query row, 4 consecutive d).
+// splits combined in index order.  One thread per (query row, VEC
+// consecutive d): 16-byte accesses (8 bf16 or 4 fp32 values) when the grid
+// still holds a wave of blocks, else 8-byte ones (4 bf16) for twice the
+// blocks at a few envs.
 // The partial O_s are fp32 on the fp32 path and bf16 on the bf16 path.
 constexpr int kMaxSplits = 16;
 
-template <typename T, int DH>
+template <typename T, int DH, int VEC>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
-  constexpr int TPR = DH / 4;     // threads per row, four consecutive d each
-  constexpr int RPB = 256 / TPR;  // rows per block
+  static_assert(VEC * sizeof(T) == 16 || VEC * sizeof(T) == 8, "8- or 16-byte accesses");
+  using Raw = typename std::conditional<VEC * sizeof(T) == 16, uint4, uint2>::type;
+  constexpr int TPR = DH / VEC;             // threads per row
+  constexpr int RPB = 256 / TPR;            // rows per block
   const int b = blockIdx.y;
-  const int rsub = threadIdx.x / TPR, d = (threadIdx.x % TPR) * 4;
+  const int rsub = threadIdx.x / TPR, d = (threadIdx.x % TPR) * VEC;
   const int rq = blockIdx.x * RPB + rsub;
   const int nrows = p.T * p.Hq;
   if (rq >= nrows) return;
@@ -1229,7 +1234,6 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   // all loads of this thread are independent: one memory round trip
   // (the raw partials are converted only after every load is issued)
   float2 ml[kMaxSplits];
-  using Raw = typename std::conditional<sizeof(T) == 2, uint2, float4>::type;
   Raw raw[kMaxSplits];
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s) {
@@ -1239,44 +1243,45 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
       raw[s] = *reinterpret_cast<const Raw*>(reinterpret_cast<const T*>(p.part_o) + prow * DH + d);
     }
   }
-  float4 ov[kMaxSplits];
-#pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s) {
-    if constexpr (sizeof(T) == 2) {
-      const uint2 w = *reinterpret_cast<const uint2*>(&raw[s]);
-      ov[s] = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
-                          __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
-    } else {
-      ov[s] = *reinterpret_cast<const float4*>(&raw[s]);
-    }
-  }
   float M = -INFINITY;
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s)
     if (s < p.nsplit) M = fmaxf(M, ml[s].x);
   const float Mu = (M == -INFINITY) ? 0.f : M;
   float L = 0.f;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float acc[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
 #pragma unroll
   for (int s = 0; s < kMaxSplits; ++s)
     if (s < p.nsplit) {
       const float w = exp2f(ml[s].x - Mu);
       L += w * ml[s].y;
-      acc.x += w * ov[s].x;
-      acc.y += w * ov[s].y;
-      acc.z += w * ov[s].z;
-      acc.w += w * ov[s].w;
+      const uint32_t* wd = reinterpret_cast<const uint32_t*>(&raw[s]);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        float v;
+        if constexpr (sizeof(T) == 2)
+          v = __uint_as_float((e & 1) ? (wd[e >> 1] & 0xffff0000u) : (wd[e >> 1] << 16));
+        else
+          v = __uint_as_float(wd[e]);
+        acc[e] += w * v;
+      }
     }
   const float inv = L > 0.f ? 1.f / L : 0.f;
   const int i = rq / p.Hq, j = rq % p.Hq;
   T* dst = reinterpret_cast<T*>(p.out) + ((int64_t)b * p.T + i) * (int64_t)(p.Hq * DH) + j * DH + d;
-  const float v[4] = {acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv};
+  Raw outw;
+  uint32_t* w = reinterpret_cast<uint32_t*>(&outw);
   if constexpr (sizeof(T) == 2) {
-    *reinterpret_cast<uint2*>(dst) = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                                                (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+#pragma unroll
+    for (int e = 0; e < VEC / 2; ++e)
+      w[e] = (uint32_t)f2bf(acc[2 * e] * inv) | ((uint32_t)f2bf(acc[2 * e + 1] * inv) << 16);
   } else {
-    *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) w[e] = __float_as_uint(acc[e] * inv);
   }
+  *reinterpret_cast<Raw*>(dst) = outw;
 }
 
 // Query rows per attention workgroup: 128 on the bf16 path, 64 on fp32.
@@ -1332,9 +1337,16 @@ static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
 
 template <typename T, int DH>
 static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
-  constexpr int RPB = 256 / (DH / 4);
-  dim3 grid((a.T * a.Hq + RPB - 1) / RPB, a.B);
-  RFX_LAUNCH((attn_merge_kernel<T, DH>), grid, dim3(256), 0, s, a);
+  constexpr int V16 = 16 / (int)sizeof(T);
+  constexpr int RPB16 = 256 / (DH / V16);
+  const int rows = a.T * a.Hq;
+  const int blocks16 = (rows + RPB16 - 1) / RPB16 * a.B;
+  if (sizeof(T) == 4 || blocks16 >= 256) {
+    RFX_LAUNCH((attn_merge_kernel<T, DH, V16>), dim3((rows + RPB16 - 1) / RPB16, a.B), dim3(256), 0, s, a);
+  } else {
+    constexpr int RPB8 = 256 / (DH / 4);
+    RFX_LAUNCH((attn_merge_kernel<T, DH, 4>), dim3((rows + RPB8 - 1) / RPB8, a.B), dim3(256), 0, s, a);
+  }
 }
 
 template <typename T>
