@@ -1255,8 +1255,11 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
       return;
     }
     // four-stage unrolled pipeline (one workgroup per CU) when one wave of
-    // workgroups covers the grid; else the two-stage one (two per CU)
-    const int nst = a.k_per_split / DST;
+    // workgroups covers the grid; else the two-stage one (two per CU).  The
+    // stage count is that of every split's K range (a single split may be
+    // given a range past K: its range is then K).
+    const int kr1 = a.splits == 1 ? a.K : (a.K == a.k_per_split * a.splits ? a.k_per_split : 0);
+    const int nst = kr1 % DST == 0 ? kr1 / DST : 0;
     if (total > 256) {
       // just over one wave of 128-row tiles: 96-row tiles, two per CU, when
       // they fit in two waves' worth (the busiest CU then holds 2 x 96 rows
@@ -1266,11 +1269,11 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
         RFX_LAUNCH((gemm_dma<EPI, 2, 0, 96>), dim3((total96 + 7) / 8 * 8), dim3(256), 0, s, a);
       else
         RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
-    } else if (a.K == a.k_per_split * a.splits && nst == 8) {
+    } else if (nst == 8) {
       RFX_LAUNCH((gemm_dma<EPI, 4, 8>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
-    } else if (a.K == a.k_per_split * a.splits && nst == 16)
+    } else if (nst == 16)
       RFX_LAUNCH((gemm_dma<EPI, 4, 16>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
-    else if (a.K == a.k_per_split * a.splits && nst == 32)
+    else if (nst == 32)
       RFX_LAUNCH((gemm_dma<EPI, 4, 32>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
     else
       RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
