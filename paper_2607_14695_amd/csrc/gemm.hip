@@ -608,7 +608,12 @@ RFX_DEV bool dma_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
   return true;
 }
 
-// BM (128 or 96) rows per tile: two waves along M hold BM/2 rows each
+// s_waitcnt operand: wait until at most n vector-memory operations are
+// outstanding (vmcnt bits [3:0] and [15:14]); expcnt and lgkmcnt left at their
+// maxima (no wait)
+constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// BM (128, 96 or 64) rows per tile: two waves along M hold BM/2 rows each
 // (MB = BM/32 blocks of 16).  96-row tiles serve grids whose 128-row count
 // just exceeds one wave of workgroups (two tiles on a few CUs would set the
 // kernel time): 340 tiles of 96 at two per CU cost 3/4 of that.
@@ -619,8 +624,8 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   // BM / 32: 16-row blocks per wave, and A copies (8 rows each) per wave per
   // stage
   static_assert(NS == 2 || NS == 4, "two or four stages");
-  static_assert(BM == 128 || BM == 96, "128- or 96-row tiles");
-  static_assert(BM == 128 || NS == 2, "the four-stage wait counts assume 8 copies per stage");
+  static_assert(BM == 128 || BM == 96 || BM == 64, "128-, 96- or 64-row tiles");
+  constexpr int CPS = BM / 32 + 4;  // copy instructions per wave per stage
   // stages sized for 128 rows (a 96-row tile uses 28 of the 32 KB)
   __shared__ __attribute__((aligned(16))) unsigned char st0[DSTAGE];
   __shared__ __attribute__((aligned(16))) unsigned char st1[DSTAGE];
@@ -713,14 +718,14 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
       brow_l[nb] = wn * 64 + nb * 16;
   }
 
-  // four stages: st, st+1, st+2 in flight at the start of stage st (eight
-  // instructions each); two stages: only st
+  // four stages: st, st+1, st+2 in flight at the start of stage st (CPS
+  // instructions each, completing in order); two stages: only st
   auto step = [&](int st, const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt)
                   __attribute__((always_inline)) {
     if (NS == 4 && st + 2 < nst)
-      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 0 | (1 << 14));  // vmcnt(16)
+      __builtin_amdgcn_s_waitcnt(vmcnt_enc(2 * CPS));
     else if (NS == 4 && st + 1 < nst)
-      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8) | 8);  // vmcnt(8)
+      __builtin_amdgcn_s_waitcnt(vmcnt_enc(CPS));
     else
       __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
     // every wave's share of stage st is in LDS and every wave has finished
@@ -1269,14 +1274,26 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
         RFX_LAUNCH((gemm_dma<EPI, 2, 0, 96>), dim3((total96 + 7) / 8 * 8), dim3(256), 0, s, a);
       else
         RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
-    } else if (nst == 8) {
-      RFX_LAUNCH((gemm_dma<EPI, 4, 8>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
-    } else if (nst == 16)
-      RFX_LAUNCH((gemm_dma<EPI, 4, 16>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
-    else if (nst == 32)
-      RFX_LAUNCH((gemm_dma<EPI, 4, 32>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
-    else
+    } else if (nst == 8 || nst == 16 || nst == 32) {
+      // 64-row tiles when even those stay within one wave of workgroups:
+      // more CUs, each with half the K loop's work (QKV at 8 envs: 140
+      // workgroups instead of 80)
+      const int total64 = nx * ((a.M + 63) / 64) * a.batch * a.splits;
+      const dim3 g64((total64 + 7) / 8 * 8), g128((total + 7) / 8 * 8);
+      const bool t64 = total64 <= 256;
+      if (nst == 8) {
+        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 8, 64>), g64, dim3(256), 0, s, a);
+        else RFX_LAUNCH((gemm_dma<EPI, 4, 8>), g128, dim3(256), 0, s, a);
+      } else if (nst == 16) {
+        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 16, 64>), g64, dim3(256), 0, s, a);
+        else RFX_LAUNCH((gemm_dma<EPI, 4, 16>), g128, dim3(256), 0, s, a);
+      } else {
+        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 32, 64>), g64, dim3(256), 0, s, a);
+        else RFX_LAUNCH((gemm_dma<EPI, 4, 32>), g128, dim3(256), 0, s, a);
+      }
+    } else {
       RFX_LAUNCH((gemm_dma<EPI, 2, 0>), dim3((total + 7) / 8 * 8), dim3(256), 0, s, a);
+    }
   }
   else
     RFX_LAUNCH((gemm_tiled<T, EPI>), grid, dim3(256), 0, s, a);
