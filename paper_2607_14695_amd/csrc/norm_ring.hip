@@ -227,18 +227,31 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   }
   __syncthreads();
   // v[a] = sum_c y[c] W[a][c]: eight threads per output, each a strided
-  // eighth of the columns, so the weight loads of a pass are independent and
-  // in flight together; the eight partial sums meet in three xor shuffles
+  // eighth of the columns; the partial sums meet in three xor shuffles.  A
+  // thread issues GU weight loads before it uses any (one L2 round trip per
+  // GU columns instead of per column); the sum runs in column order.
   const T* W = reinterpret_cast<const T*>(p.w_aout);
   const int part = threadIdx.x & 7;
+  constexpr int GU = 8;
   for (int a0 = 0; a0 < p.da; a0 += 32) {
     const int a = a0 + (threadIdx.x >> 3);
     const int ar = a < p.da ? a : p.da - 1;  // clamped row: a valid address, result unused
     float acc = 0.f;
-    for (int c4 = part; c4 < D4; c4 += 8) {
-      const float4 w = ld4f(W + (int64_t)ar * p.D + c4 * 4);
-      const float4 y = ys[c4];
-      acc += w.x * y.x + w.y * y.y + w.z * y.z + w.w * y.w;
+    for (int c0 = part; c0 < D4; c0 += 8 * GU) {
+      float4 w[GU];
+#pragma unroll
+      for (int u = 0; u < GU; ++u) {
+        const int c4 = min(c0 + 8 * u, D4 - 1);  // clamped column: a valid address, result unused
+        w[u] = ld4f(W + (int64_t)ar * p.D + c4 * 4);
+      }
+#pragma unroll
+      for (int u = 0; u < GU; ++u) {
+        const int c4 = c0 + 8 * u;
+        if (c4 < D4) {
+          const float4 y = ys[c4];
+          acc += w[u].x * y.x + w[u].y * y.y + w[u].z * y.z + w[u].w * y.w;
+        }
+      }
     }
     acc += __shfl_xor(acc, 1, 64);
     acc += __shfl_xor(acc, 2, 64);
