@@ -1164,13 +1164,15 @@ int gemm_pick_splits(int M, int N, int K, int elem_bytes) {
     while (base * s * 2 <= 256 && K % (64 * s * 2) == 0 && K / (s * 2) >= 512) s *= 2;
     // the same with 64-row tiles (which the launcher takes when they fit one
     // wave): fewer splits, so fewer fp32 partials for the residual to read,
-    // if every split's K range is still a four-stage count (8, 16 or 32
-    // stages).  Down projection at 8 envs: 4 splits instead of 8.
+    // if every split's K range is still a four-stage count of at most 16
+    // stages (a 32-stage loop on 64-row tiles, 8 accumulators per wave, was
+    // slower than two splits on 128-row tiles).  Down projection at 8 envs:
+    // 4 splits instead of 8.
     const int base64 = ((N + TBN - 1) / TBN) * ((M + 63) / 64);
     int s64 = 1;
     while (base64 * s64 * 2 <= 256 && K % (64 * s64 * 2) == 0 && K / (s64 * 2) >= 512) s64 *= 2;
     const int nst64 = K % (64 * s64) == 0 ? K / (64 * s64) : 0;
-    if (s64 < s && (nst64 == 8 || nst64 == 16 || nst64 == 32)) s = s64;
+    if (s64 < s && (nst64 == 8 || nst64 == 16)) s = s64;
     return s;
   }
   if (base >= 256 || K < 1024) return 1;
