@@ -367,26 +367,71 @@ __global__ __launch_bounds__(256) void ring_write_kernel(RingWriteArgs p) {
   T* ck = reinterpret_cast<T*>(p.cache_k) + ((int64_t)b * p.L + l) * (int64_t)p.R * DH;
   T* cv = reinterpret_cast<T*>(p.cache_vt) + ((int64_t)b * p.L + l) * (int64_t)p.R * DH;
   const int ntok = min(TJ, p.n_tok - j0);
+  constexpr int H2 = DH / 2;
+  // vector accesses (4 elements per load, 8 tokens per V^T store) when every
+  // base and stride they touch is aligned for them; else element by element.
+  // The arithmetic per element is the same either way.
+  const uintptr_t amask = (uintptr_t)(4 * sizeof(S)) - 1;
+  const bool vec = (((uintptr_t)sk | (uintptr_t)sv) & amask) == 0 && (p.sj & 3) == 0 &&
+                   (((uintptr_t)p.rope) & 15) == 0 && (((uintptr_t)ck | (uintptr_t)cv) & (8 * sizeof(T) - 1)) == 0 &&
+                   (p.row0 & 7) == 0 && (p.R & 7) == 0;
   // K with RoPE: pairs (f, f + DH/2)
-  for (int e = threadIdx.x; e < ntok * (DH / 2); e += 256) {
-    const int jj = e / (DH / 2), f = e % (DH / 2);
-    const int j = j0 + jj;
-    const S* src = sk + (int64_t)j * p.sj;
-    const float lo = to_f(src[f]), hi = to_f(src[f + DH / 2]);
-    const float2 cs = p.rope[(int64_t)j * (DH / 2) + f];
-    T* dst = ck + (int64_t)(p.row0 + j) * DH;
-    dst[f] = from_f<T>(lo * cs.x - hi * cs.y);
-    dst[f + DH / 2] = from_f<T>(hi * cs.x + lo * cs.y);
+  if (vec) {
+    for (int e = threadIdx.x; e < ntok * (H2 / 4); e += 256) {
+      const int jj = e / (H2 / 4), f = (e % (H2 / 4)) * 4;
+      const int j = j0 + jj;
+      const S* src = sk + (int64_t)j * p.sj;
+      const float4 lo = ld4f(src + f), hi = ld4f(src + f + H2);
+      const float4* csp = reinterpret_cast<const float4*>(p.rope + (int64_t)j * H2 + f);
+      const float4 c01 = csp[0], c23 = csp[1];  // (cos, sin) of f, f+1 and of f+2, f+3
+      T* dst = ck + (int64_t)(p.row0 + j) * DH;
+      st4(dst + f, make_float4(lo.x * c01.x - hi.x * c01.y, lo.y * c01.z - hi.y * c01.w, lo.z * c23.x - hi.z * c23.y,
+                               lo.w * c23.z - hi.w * c23.w));
+      st4(dst + f + H2, make_float4(hi.x * c01.x + lo.x * c01.y, hi.y * c01.z + lo.y * c01.w,
+                                    hi.z * c23.x + lo.z * c23.y, hi.w * c23.z + lo.w * c23.w));
+    }
+  } else {
+    for (int e = threadIdx.x; e < ntok * H2; e += 256) {
+      const int jj = e / H2, f = e % H2;
+      const int j = j0 + jj;
+      const S* src = sk + (int64_t)j * p.sj;
+      const float lo = to_f(src[f]), hi = to_f(src[f + H2]);
+      const float2 cs = p.rope[(int64_t)j * H2 + f];
+      T* dst = ck + (int64_t)(p.row0 + j) * DH;
+      dst[f] = from_f<T>(lo * cs.x - hi * cs.y);
+      dst[f + H2] = from_f<T>(hi * cs.x + lo * cs.y);
+    }
   }
-  // V transposed
-  for (int e = threadIdx.x; e < ntok * DH; e += 256) {
-    const int jj = e / DH, d = e % DH;
-    vt[jj][d] = to_f(sv[(int64_t)(j0 + jj) * p.sj + d]);
+  // V transposed through LDS
+  if (vec) {
+    for (int e = threadIdx.x; e < ntok * (DH / 4); e += 256) {
+      const int jj = e / (DH / 4), d = (e % (DH / 4)) * 4;
+      const float4 v = ld4f(sv + (int64_t)(j0 + jj) * p.sj + d);
+      vt[jj][d] = v.x;
+      vt[jj][d + 1] = v.y;
+      vt[jj][d + 2] = v.z;
+      vt[jj][d + 3] = v.w;
+    }
+  } else {
+    for (int e = threadIdx.x; e < ntok * DH; e += 256) {
+      const int jj = e / DH, d = e % DH;
+      vt[jj][d] = to_f(sv[(int64_t)(j0 + jj) * p.sj + d]);
+    }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < ntok * DH; e += 256) {
-    const int d = e / ntok, jj = e % ntok;
-    cv[(int64_t)d * p.R + p.row0 + j0 + jj] = from_f<T>(vt[jj][d]);
+  if (vec && ntok == TJ) {
+    // eight consecutive tokens of one d per thread
+    for (int e = threadIdx.x; e < DH * (TJ / 8); e += 256) {
+      const int d = e / (TJ / 8), j8 = (e % (TJ / 8)) * 8;
+      T* dst = cv + (int64_t)d * p.R + p.row0 + j0 + j8;
+      st4(dst, make_float4(vt[j8][d], vt[j8 + 1][d], vt[j8 + 2][d], vt[j8 + 3][d]));
+      st4(dst + 4, make_float4(vt[j8 + 4][d], vt[j8 + 5][d], vt[j8 + 6][d], vt[j8 + 7][d]));
+    }
+  } else {
+    for (int e = threadIdx.x; e < ntok * DH; e += 256) {
+      const int d = e / ntok, jj = e % ntok;
+      cv[(int64_t)d * p.R + p.row0 + j0 + jj] = from_f<T>(vt[jj][d]);
+    }
   }
 }
 
