@@ -1231,6 +1231,16 @@ static void launch_skinny(const GemmArgs& a, hipStream_t s) {
   if (sizeof(T) == 2 && (size_t)16 * skinny_mb(a.M) * ((klen * 2 + 127) & ~127) <= 160 * 1024 &&
       a.k_per_split % 32 == 0 &&
       a.K % 32 == 0) {
+    // an unsplit GEMM with few column strips (QKV at one env: 80) takes its
+    // rows in two 32-row halves: twice the workgroups, each copying half the
+    // activation rows; both halves of a strip land on the same XCD (nx is a
+    // multiple of 8), so its weights come from HBM once
+    constexpr int PAIR = EpiPair<EPI>::value;
+    const int nx = PAIR == PAIR_HEAD ? a.N / 32 : (PAIR == PAIR_N ? a.N / 16 : (a.N + 31) / 32);
+    if (skinny_mb(a.M) == 4 && a.splits == 1 && nx < 128 && nx % 8 == 0) {
+      launch_skinny_lds_pick<2, EPI>(a, s);
+      return;
+    }
     switch (skinny_mb(a.M)) {
       case 1: launch_skinny_lds_pick<1, EPI>(a, s); return;
       case 2: launch_skinny_lds_pick<2, EPI>(a, s); return;
