@@ -1214,15 +1214,16 @@ __global__ __launch_bounds__(128) void attn_pair_kernel(AttnArgs p) {
 // Merge the key splits: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,
 // splits combined in index order.  One thread per (query row, VEC
 // consecutive d): 16-byte accesses (8 bf16 or 4 fp32 values) when the grid
-// still holds a wave of blocks, else 8-byte ones (4 bf16) for twice the
-// blocks at a few envs.
+// still holds a wave of blocks, else 4-byte ones (2 bf16) for four times the
+// blocks at a few envs (one env: 3.45 -> 3.13 us against 8-byte ones).
 // The partial O_s are fp32 on the fp32 path and bf16 on the bf16 path.
 constexpr int kMaxSplits = 16;
 
 template <typename T, int DH, int VEC>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
-  static_assert(VEC * sizeof(T) == 16 || VEC * sizeof(T) == 8, "8- or 16-byte accesses");
-  using Raw = typename std::conditional<VEC * sizeof(T) == 16, uint4, uint2>::type;
+  static_assert(VEC * sizeof(T) == 16 || VEC * sizeof(T) == 8 || VEC * sizeof(T) == 4, "4-, 8- or 16-byte accesses");
+  using Raw = typename std::conditional<VEC * sizeof(T) == 16, uint4,
+                                        typename std::conditional<VEC * sizeof(T) == 8, uint2, uint32_t>::type>::type;
   constexpr int TPR = DH / VEC;             // threads per row
   constexpr int RPB = 256 / TPR;            // rows per block
   const int b = blockIdx.y;
@@ -1344,8 +1345,8 @@ static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
   if (sizeof(T) == 4 || blocks16 >= 256) {
     RFX_LAUNCH((attn_merge_kernel<T, DH, V16>), dim3((rows + RPB16 - 1) / RPB16, a.B), dim3(256), 0, s, a);
   } else {
-    constexpr int RPB8 = 256 / (DH / 4);
-    RFX_LAUNCH((attn_merge_kernel<T, DH, 4>), dim3((rows + RPB8 - 1) / RPB8, a.B), dim3(256), 0, s, a);
+    constexpr int RPB4 = 256 / (DH / 2);
+    RFX_LAUNCH((attn_merge_kernel<T, DH, 2>), dim3((rows + RPB4 - 1) / RPB4, a.B), dim3(256), 0, s, a);
   }
 }
 
