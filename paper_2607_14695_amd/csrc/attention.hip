@@ -15,15 +15,19 @@
 // and dynamic keys, and transposed dynamic values zero-padded to 64 columns,
 // so the dynamic tile is staged exactly like a cached tile.
 //
-// Decomposition and placement.  A workgroup owns one 64-row query block of one
-// env and a contiguous range of 64-key tiles (a key split); the dynamic tile
-// comes last.  All query blocks of one (env, split) group share the same K/V
-// tiles, so the 1-D grid is laid out such that a group's blocks are
-// dispatched to the same XCD (workgroups go round-robin over the 8 XCDs): the
-// tiles then come from HBM once and from that XCD's L2 for the other blocks.
-// Each tile's K rows and V^T columns are staged in LDS and reused by the
-// block's 64 rows (4 waves x 16 rows); the next tile's global loads are issued
-// into registers before the current tile's MFMAs.
+// Decomposition and placement.  A workgroup owns one query block of one env
+// (64 rows on the fp32 path; 128 rows as eight 16-row waves, or 32 rows as
+// one wave pair, on the bf16 path) and a contiguous range of 64-key tiles (a
+// key split); the dynamic tile comes last.  All query blocks of one (env,
+// split) group share the same K/V tiles, so the 1-D grid is laid out such
+// that a group's blocks are dispatched to the same XCD (workgroups go
+// round-robin over the 8 XCDs): the tiles then come from HBM once and from
+// that XCD's L2 for the other blocks.  Each tile's K rows and V^T columns are
+// staged in LDS and reused by every row of the block.  The fp32 kernel loads
+// the next tile into registers during the current one's MFMAs; the bf16
+// kernels copy it into a second LDS stage with global_load_lds, and the
+// software-pipelined one also computes the next tile's scores and softmax
+// under the current tile's P.V.
 //
 // Per wave the scores are computed transposed, S^T = K Q^T (A = K rows from
 // LDS, B = the wave's 16 query rows held in registers).  In that layout each
@@ -31,7 +35,8 @@
 // exp(S^T - m) is already the B operand of O^T = V^T P^T: the probabilities
 // never leave registers.  V is stored transposed (d-major) so V^T[d][keys] is
 // a contiguous LDS read.  Online softmax in base 2; the row max / sum cross
-// the 4 lane groups with two xor shuffles.
+// the 4 lane groups with two xor shuffles (lane swaps on the pipelined
+// kernel).
 //
 // With more than one key split each block writes (O unnormalised, m, l) and a
 // merge kernel combines the splits with log-sum-exp weights in a fixed order.
