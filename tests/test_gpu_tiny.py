@@ -242,6 +242,29 @@ def test_multi_tile_splits_pipelined_equals_rows16(head_dim):
         e.close()
 
 
+def test_tiled_gemms_on_64_row_tiles_bf16():
+    """Eight envs of 51 dynamic rows (M = 408 GEMM rows) at width 512 with
+    128-wide heads: the packed QKV (RoPE epilogue), gate|up (gated GELU) and
+    down (fp32 output) GEMMs all take the tiled path with 64-row tiles on the
+    four-stage pipeline (8 stages of 64 over K = 512), every env checked
+    against the oracle within the bf16 tolerance."""
+    cfg = RAGGED.replace(name="tiled64_bf16", dtype="bf16", batch=8, action_horizon=50, width=512, mlp_dim=512,
+                         n_q_heads=2, head_dim=128, frame_dim=0, n_layers=1, num_steps=2, window_frames=2)
+    w, sk, sv, frames = _setup(cfg, 2)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(2):
+        eng.write_frame(frames[t])
+    state, noise = WL.make_state(cfg, 1), WL.make_noise(cfg, 1)
+    got = eng.denoise(state, noise).cpu().numpy()
+    eng.synchronize()
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 2, state, noise, cfg.taus())
+    rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    mx = float(np.max(np.abs(got - ref)))
+    print(f"tiled 64-row: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+    assert rel <= BF16_REL and mx <= BF16_ABS, (rel, mx)
+    eng.close()
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_limits_t64_no_static_prefix(dtype):
     """Boundary shapes: 63 actions (T = 64, a full dynamic tile and T*Hq = 192
