@@ -242,14 +242,18 @@ def test_multi_tile_splits_pipelined_equals_rows16(head_dim):
         e.close()
 
 
-def test_tiled_gemms_on_64_row_tiles_bf16():
-    """Eight envs of 51 dynamic rows (M = 408 GEMM rows) at width 512 with
-    128-wide heads: the packed QKV (RoPE epilogue), gate|up (gated GELU) and
-    down (fp32 output) GEMMs all take the tiled path with 64-row tiles on the
-    four-stage pipeline (8 stages of 64 over K = 512), every env checked
-    against the oracle within the bf16 tolerance."""
-    cfg = RAGGED.replace(name="tiled64_bf16", dtype="bf16", batch=8, action_horizon=50, width=512, mlp_dim=512,
-                         n_q_heads=2, head_dim=128, frame_dim=0, n_layers=1, num_steps=2, window_frames=2)
+@pytest.mark.parametrize("batch", [1, 8])
+def test_gemm_row_tilings_bf16(batch):
+    """51 dynamic rows per env at width 512 with 128-wide heads.  Eight envs
+    (M = 408 GEMM rows): the packed QKV (RoPE epilogue), gate|up (gated GELU)
+    and down (fp32 output) GEMMs take the tiled path with 64-row tiles on the
+    four-stage pipeline (8 stages of 64 over K = 512).  One env (M = 51): the
+    unsplit skinny GEMMs with few column strips (QKV, gate|up) take their rows
+    in two 32-row halves, and the split merge its 4-byte form.  Every env is
+    checked against the oracle within the bf16 tolerance."""
+    cfg = RAGGED.replace(name=f"rowtile_bf16_b{batch}", dtype="bf16", batch=batch, action_horizon=50, width=512,
+                         mlp_dim=512, n_q_heads=2, head_dim=128, frame_dim=0, n_layers=1, num_steps=2,
+                         window_frames=2)
     w, sk, sv, frames = _setup(cfg, 2)
     eng = R.ReflexEngine(cfg, w, sk, sv)
     for t in range(2):
@@ -260,7 +264,7 @@ def test_tiled_gemms_on_64_row_tiles_bf16():
     ref = O.denoise_chunk(cfg, w, sk, sv, frames, 2, state, noise, cfg.taus())
     rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
     mx = float(np.max(np.abs(got - ref)))
-    print(f"tiled 64-row: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+    print(f"row tilings B={batch}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
     assert rel <= BF16_REL and mx <= BF16_ABS, (rel, mx)
     eng.close()
 
