@@ -32,17 +32,27 @@ RFX_DEV void st4(bf16_t* p, float4 v) {
 }
 RFX_DEV float4 f4add(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
 
-// sum of nparts split-K partial rows, fixed order, loads issued in groups of 4
-RFX_DEV float4 sum_parts(const float* pp, int64_t stride, int nparts) {
+// sum of nparts split-K partial rows in index order.  The loads of a group
+// of G partials are all issued before any is added, so up to G partials cost
+// one memory round trip (a loop with a dynamic trip count would wait for each
+// group's loads before issuing the next).
+template <int G>
+RFX_DEV float4 sum_parts_g(const float* pp, int64_t stride, int nparts) {
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  int s = 0;
-  for (; s + 4 <= nparts; s += 4) {
-    const float4 a0 = ld4f(pp + (s + 0) * stride), a1 = ld4f(pp + (s + 1) * stride);
-    const float4 a2 = ld4f(pp + (s + 2) * stride), a3 = ld4f(pp + (s + 3) * stride);
-    acc = f4add(acc, a0); acc = f4add(acc, a1); acc = f4add(acc, a2); acc = f4add(acc, a3);
+  for (int s0 = 0; s0 < nparts; s0 += G) {
+    float4 a[G];
+#pragma unroll
+    for (int i = 0; i < G; ++i) a[i] = ld4f(pp + (int64_t)min(s0 + i, nparts - 1) * stride);  // clamped: valid, unused
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+      if (s0 + i < nparts) acc = f4add(acc, a[i]);
   }
-  for (; s < nparts; ++s) acc = f4add(acc, ld4f(pp + s * stride));
   return acc;
+}
+RFX_DEV float4 sum_parts(const float* pp, int64_t stride, int nparts) {
+  if (nparts <= 2) return sum_parts_g<2>(pp, stride, nparts);
+  if (nparts <= 4) return sum_parts_g<4>(pp, stride, nparts);
+  return sum_parts_g<8>(pp, stride, nparts);
 }
 
 // bf16 rounding of an fp32 value (round to nearest even), kept in fp32
@@ -132,9 +142,8 @@ hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // residual + norm: one block per row, 4 columns per thread
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, int MAXC>  // MAXC 4-column chunks per thread: D <= 1024 * MAXC
 __global__ __launch_bounds__(256) void resid_norm_kernel(ResidArgs p) {
-  constexpr int MAXC = 4;  // D <= 4096: at most four 4-column chunks per thread
   __shared__ float red[4];
   const int m = blockIdx.x, b = m / p.T;
   const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
@@ -151,9 +160,9 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(ResidArgs p) {
       const int c = c4 * 4;
       sc[u] = ld4f(nmod + c);
       sh[u] = ld4f(nmod + p.D + c);
-      const float4 acc = sum_parts(p.parts + (int64_t)m * p.D + c, p.part_stride, p.nparts);
       const float4 h = ld4f(p.h + (int64_t)m * p.D + c);
       const float4 gt = ld4f(gmod + c);
+      const float4 acc = sum_parts(p.parts + (int64_t)m * p.D + c, p.part_stride, p.nparts);
       v[u] = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
       if (p.norm_mode != NORM_FP32) v[u] = rbf4(v[u]);  // bf16 residual stream
       ss = add_ssq(ss, v[u], p.norm_mode == NORM_BF16);
@@ -177,14 +186,20 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(ResidArgs p) {
 template <typename T>
 hipError_t launch_resid_norm(const ResidArgs& a, hipStream_t s) {
   if (a.D > 16 * 256 || (a.D & 3)) return hipErrorInvalidValue;
-  RFX_LAUNCH((resid_norm_kernel<T>), dim3(a.M), dim3(256), 0, s, a);
+  // registers for only as many column chunks as the row needs
+  if (a.D <= 1024)
+    RFX_LAUNCH((resid_norm_kernel<T, 1>), dim3(a.M), dim3(256), 0, s, a);
+  else if (a.D <= 2048)
+    RFX_LAUNCH((resid_norm_kernel<T, 2>), dim3(a.M), dim3(256), 0, s, a);
+  else
+    RFX_LAUNCH((resid_norm_kernel<T, 4>), dim3(a.M), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // last residual + final norm + action head + Euler: one block per action row
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, int MAXC>  // MAXC 4-column chunks per thread: D <= 1024 * MAXC
 __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   __shared__ float red[4];
   __shared__ float4 ys[4 * 256];
@@ -195,7 +210,6 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
   const float* fmod = p.final_mod + (int64_t)b * 3 * p.D;
   const int D4 = p.D >> 2;
-  constexpr int MAXC = 4;  // D <= 4096
   float4 sc[MAXC], sh[MAXC];
   float ss = 0.f;
 #pragma unroll
@@ -205,9 +219,9 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
       const int c = c4 * 4;
       sc[u] = ld4f(fmod + c);  // loaded with the residual inputs: one round trip
       sh[u] = ld4f(fmod + p.D + c);
-      const float4 acc = sum_parts(p.parts + m * p.D + c, p.part_stride, p.nparts);
       const float4 h = ld4f(p.h + m * p.D + c);
       const float4 gt = ld4f(gmod + c);
+      const float4 acc = sum_parts(p.parts + m * p.D + c, p.part_stride, p.nparts);
       float4 v = make_float4(h.x + gt.x * acc.x, h.y + gt.y * acc.y, h.z + gt.z * acc.z, h.w + gt.w * acc.w);
       if (p.norm_mode != NORM_FP32) v = rbf4(v);  // bf16 residual stream
       ys[c4] = v;
@@ -266,7 +280,13 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
 template <typename T>
 hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s) {
   if (a.D > 16 * 256 || (a.D & 3) || a.da > 64) return hipErrorInvalidValue;
-  RFX_LAUNCH((final_euler_kernel<T>), dim3(a.B * (a.T - 1)), dim3(256), 0, s, a);
+  const dim3 grid(a.B * (a.T - 1));
+  if (a.D <= 1024)
+    RFX_LAUNCH((final_euler_kernel<T, 1>), grid, dim3(256), 0, s, a);
+  else if (a.D <= 2048)
+    RFX_LAUNCH((final_euler_kernel<T, 2>), grid, dim3(256), 0, s, a);
+  else
+    RFX_LAUNCH((final_euler_kernel<T, 4>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
