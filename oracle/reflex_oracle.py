@@ -42,10 +42,11 @@ Model readings where the paper is silent (all in float64):
 
 Weights use the "rows are output features" convention: y = x @ W.T.
 
-Parity status: each function below names the test that pins it; the end-to-end
-numeric values beyond those pins are "parity unpinned" (the paper prints no
-worked numerical example); they are fixed only by the definitions above and the
-invariants in tests/test_oracle_pins.py.
+Parity status: each function below names what pins it.  The whole chunk is
+also pinned end to end at micro and tiny shapes by re-derivations that share
+nothing with this module (scalar loops, torch library routines) and rebuild
+the cached context from the raw sources with hand-enumerated positions
+(tests/test_oracle_pins.py); the paper prints no worked numerical example.
 """
 from __future__ import annotations
 
@@ -201,7 +202,11 @@ def dyn_pos0(cfg, frames_written: int) -> int:
 # context K/V from sources (no cache)
 # ---------------------------------------------------------------------------
 def static_kv(cfg, static_k: np.ndarray, static_v: np.ndarray, layer: int, env: int):
-    """Pinned prefix K (RoPE at 0..Ls-1) and V for one env and layer: [Ls, Hkv, dh]."""
+    """Pinned prefix K (RoPE at 0..Ls-1) and V for one env and layer: [Ls, Hkv, dh].
+
+    Pinned by positions read back from its output and by the raw-source
+    brute force of the whole chunk.
+    """
     Hkv, dh = cfg.n_kv_heads, cfg.head_dim
     k = np.asarray(static_k[env, layer], F64).reshape(-1, Hkv, dh)
     v = np.asarray(static_v[env, layer], F64).reshape(-1, Hkv, dh)
@@ -214,7 +219,9 @@ def frame_kv(cfg, weights, frame_env: np.ndarray, frame_index: int, layer: int):
 
     Embedding path (frame_dim > 0): K = E W_k^T, V = E W_v^T with the layer's
     frame projection, RoPE on K at the frame's absolute positions.  Direct path
-    (frame_dim == 0): the frame carries pre-RoPE K/V per layer.
+    (frame_dim == 0): the frame carries pre-RoPE K/V per layer.  Pinned by
+    positions read back from its output against the hand-enumerated ring trace
+    and by the raw-source brute force of the whole chunk.
     """
     Hkv, dh, F = cfg.n_kv_heads, cfg.head_dim, cfg.frame_tokens
     pos = cfg.static_len + frame_index * F + np.arange(F)

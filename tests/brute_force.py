@@ -135,3 +135,52 @@ def velocity_loops(cfg, weights, state, x, tau, ctx_k, ctx_v, dyn_pos):
         y = _norm_mod(h[t], scf, shf, cfg.rms_eps)
         out.append(_matvec(W["w_aout"], y))
     return out
+
+
+def context_loops(cfg, weights, static_k, static_v, frames, window, env, static_pos, frame_pos):
+    """Cached K/V of every layer rebuilt from the raw sources with loops.
+
+    static_k / static_v: [B][L][Ls][Hkv*dh] pre-RoPE prefix; frames: frame
+    index -> per-env frame ([B][F][frame_dim] embeddings, or [B][L][2][F][Hkv*dh]
+    pre-RoPE K then V); window: the frame indices in the window, oldest first.
+    static_pos: the Ls prefix positions; frame_pos[f]: the F positions of frame f.
+    On the embedding path the frame projection w_kv[l] holds the Hkv*dh K rows
+    first and then the Hkv*dh V rows (the packed layout the C header documents).
+    RoPE goes on K only.  Returns per-layer lists of context rows, each row a
+    list of Hkv heads of dh floats: (keys, values).
+    """
+    Hkv, dh, L = cfg.n_kv_heads, cfg.head_dim, cfg.n_layers
+    sk = _tolist(static_k)[env]
+    sv = _tolist(static_v)[env]
+    keys, vals = [], []
+    for l in range(L):
+        kl, vl = [], []
+        for r in range(cfg.static_len):
+            kl.append([_rot(sk[l][r][j * dh:(j + 1) * dh], static_pos[r], cfg.rope_theta) for j in range(Hkv)])
+            vl.append([list(sv[l][r][j * dh:(j + 1) * dh]) for j in range(Hkv)])
+        for f in window:
+            fr = _tolist(frames[f])[env]
+            for t in range(cfg.frame_tokens):
+                if cfg.frame_dim > 0:
+                    wkv = _tolist(weights["w_kv"])[l]
+                    e = fr[t]
+                    krow = [sum(wkv[o][i] * e[i] for i in range(cfg.frame_dim)) for o in range(Hkv * dh)]
+                    vrow = [sum(wkv[Hkv * dh + o][i] * e[i] for i in range(cfg.frame_dim)) for o in range(Hkv * dh)]
+                else:
+                    krow = list(fr[l][0][t])
+                    vrow = list(fr[l][1][t])
+                kl.append([_rot(krow[j * dh:(j + 1) * dh], frame_pos[f][t], cfg.rope_theta) for j in range(Hkv)])
+                vl.append([vrow[j * dh:(j + 1) * dh] for j in range(Hkv)])
+        keys.append(kl)
+        vals.append(vl)
+    return keys, vals
+
+
+def euler_loops(vel, x0, taus):
+    """x_{k+1} = x_k + (tau_{k+1} - tau_k) v(x_k, tau_k) on lists of rows."""
+    x = [list(r) for r in _tolist(x0)]
+    for k in range(len(taus) - 1):
+        v = vel(x, float(taus[k]))
+        dt = float(taus[k + 1]) - float(taus[k])
+        x = [[x[i][j] + dt * v[i][j] for j in range(len(x[i]))] for i in range(len(x))]
+    return x

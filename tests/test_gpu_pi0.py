@@ -169,6 +169,8 @@ def test_pi0_stream_bf16_500_ticks():
 
 def test_pi0_batch32_bf16_sampled_envs():
     cfg, eng, exp, envs = _run_stream("pi0_batch32_bf16")
+    state, noise = _io(cfg, 199, envs)
+    _check_steps(cfg, eng, exp, 199, 31, state, noise)
     eng.close()
 
 

@@ -202,11 +202,7 @@ def test_partitioned_attention_equals_full():
 
 # ---------------------------------------------------------------- ring
 def test_ring_trace_golden():
-    rows = []
-    with open(os.path.join(GOLDEN, "ring_trace_w2_f32_ls64.txt")) as fh:
-        for line in fh:
-            if line.strip() and not line.startswith("#"):
-                rows.append([int(t) for t in line.split()])
+    rows = _trace_rows()
     assert len(rows) == 5
     for f, slot, p0, p1, nv, ev, dyn in rows:
         st = O.ring_step(f, 2, 32, 64)
@@ -243,21 +239,116 @@ def _inputs(cfg, ticks):
     return w, sk, sv, frames
 
 
+# Hand-enumerated bookkeeping of the micro shape (static_len 3, 2-token frames,
+# a 2-frame ring) after frames 0, 1, 2 were written: the FIFO window holds
+# frames 1 and 2 (frame 2 sits in slot 0 after the wrap); frame f token j is at
+# 3 + 2f + j, the static prefix at 0, 1, 2, and the three dynamic tokens follow
+# the newest frame at 3 + 3*2 = 9, 10, 11.
+MICRO_WINDOW = [1, 2]
+MICRO_STATIC_POS = [0, 1, 2]
+MICRO_FRAME_POS = {1: [5, 6], 2: [7, 8]}
+MICRO_DYN_POS = [9, 10, 11]
+
+
 @pytest.mark.parametrize("frame_dim,mod_mode,hkv", [(5, "full", 1), (0, "full", 1), (5, "scale_only", 2)])
-def test_velocity_matches_scalar_brute_force(frame_dim, mod_mode, hkv):
+def test_chunk_matches_scalar_brute_force(frame_dim, mod_mode, hkv):
+    """The oracle's whole chunk (its own window, positions, context K/V and
+    Euler loop) against scalar loops that rebuild the context from the raw
+    static K/V, frames and w_kv rows, with hand-enumerated positions."""
     cfg = WL.micro_config(frame_dim=frame_dim, mod_mode=mod_mode, n_kv_heads=hkv,
                           embed_scale=1.5 if hkv == 2 else 1.0)
     w, sk, sv, frames = _inputs(cfg, 3)
-    fw = 3  # ring has wrapped once
-    state = WL.make_state(cfg, 0)[0]
-    x = WL.make_noise(cfg, 0)[0]
-    pos = O.dyn_pos0(cfg, fw) + np.arange(cfg.action_horizon + 1)
-    attend = O.full_batch_attend(cfg, w, sk, sv, frames, fw, 0)
-    v = O.velocity(cfg, w, state, x, 0.6, pos, attend)
-    ctx = [O.context_kv(cfg, w, sk, sv, frames, fw, l, 0) for l in range(cfg.n_layers)]
-    ref = brute_force.velocity_loops(cfg, w, state, x, 0.6, [c[0] for c in ctx], [c[1] for c in ctx],
-                                     list(pos))
-    np.testing.assert_allclose(v, np.array(ref), rtol=0, atol=1e-12)
+    fw = 3  # the ring has wrapped once
+    state = WL.make_state(cfg, 0)
+    noise = WL.make_noise(cfg, 0)
+    taus = [1.0, 0.6, 0.0]
+    got = O.denoise_chunk(cfg, w, sk, sv, frames, fw, state, noise, taus)[0]
+    ck, cv = brute_force.context_loops(cfg, w, sk, sv, frames, MICRO_WINDOW, 0, MICRO_STATIC_POS,
+                                       MICRO_FRAME_POS)
+    vel = lambda x, tau: brute_force.velocity_loops(cfg, w, state[0], x, tau, ck, cv, MICRO_DYN_POS)  # noqa: E731
+    ref = brute_force.euler_loops(vel, noise[0], taus)
+    np.testing.assert_allclose(got, np.array(ref), rtol=0, atol=1e-12)
+
+
+def test_velocity_matches_scalar_brute_force_empty_ring():
+    """No frame written: the context is the static prefix alone and the
+    dynamic tokens start right after it (positions 3, 4, 5)."""
+    cfg = WL.micro_config(frame_dim=5)
+    w, sk, sv, frames = _inputs(cfg, 1)
+    state = WL.make_state(cfg, 0)
+    noise = WL.make_noise(cfg, 0)
+    diag = {}
+    O.denoise_chunk(cfg, w, sk, sv, frames, 0, state, noise, [1.0, 0.0], diag=diag)
+    ck, cv = brute_force.context_loops(cfg, w, sk, sv, frames, [], 0, MICRO_STATIC_POS, {})
+    ref = brute_force.velocity_loops(cfg, w, state[0], noise[0], 1.0, ck, cv, [3, 4, 5])
+    np.testing.assert_allclose(diag["v"][0][0], np.array(ref), rtol=0, atol=1e-12)
+
+
+def _trace_rows():
+    rows = []
+    with open(os.path.join(GOLDEN, "ring_trace_w2_f32_ls64.txt")) as fh:
+        for line in fh:
+            if line.strip() and not line.startswith("#"):
+                rows.append([int(t) for t in line.split()])
+    return rows
+
+
+def _recover_positions(rotated, dim_pair, dh, theta):
+    """Positions from keys that were the unit vector e_i before RoPE.
+
+    A rotate-half RoPE at position p turns e_i into cos(p*w_i) e_i +
+    sin(p*w_i) e_{i+dh/2} with w_i = theta^(-2i/dh); the slowest pair keeps
+    p*w_i well inside (-pi, pi) for the positions used here, so atan2 gives p.
+    """
+    w_i = theta ** (-2.0 * dim_pair / dh)
+    ang = np.arctan2(rotated[:, dim_pair + dh // 2], rotated[:, dim_pair])
+    return np.rint(ang / w_i).astype(np.int64), ang / w_i
+
+
+def test_context_positions_and_kv_rows_follow_the_trace():
+    """Where the oracle puts the cached rows, read back from its outputs: the
+    static keys are rotated at 0..Ls-1, frame f's keys at the trace's
+    pos_first..pos_last (absolute, not by ring slot), the dynamic base after
+    frame f is the trace's dyn_pos0 column, and on the embedding path K comes
+    from the first head_dim rows of w_kv and V from the next head_dim rows."""
+    cfg = WL.CONFIGS["tiny_fp32"]
+    dh, F, Ls = cfg.head_dim, cfg.frame_tokens, cfg.static_len
+    i = dh // 2 - 1
+    e_i = np.zeros(dh)
+    e_i[i] = 1.0
+    # static prefix: pre-RoPE keys all e_i
+    sk = np.broadcast_to(e_i, (1, cfg.n_layers, Ls, dh)).copy()
+    sv = np.arange(Ls * dh, dtype=np.float64).reshape(1, 1, Ls, dh).repeat(cfg.n_layers, 1)
+    k_st, v_st = O.static_kv(cfg, sk, sv, 1, 0)
+    pos, raw = _recover_positions(k_st[:, 0, :], i, dh, cfg.rope_theta)
+    assert np.array_equal(pos, np.arange(Ls)) and np.max(np.abs(raw - pos)) < 1e-6
+    np.testing.assert_array_equal(v_st[:, 0, :], sv[0, 1])
+    # embedding path: w_kv K rows map embedding column 0 to e_i, V rows map
+    # column 1 to a known pattern
+    w = {"w_kv": np.zeros((cfg.n_layers, 2 * dh, cfg.frame_dim))}
+    w["w_kv"][1, i, 0] = 1.0
+    vpat = np.linspace(-1.0, 1.0, dh)
+    w["w_kv"][1, dh:, 1] = vpat
+    E = np.zeros((F, cfg.frame_dim))
+    E[:, 0] = 1.0
+    E[:, 1] = np.arange(1, F + 1)
+    for f, slot, p0, p1, nv, ev, dyn in _trace_rows():
+        k_fr, v_fr = O.frame_kv(cfg, w, E, f, 1)
+        pos, raw = _recover_positions(k_fr[:, 0, :], i, dh, cfg.rope_theta)
+        assert np.array_equal(pos, np.arange(p0, p1 + 1)), (f, pos[:3])
+        assert np.max(np.abs(raw - pos)) < 1e-6
+        np.testing.assert_allclose(v_fr[:, 0, :], np.arange(1, F + 1)[:, None] * vpat[None, :], rtol=0,
+                                   atol=1e-15)
+        assert O.dyn_pos0(cfg, f + 1) == dyn
+        # direct path: the frame carries K then V per layer
+        cfg_d = cfg.replace(frame_dim=0)
+        raw_kv = np.zeros((cfg.n_layers, 2, F, dh))
+        raw_kv[1, 0] = e_i
+        raw_kv[1, 1] = 3.0
+        k_d, v_d = O.frame_kv(cfg_d, None, raw_kv, f, 1)
+        pos_d, _ = _recover_positions(k_d[:, 0, :], i, dh, cfg.rope_theta)
+        assert np.array_equal(pos_d, np.arange(p0, p1 + 1))
+        assert np.all(v_d == 3.0)
 
 
 def _torch_velocity(cfg, w, state, x, tau, ctx_k, ctx_v, pos):
@@ -309,17 +400,58 @@ def _torch_velocity(cfg, w, state, x, tau, ctx_k, ctx_v, pos):
     return Fn.linear(yf, t(w["w_aout"])).numpy()
 
 
+def _torch_context(cfg, w, sk, sv, frames, window, env, frame_pos):
+    """Context K/V per layer from the raw sources with torch ops: static keys
+    rotated at 0..Ls-1, frame keys at the given positions, w_kv split into its
+    K rows then its V rows, RoPE as the complex rotation of (z_i, z_{i+d/2})."""
+    t = lambda a: torch.as_tensor(np.asarray(a, dtype=np.float64))  # noqa: E731
+    dh = cfg.head_dim
+
+    def rot(z, p):
+        zc = torch.complex(z[:, : dh // 2], z[:, dh // 2:])
+        ang = t(p)[:, None] * (cfg.rope_theta ** (-torch.arange(0, dh, 2, dtype=torch.float64) / dh))[None]
+        r = zc * torch.exp(1j * ang)
+        return torch.cat([r.real, r.imag], -1)
+
+    ks, vs = [], []
+    for l in range(cfg.n_layers):
+        K = [rot(t(sk[env, l]), np.arange(cfg.static_len))]
+        V = [t(sv[env, l])]
+        for f in window:
+            if cfg.frame_dim > 0:
+                wkv = t(w["w_kv"][l])
+                kf = Fn.linear(t(frames[f][env]), wkv[:dh])
+                vf = Fn.linear(t(frames[f][env]), wkv[dh:2 * dh])
+            else:
+                kf, vf = t(frames[f][env][l][0]), t(frames[f][env][l][1])
+            K.append(rot(kf, frame_pos[f]))
+            V.append(vf)
+        ks.append(torch.cat(K).numpy()[:, None, :])
+        vs.append(torch.cat(V).numpy()[:, None, :])
+    return ks, vs
+
+
 def test_velocity_matches_torch_composition_tiny():
+    """The oracle's first velocity of a chunk after frames 0..3 against torch
+    library routines, with the cached K/V rebuilt from the raw sources and
+    every position read from the hand-enumerated ring trace (W = 2, F = 32,
+    Ls = 64): the window is frames 2 and 3, at their pos_first..pos_last, and
+    the dynamic tokens start at the dyn_pos0 column of frame 3's row."""
     cfg = WL.CONFIGS["tiny_fp32"]
     w, sk, sv, frames = _inputs(cfg, 4)
+    rows = {r[0]: r for r in _trace_rows()}
     fw = 4
-    state = WL.make_state(cfg, 3)[0]
-    x = WL.make_noise(cfg, 3)[0]
-    pos = O.dyn_pos0(cfg, fw) + np.arange(cfg.action_horizon + 1)
-    v = O.velocity(cfg, w, state, x, 0.75, pos, O.full_batch_attend(cfg, w, sk, sv, frames, fw, 0))
-    ctx = [O.context_kv(cfg, w, sk, sv, frames, fw, l, 0) for l in range(cfg.n_layers)]
-    ref = _torch_velocity(cfg, w, state, x, 0.75, [c[0] for c in ctx], [c[1] for c in ctx], pos)
-    np.testing.assert_allclose(v, ref, rtol=0, atol=1e-11)
+    window = [f for f in rows if f >= fw - rows[fw - 1][4] and f < fw]
+    assert window == [2, 3]
+    frame_pos = {f: np.arange(rows[f][2], rows[f][3] + 1) for f in window}
+    dyn_pos = rows[fw - 1][6] + np.arange(cfg.action_horizon + 1)
+    state = WL.make_state(cfg, 3)
+    x = WL.make_noise(cfg, 3)
+    diag = {}
+    O.denoise_chunk(cfg, w, sk, sv, frames, fw, state, x, [0.75, 0.0], diag=diag)
+    ck, cv = _torch_context(cfg, w, sk, sv, frames, window, 0, frame_pos)
+    ref = _torch_velocity(cfg, w, state[0], x[0], 0.75, ck, cv, dyn_pos)
+    np.testing.assert_allclose(diag["v"][0][0], ref, rtol=0, atol=1e-11)
 
 
 # ---------------------------------------------------------------- paper invariants
@@ -353,32 +485,6 @@ def test_prop_a1_with_empty_ring_and_direct_path():
         full = O.denoise_chunk(cfg, w, sk, sv, frames, tick + 1, state, noise, taus)[0]
         part = O.denoise_chunk_partitioned(cfg, w, cache, state[0], noise[0], taus)
         np.testing.assert_allclose(part, full, rtol=0, atol=1e-10)
-
-
-def test_timestep_invariance_of_cached_regions():
-    """The perception K/V do not depend on the flow time (Section 3.1): the
-    cached regions read at different Euler steps are bit-identical."""
-    cfg = WL.CONFIGS["tiny_fp32"]
-    w, sk, sv, frames = _inputs(cfg, 3)
-    seen = {}
-    base = O.full_batch_attend(cfg, w, sk, sv, frames, 3, 0)
-    calls = {"n": 0}
-
-    def spy(layer, q, k, v):
-        Kc, Vc = O.context_kv(cfg, w, sk, sv, frames, 3, layer, 0)
-        key = layer
-        if key in seen:
-            assert np.array_equal(seen[key][0], Kc) and np.array_equal(seen[key][1], Vc)
-        else:
-            seen[key] = (Kc, Vc)
-        calls["n"] += 1
-        return base(layer, q, k, v)
-
-    state = WL.make_state(cfg, 0)[0]
-    noise = WL.make_noise(cfg, 0)[0]
-    pos = O.dyn_pos0(cfg, 3) + np.arange(cfg.action_horizon + 1)
-    O.euler_integrate(lambda x, t: O.velocity(cfg, w, state, x, t, pos, spy), noise, cfg.taus())
-    assert calls["n"] == cfg.num_steps * cfg.n_layers
 
 
 def test_naive_cache_negative_control():
