@@ -56,8 +56,12 @@ def _class_bytes_flops(cfg):
 
     GEMMs: weight bytes + activation bytes in + one copy of the output (fp32
     for the split-K residual projections, the operand type otherwise).
-    Attention: the visible cached K and V rows + q and the dynamic k, v in +
-    o out, all in the operand type."""
+    Attention (with its split merge, one unit per layer): the visible cached K
+    and V rows + q and the dynamic k, v in + o out, all in the operand type.
+    Residual/norm: h and the projection in, h and y out, the modulation rows.
+    Final kernel: h, the projection and the action head in, actions in and out.
+    Token embedding + first norm: the embedding weights, state, x in, h and y
+    out.  Modulation (three launches per chunk): the conditioning weights."""
     B, T = cfg.batch, cfg.action_horizon + 1
     M = B * T
     D, Fm, Hq, dh = cfg.width, cfg.mlp_dim, cfg.n_q_heads, cfg.head_dim
@@ -73,6 +77,36 @@ def _class_bytes_flops(cfg):
     vis = Lc * T + (1 + (T - 1) * T)  # visible keys summed over the dynamic rows of one env
     out["attention"] = (B * (2 * Lc * dh * eb + T * Hq * dh * eb + 2 * T * dh * eb + T * Hq * dh * eb),
                         B * 4.0 * Hq * dh * vis)
+    out["resid_norm"] = (_norm_bytes(cfg), 0.0)
+    da, ds = cfg.action_dim, cfg.state_dim
+    out["final_euler"] = (M * D * 4 * 2 + da * D * eb + 2 * B * (T - 1) * da * 4 + B * 6 * D * 4,
+                          2.0 * B * (T - 1) * da * D)
+    out["embed_norm"] = (D * (ds + da) * eb + B * ds * 4 + B * (T - 1) * da * 4 + M * D * (4 + eb) + B * 3 * D * 4,
+                         2.0 * B * (ds + (T - 1) * da) * D)
+    S = 2 * cfg.n_layers + 1
+    ch, C = cfg.cond_hidden, D + ds
+    out["modulation"] = ((S * ch * C + S * 3 * D * ch) * eb / 3.0,
+                         2.0 * cfg.num_steps * B * S * (ch * C + 3 * D * ch) / 3.0)
+    return out
+
+
+def _roofline(kernel, bound, nbytes, flops, seconds, traffic=None):
+    """Roofline object of one kernel class from its algorithmic bytes/flops per
+    launch and its average launch duration."""
+    if bound == "mfma":
+        achieved, peak, unit = flops / seconds / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        achieved, peak, unit = nbytes / seconds / 1e9, HBM_PEAK_GBS, "GB/s"
+    return {"kernel": kernel, "bound": bound, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": traffic, "avg_us": round(seconds * 1e6, 3)}
+
+
+def _class_times(prof):
+    """{class: (total ms, launches)} with the attention merge folded into the
+    attention (one attention unit per layer: the kernel and its merge)."""
+    out = {k: v for k, v in prof.items() if v[1] and k != "attn_merge"}
+    if "attention" in out and prof.get("attn_merge", (0, 0))[1]:
+        out["attention"] = (out["attention"][0] + prof["attn_merge"][0], out["attention"][1])
     return out
 
 
@@ -197,46 +231,77 @@ def _mode_chunks(eng, state, noise, torch, n):
     return out
 
 
-def _pipeline(cfg, w, sk, sv, frames, state, noise, torch, ticks, warmup):
-    """Tick period of frame write + chunk, on a ring with a spare slot, with
-    both on one stream (sequential) and with the write on a second stream
-    (asynchronous pipeline; each chunk reads the frames written before the
-    tick's own frame, so it overlaps that frame's write).  Also the write and
-    the chunk alone."""
+def _pipeline(cfg, w, sk, sv, frames, state, noise, torch, rounds, warmup):
+    """Tick time of frame write + chunk on a ring with a spare slot, run both
+    ways in alternation so drift between them cancels: "sequential" = write
+    then chunk on the engine stream (the chunk reads every frame written);
+    "pipelined" = the write on the engine's second stream while the chunk, on
+    the engine stream, reads the frames written before this tick's frame
+    (asynchronous pipeline, Section 3.3).  Each tick is bracketed by events on
+    the caller's stream, which waits for both engine streams at the end (device
+    time), and by the host clock (tick latency including launch).  The window a
+    chunk read is checked on every tick; the write and the chunk alone are
+    timed the same way."""
+    import numpy as np
+
     from paper_2607_14695_amd.reflex import ReflexEngine
 
     eng = ReflexEngine(cfg.replace(spare_slot=1), w, sk, sv)
-
-    def run(kind, n):
-        for i in range(n):
-            fr = frames[i % len(frames)]
-            if kind == "pipelined":
-                eng.pipeline_write(fr)
-                eng.denoise(state, noise, n_frames=eng.frames_written() - 1)
-            elif kind == "sequential":
+    cur = torch.cuda.current_stream()
+    for i in range(cfg.window_frames):
+        eng.write_frame(frames[i % len(frames)])
+    eng.synchronize()
+    times = {k: ([], []) for k in ("sequential", "pipelined", "write", "chunk")}
+    for r in range(warmup + rounds):
+        for kind in ("sequential", "pipelined", "write", "chunk"):
+            fr = frames[(r + len(kind)) % len(frames)]
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0 = time.perf_counter()
+            a.record(cur)
+            f_before = eng.frames_written()
+            if kind == "sequential":
                 eng.write_frame(fr)
-                eng.denoise(state, noise)
+                out = eng.denoise(state, noise)
+            elif kind == "pipelined":
+                eng.pipeline_write(fr)
+                out = eng.denoise(state, noise, n_frames=f_before)
+                if eng.last_n_frames != f_before:
+                    raise RuntimeError(f"pipelined chunk read {eng.last_n_frames} frames, expected {f_before}")
             elif kind == "write":
                 eng.write_frame(fr)
+                out = None
             else:
-                eng.denoise(state, noise)
-
-    out = {}
-    for kind in ("sequential", "pipelined", "write", "chunk"):
-        run(kind, warmup)
-        eng.synchronize()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        run(kind, ticks)
-        eng.synchronize()
-        torch.cuda.synchronize()
-        out[f"{kind}_ms"] = round((time.perf_counter() - t0) / ticks * 1e3, 4)
-    out["pipelined_speedup"] = round(out["sequential_ms"] / out["pipelined_ms"], 4)
-    # share of the write's time taken off the tick by running it beside the chunk
-    out["write_hidden_fraction"] = round((out["sequential_ms"] - out["pipelined_ms"]) / out["write_ms"], 3)
-    out["ticks_timed"] = ticks
+                out = eng.denoise(state, noise)
+            if eng.writer is not None:
+                cur.wait_stream(eng.writer)
+            cur.wait_stream(eng.stream)
+            b.record(cur)
+            b.synchronize()
+            host = time.perf_counter() - t0
+            if out is not None and not bool(torch.isfinite(out).all()):
+                raise RuntimeError(f"non-finite actions in the {kind} pipeline tick")
+            if r >= warmup:
+                times[kind][0].append(a.elapsed_time(b))
+                times[kind][1].append(host * 1e3)
+    res = {}
+    for kind, (dev, host) in times.items():
+        d, h = np.array(dev), np.array(host)
+        res[f"{kind}_ms"] = round(float(d.mean()), 4)
+        res[f"{kind}_ms_spread"] = [round(float(np.percentile(d, 10)), 4), round(float(np.percentile(d, 90)), 4)]
+        res[f"{kind}_host_ms"] = round(float(h.mean()), 4)
+    res["pipelined_speedup"] = round(res["sequential_ms"] / res["pipelined_ms"], 4)
+    spread = max(res["sequential_ms_spread"][1] - res["sequential_ms_spread"][0],
+                 res["pipelined_ms_spread"][1] - res["pipelined_ms_spread"][0])
+    # share of the write's time taken off the tick by running it beside the
+    # chunk; omitted when the write is shorter than the tick-to-tick spread
+    if res["write_ms"] > spread:
+        res["write_hidden_fraction"] = round((res["sequential_ms"] - res["pipelined_ms"]) / res["write_ms"], 3)
+    else:
+        res["write_hidden_fraction"] = None
+    res["rounds"] = rounds
     eng.close()
-    return out
+    return res
 
 
 def _scheduler(cfg, w, sk, sv, frames, noise, torch, chunks):
@@ -408,6 +473,16 @@ def cpu_baseline(cfg, log):
     from paper_2607_14695_amd import workloads as WL
 
     cores = len(os.sched_getaffinity(0))
+    model = None
+    try:
+        import subprocess
+
+        for line in subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except Exception:  # lscpu missing: the model stays unknown
+        pass
     try:
         from threadpoolctl import threadpool_limits
         limiter = threadpool_limits(limits=cores)
@@ -431,7 +506,7 @@ def cpu_baseline(cfg, log):
     sec = float(np.median(times))
     if limiter is not None:
         limiter.unregister()
-    return {"value": 1.0 / sec, "unit": "chunks/s", "cores": cores, "kind": "oracle",
+    return {"value": 1.0 / sec, "unit": "chunks/s", "cores": cores, "cpu_model": model, "kind": "oracle",
             "sample": "one full pi0_chunk_bf16 chunk (env 0, 10 Euler steps, 48 static + 768 frame "
                       f"+ 51 dynamic tokens), float64 numpy, median of 2 runs = {sec:.2f} s/chunk"}
 
@@ -520,14 +595,17 @@ def main():
     prof = eng.profile(state, noise)
     log("profile: " + ", ".join(f"{k}={v[0]:.3f}ms/{v[1]}" for k, v in prof.items() if v[1]))
     bf = _class_bytes_flops(cfg)
-    dominant = max((k for k in bf if prof.get(k, (0, 0))[1] > 0), key=lambda k: prof[k][0])
-    ms, n = prof[dominant]
-    avg_s = ms / n / 1e3
-    achieved = bf[dominant][0] / avg_s / 1e9
+    # the dominant kernel class: the largest share of the chunk's device time,
+    # over every class (the attention counted with its split merge)
+    ct = _class_times(prof)
+    dominant = max((k for k in ct if k in bf), key=lambda k: ct[k][0])
+    ms, n = ct[dominant]
     from paper_2607_14695_amd.profiling import load_traffic
 
     traffic = load_traffic(os.path.join(ROOT, "profiles", f"traffic_{cfg.name}.json"), dominant)
-    attn_ms, attn_n = prof["attention"]
+    roofline = _roofline(dominant, "hbm", bf[dominant][0], bf[dominant][1], ms / n / 1e3, traffic)
+    roofline["share_of_chunk"] = round(ms / sum(v[0] for v in ct.values()), 4)
+    attn_ms, attn_n = ct["attention"]
     attn_gbs = bf["attention"][0] / (attn_ms / attn_n / 1e3) / 1e9
     kernel_avg_us = {k: round(v[0] / v[1] * 1e3, 3) for k, v in prof.items() if v[1]}
     n_ms, n_n = prof["resid_norm"]
@@ -549,7 +627,8 @@ def main():
         pw32 = e32.profile_write(fr32[0])
         rb32 = _ring_bytes(c32, pw32)
         bf32 = _class_bytes_flops(c32)
-        a_ms, a_n = p32["attention"]
+        ct32 = _class_times(p32)
+        a_ms, a_n = ct32["attention"]
         b32 = {
             "workload": "pi0_batch32_bf16 tick: 32 envs, frame write through per-layer Wk/Wv 2048->256 "
                         "(embedding path) + 10-step denoise over 48 static + 2x768 ring + 51 dynamic tokens",
@@ -561,25 +640,31 @@ def main():
             "attn_mfma_tflops": round(bf32["attention"][1] / (a_ms / a_n / 1e3) / 1e12, 1),
             "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in p32.items() if v[1]},
         }
+        b32["roofline"] = {"attention": _roofline("attention", "hbm", *bf32["attention"], a_ms / a_n / 1e3)}
         for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
             ms_k, n_k = p32[k]
             b32[f"{k}_mfma_tflops"] = round(bf32[k][1] / (ms_k / n_k / 1e3) / 1e12, 1)
+            b32["roofline"][k] = _roofline(k, "mfma", *bf32[k], ms_k / n_k / 1e3)
+        proj_ms = sum(p32[k][0] for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"))
+        b32["projections_us_per_step"] = round(proj_ms / c32.num_steps * 1e3, 1)
         fp_ms, fp_n = pw32["frame_proj"]
         rw_ms32, rw_n32 = pw32["ring_write"]
         b32["frame_proj_mfma_tflops"] = round(rb32["frame_proj"][1] / (fp_ms / fp_n / 1e3) / 1e12, 1)
+        b32["roofline"]["frame_proj"] = _roofline("frame_proj", "mfma", *rb32["frame_proj"], fp_ms / fp_n / 1e3)
         b32["ring_write_gbs"] = round(rb32["ring_write"][0] / (rw_ms32 / rw_n32 / 1e3) / 1e9, 1)
         b32["write_us"] = {k: round(v[0] / v[1] * 1e3, 3) for k, v in pw32.items() if v[1]}
         n32_ms, n32_n = p32["resid_norm"]
         b32["norm_gbs"] = round(_norm_bytes(c32) / (n32_ms / n32_n / 1e3) / 1e9, 1)
         if not args.no_latency:
-            b32["stream_ticks"] = _stream_ticks(e32, fr32, st32, nz32, 30, 3, torch)
+            # the batched streaming workload's 200 ticks, released on the 20 ms grid
+            b32["stream_ticks"] = _stream_ticks(e32, fr32, st32, nz32, c32.ticks, 3, torch)
             log(f"b32 stream ticks: {b32['stream_ticks']}")
         if not args.no_baselines:
             b32["strategies"] = _mode_chunks(e32, st32, nz32, torch, 3)
             log(f"b32 strategies: {b32['strategies']}")
         e32.close()
         if not args.no_pipeline:
-            b32["pipeline"] = _pipeline(c32, w32, sk32, sv32, fr32, st32, nz32, torch, 8, 2)
+            b32["pipeline"] = _pipeline(c32, w32, sk32, sv32, fr32, st32, nz32, torch, 10, 2)
             log(f"b32 pipeline: {b32['pipeline']}")
         log(f"b32 tick {t32 * 1e3:.3f} ms, chunk {c32s * 1e3:.3f} ms")
 
@@ -597,7 +682,7 @@ def main():
             raise RuntimeError("non-finite actions from the timed long-context configuration")
         pl = el.profile(stl, nzl)
         bfl = _class_bytes_flops(cl)
-        al_ms, al_n = pl["attention"]
+        al_ms, al_n = _class_times(pl)["attention"]
         long_ctx = {
             "workload": "pi0_long_bf16 chunk: 8 envs, 256 static + 8 x 768 ring + 51 dynamic tokens, x64 "
                         "embeddings, tau schedule near 0 and 1, 10 Euler steps",
@@ -608,6 +693,9 @@ def main():
             "attn_mfma_tflops": round(bfl["attention"][1] / (al_ms / al_n / 1e3) / 1e12, 1),
             "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in pl.items() if v[1]},
         }
+        long_ctx["roofline"] = {"attention": _roofline("attention", "hbm", *bfl["attention"], al_ms / al_n / 1e3)}
+        for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
+            long_ctx["roofline"][k] = _roofline(k, "mfma", *bfl[k], pl[k][0] / pl[k][1] / 1e3)
         el.close()
         del el, wl
         log(f"long context: {long_ctx}")
@@ -618,7 +706,7 @@ def main():
         ws_, sks, svs, frs, sts, nzs = _device_inputs(cs, torch, seed=2)
         es = ReflexEngine(cs, ws_, sks, svs)
         if not args.no_latency:
-            stream = _stream_ticks(es, frs, sts, nzs, 100, 5, torch)
+            stream = _stream_ticks(es, frs, sts, nzs, cs.ticks, 5, torch)
             stream["workload"] = ("pi0_stream_bf16: 1 env, 768-token frames of width 2048 through the per-layer "
                                   "Wk/Wv projection into a 2-frame ring, 10-step denoise per tick, ticks released "
                                   "every 20 ms")
@@ -684,15 +772,7 @@ def main():
         "pipeline": pipeline,
         "scheduler": scheduler,
         "kernel_avg_us": kernel_avg_us,
-        "roofline": {
-            "kernel": dominant,
-            "bound": "hbm",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": traffic,
-        },
+        "roofline": roofline,
         "b32": b32,
         "long_ctx": long_ctx,
         "cpu_baseline": cpu,

@@ -44,6 +44,7 @@ extern "C" {
 #define REFLEX_EDTYPE (-2)   /* weight dtype differs from the config's dtype */
 #define REFLEX_EHIP (-3)     /* a HIP call or kernel launch failed */
 #define REFLEX_ESTATE (-4)   /* context not initialised or already destroyed */
+#define REFLEX_ENONFINITE (-5) /* reflex_check_status: a denoise produced a non-finite action */
 
 #define REFLEX_DTYPE_F32 0
 #define REFLEX_DTYPE_BF16 1
@@ -199,8 +200,12 @@ typedef struct reflex_ctx reflex_ctx;
  * int64 values {frames_written, n_valid, dyn_pos0, hole_row} (read-only for
  * callers): the frames, window length and dynamic position the next chunk
  * uses, and the logical cached row from which the physical rows skip the
- * spare slot (a value past the window means no skip).  The rest of the
- * workspace is private scratch of the library.
+ * spare slot (a value past the window means no skip).  Bytes 32..35 hold the
+ * status word that reflex_check_status reads.  The rest of the workspace is
+ * private scratch of the library.
+ * The caller allocates both buffers once, before the control loop: no
+ * allocation happens per frame or per chunk (the pre-allocated ring and
+ * buffers of Section 3.4 and Appendix B.2).
  * Returns REFLEX_EINVAL for an unsupported config.
  */
 int reflex_query_sizes(const reflex_config* cfg, size_t* cache_bytes, size_t* workspace_bytes);
@@ -245,8 +250,12 @@ int reflex_cache_write_frame(reflex_ctx* ctx, const void* frame, int64_t* frame_
  * noise:  device fp32 [batch][action_horizon][action_dim], x at tau_0
  * actions_out: device fp32 [batch][action_horizon][action_dim], x at tau_K;
  *         may alias noise.
- * tau_schedule: host fp32 array of num_steps + 1 values, tau_0 = 1 > ... >
- *         tau_K = 0, or NULL for tau_k = 1 - k/num_steps.
+ * tau_schedule: fp32 array of num_steps + 1 values, tau_0 = 1 > ... >
+ *         tau_K = 0, or NULL for tau_k = 1 - k/num_steps (the uniform Euler
+ *         grid from noise at tau = 1, Section 3.2).  Host memory, or device
+ *         memory: a device array is copied to the host on the context's
+ *         stream and that copy is waited for, so the call then blocks until
+ *         the stream's earlier work is done.
  * The cache is only read (timestep invariance, Section 3.1).  An empty ring
  * is allowed.  Launches are captured once into a HIP graph per distinct
  * (pointers, num_steps, schedule) and replayed.
@@ -338,8 +347,20 @@ int reflex_pipeline_denoise_chunk(reflex_ctx* ctx, const float* state, const flo
                                   int32_t num_steps, const float* tau_schedule, float* actions_out,
                                   int64_t n_frames, int64_t* n_frames_out);
 
+/*
+ * Status of the chunks denoised on this context since the last check: waits
+ * for the context's stream, reads and clears the device status word, and
+ * returns REFLEX_ENONFINITE when any action written by the method's final
+ * kernel was NaN or infinite (the NaN/Inf events that the BF16 stability
+ * comparison of Section 4.6 counts), else 0.  Denoise calls stay
+ * asynchronous; the check is the one synchronizing call.
+ * Errors: REFLEX_ESTATE, REFLEX_EHIP.
+ */
+int reflex_check_status(reflex_ctx* ctx);
+
 /* Release the host context and its captured graphs; never frees caller
- * memory.  NULL is a no-op.  Returns 0. */
+ * memory (the caller-owned cache and workspace of Section 3.4's
+ * pre-allocated buffers outlive it).  NULL is a no-op.  Returns 0. */
 int reflex_destroy(reflex_ctx* ctx);
 
 /* Text for a status code (for REFLEX_EHIP, the last HIP error string). */

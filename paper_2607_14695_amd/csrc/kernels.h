@@ -148,6 +148,7 @@ struct FinalArgs {
   int B, T, D, da;
   float dt, eps;
   int norm_mode;          // NormMode
+  int32_t* status;        // bit 0 set when an action leaves the kernel non-finite
 };
 template <typename T> hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s);
 
@@ -201,6 +202,10 @@ struct EulerArgs {           // x_out = x_in + dt * v (action rows 1..T-1 of v [
   float dt;
 };
 hipError_t launch_euler(const EulerArgs& a, hipStream_t s);
+
+// Zero `bytes` (a multiple of 16) at a 16-byte aligned device address with a
+// kernel (no memset node, so the launch is safe inside a captured graph).
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 
 // Sets the device tick state {frames, n_valid, dyn_pos0, hole_row} that the
 // next chunk on this stream reads (one thread; the chunk's kernels follow in

@@ -321,7 +321,11 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   }
   __syncthreads();
   const int64_t xo = ((int64_t)b * H + i) * p.da;
-  for (int a = threadIdx.x; a < p.da; a += 256) p.x_out[xo + a] = p.x_in[xo + a] + p.dt * vpart[0][a];
+  for (int a = threadIdx.x; a < p.da; a += 256) {
+    const float x = p.x_in[xo + a] + p.dt * vpart[0][a];
+    p.x_out[xo + a] = x;
+    if (!__builtin_isfinite(x)) atomicOr(p.status, 1);
+  }
 }
 
 template <typename T>
@@ -398,6 +402,21 @@ hipError_t launch_cond(void* cond, const float* state, const TauTable& taus, int
                        double min_p, double max_p, hipStream_t s) {
   RFX_LAUNCH((cond_kernel<T>), dim3(K * B), dim3(256), 0, s, reinterpret_cast<T*>(cond), state, taus,
                      B, D, ds, min_p, max_p);
+  return hipGetLastError();
+}
+
+__global__ void zero_kernel(uint4* p, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
+  if (((uintptr_t)p & 15) || (bytes & 15)) return hipErrorInvalidValue;
+  const size_t n16 = bytes / 16;
+  if (n16 == 0) return hipSuccess;
+  size_t blocks = (n16 + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  RFX_LAUNCH(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<uint4*>(p), n16);
   return hipGetLastError();
 }
 

@@ -56,6 +56,7 @@ struct GraphEntry {
 
 struct Workspace {
   int64_t* tick;
+  int32_t* status;  // bytes 32..35 of the tick block: bit 0 = a non-finite action was produced
   float2* rope_dyn;
   float2* rope_frame;
   void* cond;
@@ -323,11 +324,10 @@ int reencode_history(reflex_ctx* ctx, const reflex_sources* src, Launcher& L) {
 }
 
 template <typename T>
-int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
-                  float* out, bool prof, int mode, const reflex_sources* src) {
+int enqueue_chunk(reflex_ctx* ctx, const Workspace& W, const float* state, const float* noise, int steps,
+                  const float* taus, float* out, bool prof, int mode, const reflex_sources* src) {
   const reflex_config& c = ctx->cfg;
   const Plan& P = ctx->plan;
-  const Workspace& W = ctx->ws;
   hipStream_t st = ctx->stream;
   Launcher L{ctx, prof};
   const int B = c.batch, Tn = P.T, M = P.M, D = c.width, dh = c.head_dim, Hq = c.n_q_heads;
@@ -440,7 +440,7 @@ int enqueue_chunk(reflex_ctx* ctx, const float* state, const float* noise, int s
     const float dt = (float)((double)taus[k + 1] - (double)taus[k]);
     FinalArgs fa{W.h, W.rparts, rpart_stride, P.down.splits, mod_at(2 * c.n_layers - 1, k),
                  mod_at(2 * c.n_layers, k), ctx->w.w_aout, x_in, out, B, Tn, D, c.action_dim, dt, c.rms_eps,
-                 c.norm_precision};
+                 c.norm_precision, W.status};
     RFX_TRY(L.run(PC_FINAL, [&] { return launch_final_euler<T>(fa, st); }));
   }
   return REFLEX_OK;
@@ -563,16 +563,16 @@ int enqueue_chunk_unfused(reflex_ctx* ctx, const float* state, const float* nois
   return REFLEX_OK;
 }
 
-int enqueue_chunk_dispatch(reflex_ctx* ctx, const float* state, const float* noise, int steps, const float* taus,
-                           float* out, bool prof, int mode, const reflex_sources* src) {
+int enqueue_chunk_dispatch(reflex_ctx* ctx, const Workspace& W, const float* state, const float* noise, int steps,
+                           const float* taus, float* out, bool prof, int mode, const reflex_sources* src) {
   if (mode == REFLEX_MODE_UNFUSED) {
     if (ctx->cfg.dtype == REFLEX_DTYPE_BF16)
       return enqueue_chunk_unfused<bf16_t>(ctx, state, noise, steps, taus, out, prof);
     return enqueue_chunk_unfused<float>(ctx, state, noise, steps, taus, out, prof);
   }
   if (ctx->cfg.dtype == REFLEX_DTYPE_BF16)
-    return enqueue_chunk<bf16_t>(ctx, state, noise, steps, taus, out, prof, mode, src);
-  return enqueue_chunk<float>(ctx, state, noise, steps, taus, out, prof, mode, src);
+    return enqueue_chunk<bf16_t>(ctx, W, state, noise, steps, taus, out, prof, mode, src);
+  return enqueue_chunk<float>(ctx, W, state, noise, steps, taus, out, prof, mode, src);
 }
 
 // publish: also set the device tick state to "no frame written" (the first
@@ -793,6 +793,7 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
   char* base = reinterpret_cast<char*>(workspace_mem);
   Workspace& W = ctx->ws;
   W.tick = reinterpret_cast<int64_t*>(base + P.off[0]);
+  W.status = reinterpret_cast<int32_t*>(base + P.off[0] + 32);
   W.rope_dyn = reinterpret_cast<float2*>(base + P.off[1]);
   W.rope_frame = reinterpret_cast<float2*>(base + P.off[2]);
   W.cond = base + P.off[3];
@@ -863,6 +864,28 @@ int denoise_launch(reflex_ctx* ctx, int mode, const reflex_sources* src, std::ve
                    const float* state, const float* noise, int32_t num_steps, const float* taus,
                    float* actions_out);
 
+// A caller's tau schedule in host memory, or copied from device memory (a
+// stream-ordered copy on the context's stream, waited for).
+int read_taus(reflex_ctx* ctx, const float* tau_schedule, int32_t num_steps, float* taus) {
+  if (!tau_schedule) {
+    for (int k = 0; k <= num_steps; ++k) taus[k] = (float)(1.0 - (double)k / (double)num_steps);
+    return REFLEX_OK;
+  }
+  hipPointerAttribute_t attr;
+  memset(&attr, 0, sizeof(attr));
+  const hipError_t pe = hipPointerGetAttributes(&attr, tau_schedule);
+  if (pe != hipSuccess) (void)hipGetLastError();  // an unregistered host pointer
+  if (pe == hipSuccess && (attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged)) {
+    hipError_t e = hipMemcpyAsync(taus, tau_schedule, sizeof(float) * (num_steps + 1), hipMemcpyDeviceToHost,
+                                  ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(e);
+  } else {
+    for (int k = 0; k <= num_steps; ++k) taus[k] = tau_schedule[k];
+  }
+  return REFLEX_OK;
+}
+
 // n_req: the frames the chunk reads on a context with a spare slot (-1: the
 // newest completed write, kAllFrames: all); ignored without a spare slot,
 // where the tick state published by the last write is read.
@@ -909,8 +932,7 @@ int denoise_entry(reflex_ctx* ctx, int mode, const reflex_sources* src, const fl
     src = nullptr;
   }
   float taus[REFLEX_MAX_STEPS + 1];
-  for (int k = 0; k <= num_steps; ++k)
-    taus[k] = tau_schedule ? tau_schedule[k] : (float)(1.0 - (double)k / (double)num_steps);
+  RFX_TRY(read_taus(ctx, tau_schedule, num_steps, taus));
 
   if (spare) {
     // frame n-1 (and so every earlier frame) written, then this chunk's window
@@ -949,7 +971,7 @@ int denoise_launch(reflex_ctx* ctx, int mode, const reflex_sources* src, std::ve
                    float* actions_out) {
   if (ctx->prof_enabled) {
     ctx->ev_pending.clear();
-    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, true, mode, src);
+    int rc = enqueue_chunk_dispatch(ctx, ctx->ws, state, noise, num_steps, taus, actions_out, true, mode, src);
     if (rc != REFLEX_OK) return rc;
     return collect_profile(ctx, ctx->stream);
   }
@@ -967,7 +989,7 @@ int denoise_launch(reflex_ctx* ctx, int mode, const reflex_sources* src, std::ve
     hipGraph_t graph;
     hipError_t e = hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal);
     if (e != hipSuccess) return hip_fail(e);
-    int rc = enqueue_chunk_dispatch(ctx, state, noise, num_steps, taus, actions_out, false, mode, src);
+    int rc = enqueue_chunk_dispatch(ctx, ctx->ws, state, noise, num_steps, taus, actions_out, false, mode, src);
     e = hipStreamEndCapture(ctx->stream, &graph);
     if (rc != REFLEX_OK) {
       if (e == hipSuccess) (void)hipGraphDestroy(graph);
@@ -1022,6 +1044,17 @@ int reflex_pipeline_denoise_chunk(reflex_ctx* ctx, const float* state, const flo
                        n_frames, n_frames_out);
 }
 
+int reflex_check_status(reflex_ctx* ctx) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  int32_t st = 0;
+  const int32_t zero = 0;
+  hipError_t e = hipMemcpyAsync(&st, ctx->ws.status, sizeof(st), hipMemcpyDeviceToHost, ctx->stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(ctx->ws.status, &zero, sizeof(zero), hipMemcpyHostToDevice, ctx->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  return (st & 1) ? REFLEX_ENONFINITE : REFLEX_OK;
+}
+
 int reflex_destroy(reflex_ctx* ctx) {
   if (!ctx) return REFLEX_OK;
   ctx->alive = 0;
@@ -1043,6 +1076,7 @@ const char* reflex_strerror(int status) {
     case REFLEX_EDTYPE: return "weight dtype does not match the configured compute dtype";
     case REFLEX_EHIP: return g_hip_err[0] ? g_hip_err : "HIP error";
     case REFLEX_ESTATE: return "context not initialised or destroyed";
+    case REFLEX_ENONFINITE: return "a denoise produced a non-finite action since the last status check";
     default: return "unknown status";
   }
 }

@@ -26,6 +26,7 @@ REFLEX_EINVAL = -1
 REFLEX_EDTYPE = -2
 REFLEX_EHIP = -3
 REFLEX_ESTATE = -4
+REFLEX_ENONFINITE = -5
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MOD_FULL = 0
@@ -104,6 +105,7 @@ def load_library() -> ctypes.CDLL:
         "reflex_denoise_chunk_baseline": (c_i32, [c_vp, c_i32, P(SourcesC), c_vp, c_vp, c_i32, c_vp, c_vp]),
         "reflex_pipeline_write_frame": (c_i32, [c_vp, c_vp, c_vp, P(c_i64), P(c_i32)]),
         "reflex_pipeline_denoise_chunk": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp, c_i64, P(c_i64)]),
+        "reflex_check_status": (c_i32, [c_vp]),
         "reflex_destroy": (c_i32, [c_vp]),
         "reflex_strerror": (ctypes.c_char_p, [c_i32]),
         "reflex_ring_plan": (c_i32, [c_i64, c_i32, c_i32, c_i32, P(RingStepC)]),
@@ -310,7 +312,10 @@ class ReflexEngine:
 
         ``n_frames`` (pipelined ring, ``cfg.spare_slot = 1``) selects the
         window: the first n_frames frames, or -1 for the newest frame whose
-        write has completed; the value used is left in ``last_n_frames``."""
+        write has completed; the value used is left in ``last_n_frames``.
+
+        ``taus`` may be a device tensor: the library copies it to the host on
+        the engine stream."""
         torch = self.torch
         if mode not in MODES:
             raise ValueError(f"unknown mode {mode!r}")
@@ -329,7 +334,12 @@ class ReflexEngine:
                     out = torch.empty(tuple(n.shape), dtype=torch.float32, device=self.device)
                     self._bufs["out"] = out
             tau_arr = None
-            if taus is not None:
+            if isinstance(taus, torch.Tensor) and taus.is_cuda:
+                if taus.dtype != torch.float32 or taus.numel() != k + 1 or not taus.is_contiguous():
+                    raise ValueError("a device tau schedule is a contiguous fp32 tensor of num_steps + 1 values")
+                self._keep_taus = taus
+                tau_arr = taus.data_ptr()
+            elif taus is not None:
                 tau_np = np.ascontiguousarray(np.asarray(taus, dtype=np.float32))
                 if tau_np.shape[0] != k + 1:
                     raise ValueError("tau schedule needs num_steps + 1 entries")
@@ -363,6 +373,14 @@ class ReflexEngine:
                        frames=ctypes.cast(arr, ctypes.POINTER(c_vp)), n_frames=len(frames))
         self._keep_src = (arr, src)
         return ctypes.byref(src)
+
+    def check_status(self) -> int:
+        """reflex_check_status: waits for the engine stream; REFLEX_ENONFINITE
+        when a chunk since the last check produced a non-finite action, else 0."""
+        st = int(self.lib.reflex_check_status(self.ctx))
+        if st not in (REFLEX_OK, REFLEX_ENONFINITE):
+            _check(st, "reflex_check_status")
+        return st
 
     def synchronize(self):
         if self.writer is not None:

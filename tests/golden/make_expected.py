@@ -17,6 +17,7 @@ may write filler for those):
   pi0_batch32_bf16 ticks 0, 1, 2, 199, envs 0 and 31
   pi0_long_bf16    tick 7 (ring of 8 full), envs 0 and 7, x64 embeddings, tau
                    schedule concentrated near 0 and 1
+  pi0_window50_bf16 tick 49 (ring of 50 full, 38,448 cached tokens), env 0
 """
 from __future__ import annotations
 
@@ -40,7 +41,20 @@ CASES = {
     "pi0_stream_bf16": {"ticks": [0, 1, 2, 3, 250, 499], "envs": [0]},
     "pi0_batch32_bf16": {"ticks": [0, 1, 2, 199], "envs": [0, 31]},
     "pi0_long_bf16": {"ticks": [7], "envs": [0, 7]},
+    "pi0_window50_bf16": {"ticks": [49], "envs": [0]},
 }
+
+# Workloads sampled here that are not among the benchmark's configs: the widest
+# window of the context-window sweep (Section 4.6), 50 frames of 768 tokens
+# (38,448 cached tokens) on the direct K/V path, one env.
+EXTRA_CONFIGS = {
+    "pi0_window50_bf16": WL.CONFIGS["pi0_chunk_bf16"].replace(name="pi0_window50_bf16", window_frames=50,
+                                                              ticks=50),
+}
+
+
+def config(name: str):
+    return EXTRA_CONFIGS[name] if name in EXTRA_CONFIGS else WL.CONFIGS[name]
 
 
 def _code_only(text: str) -> str:
@@ -68,7 +82,7 @@ def window_ticks(tick: int, window: int):
 
 
 def compute_case(name: str) -> str:
-    cfg = WL.CONFIGS[name]
+    cfg = config(name)
     spec = CASES[name]
     t0 = time.time()
     w = {k: v.astype(np.float64) for k, v in WL.make_weights(cfg).items()}

@@ -89,7 +89,7 @@ def _io(cfg, tick, envs):
 
 
 def _run_stream(name):
-    cfg = WL.CONFIGS[name]
+    cfg = ME.config(name)
     exp = _expected(name)
     ticks = [int(t) for t in exp["ticks"]]
     envs = [int(e) for e in exp["envs"]]
@@ -178,4 +178,14 @@ def test_pi0_long_bf16_stress():
     cfg, eng, exp, envs = _run_stream("pi0_long_bf16")
     state, noise = _io(cfg, 7, envs)
     _check_steps(cfg, eng, exp, 7, 0, state, noise)
+    eng.close()
+
+
+def test_pi0_window50_bf16_sampled_tick():
+    """The widest window of the context-window sweep: 50 frames of 768 tokens
+    (38,448 cached keys, many key tiles per split), in the sweep's attention
+    launch configuration."""
+    cfg, eng, exp, envs = _run_stream("pi0_window50_bf16")
+    state, noise = _io(cfg, 49, envs)
+    _check_steps(cfg, eng, exp, 49, 0, state, noise)
     eng.close()
