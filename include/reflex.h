@@ -45,6 +45,8 @@ extern "C" {
 #define REFLEX_EHIP (-3)     /* a HIP call or kernel launch failed */
 #define REFLEX_ESTATE (-4)   /* context not initialised or already destroyed */
 #define REFLEX_ENONFINITE (-5) /* reflex_check_status: a denoise produced a non-finite action */
+#define REFLEX_ESCRATCH (-6) /* reflex_denoise_chunk_static: the chunk needs more scratch than
+                                the library's static device array holds */
 
 #define REFLEX_DTYPE_F32 0
 #define REFLEX_DTYPE_BF16 1
@@ -346,6 +348,30 @@ int reflex_pipeline_write_frame(reflex_ctx* ctx, const void* frame, void* writer
 int reflex_pipeline_denoise_chunk(reflex_ctx* ctx, const float* state, const float* noise,
                                   int32_t num_steps, const float* tau_schedule, float* actions_out,
                                   int64_t n_frames, int64_t* n_frames_out);
+
+/*
+ * reflex_denoise_chunk for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * chunk, with the same kernels and the same results, but the chunk's
+ * transient buffers (modulation, residual stream, activations, attention and
+ * split-K partials) live in one static device array of the library
+ * (64 MiB, allocated with the library's code on each device it runs on and
+ * held until the process ends) instead of the context's workspace, and the
+ * launches are enqueued directly on the context's stream (no graph is
+ * instantiated).  No hipMalloc, hipFree or allocating library routine is
+ * called.  Arguments, the tau schedule and the window as for
+ * reflex_denoise_chunk; only the method's strategy is offered.
+ * Every call on a device shares that device's array: calls that overlap on
+ * one device (two contexts on two streams, or a call while another's work is
+ * still in flight on another stream) race and give wrong results; calls in
+ * stream order, on any contexts, are safe.  The array keeps the last call's
+ * contents; the call clears what its kernels need zeroed.
+ * Errors: REFLEX_ESCRATCH when the chunk needs more than 64 MiB (16 MiB at
+ * batch 1 at the pi0 shapes with max_steps 10, so up to batch 4 fits; the
+ * transient bytes grow with batch and max_steps), and as reflex_denoise_chunk.
+ */
+int reflex_denoise_chunk_static(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                                const float* tau_schedule, float* actions_out);
 
 /*
  * Status of the chunks denoised on this context since the last check: waits

@@ -863,6 +863,8 @@ constexpr int64_t kAllFrames = INT64_MIN;  // every frame written so far
 int denoise_launch(reflex_ctx* ctx, int mode, const reflex_sources* src, std::vector<const void*> srcs,
                    const float* state, const float* noise, int32_t num_steps, const float* taus,
                    float* actions_out);
+int denoise_launch_static(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                          const float* taus, float* actions_out);
 
 // A caller's tau schedule in host memory, or copied from device memory (a
 // stream-ordered copy on the context's stream, waited for).
@@ -891,7 +893,7 @@ int read_taus(reflex_ctx* ctx, const float* tau_schedule, int32_t num_steps, flo
 // where the tick state published by the last write is read.
 int denoise_entry(reflex_ctx* ctx, int mode, const reflex_sources* src, const float* state, const float* noise,
                   int32_t num_steps, const float* tau_schedule, float* actions_out, int64_t n_req,
-                  int64_t* n_out) {
+                  int64_t* n_out, bool use_static = false) {
   if (!ctx || !ctx->alive) return REFLEX_ESTATE;
   if (!state || !noise || !actions_out) return REFLEX_EINVAL;
   if (num_steps < 1 || num_steps > ctx->cfg.max_steps) return REFLEX_EINVAL;
@@ -945,7 +947,8 @@ int denoise_entry(reflex_ctx* ctx, int mode, const reflex_sources* src, const fl
                         (int64_t)c.static_len + n * c.frame_tokens, hole_row(ctx, n), ctx->stream);
     if (e != hipSuccess) return hip_fail(e);
   }
-  const int rc = denoise_launch(ctx, mode, src, std::move(srcs), state, noise, num_steps, taus, actions_out);
+  const int rc = use_static ? denoise_launch_static(ctx, state, noise, num_steps, taus, actions_out)
+                            : denoise_launch(ctx, mode, src, std::move(srcs), state, noise, num_steps, taus, actions_out);
   if (rc != REFLEX_OK) return rc;
   if (spare) {
     hipError_t e;
@@ -1019,6 +1022,71 @@ int denoise_launch(reflex_ctx* ctx, int mode, const reflex_sources* src, std::ve
   return e == hipSuccess ? REFLEX_OK : hip_fail(e);
 }
 
+// ---------------------------------------------------------------------------
+// Allocation-free denoise: the chunk's transient buffers live in a static
+// device array instead of the context's workspace, and the launches run
+// eagerly (instantiating a graph allocates).  One array per device, shared by
+// every such call on that device.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+void* g_scratch_dev[kMaxDevices];  // device address of `scratch` per device (null until set up)
+std::mutex g_scratch_mu;
+
+// Device address of this device's copy of the array, looked up once per
+// device with that device current.
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (dev < 0 || dev >= kMaxDevices) return REFLEX_EINVAL;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e);
+    if (!ptr) return hip_fail(hipErrorInvalidSymbol);
+    g_scratch_dev[dev] = ptr;
+  }
+  *out = g_scratch_dev[dev];
+  return REFLEX_OK;
+}
+
+// Bytes of static scratch a chunk of this context needs: workspace parts 1..16
+// (the RoPE tables through the split-K partials), laid out as in the workspace.
+size_t static_scratch_bytes(const Plan& P) { return P.off[17] - P.off[1]; }
+
+int denoise_launch_static(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                          const float* taus, float* actions_out) {
+  const Plan& P = ctx->plan;
+  void* base = nullptr;
+  RFX_TRY(scratch_address(&base));
+  Workspace W = ctx->ws;  // tick state, status word and the frame path's tables stay in the workspace
+  char* b = reinterpret_cast<char*>(base) - P.off[1];
+  W.rope_dyn = reinterpret_cast<float2*>(b + P.off[1]);
+  W.cond = b + P.off[3];
+  W.hid = b + P.off[4];
+  W.mod = reinterpret_cast<float*>(b + P.off[5]);
+  W.h = reinterpret_cast<float*>(b + P.off[6]);
+  W.y = b + P.off[7];
+  W.q = b + P.off[8];
+  W.kd = b + P.off[9];
+  W.vdt = b + P.off[10];
+  W.counters = reinterpret_cast<int32_t*>(b + P.off[11]);
+  W.o = b + P.off[12];
+  W.part_o = reinterpret_cast<float*>(b + P.off[13]);
+  W.part_ml = reinterpret_cast<float*>(b + P.off[14]);
+  W.z = b + P.off[15];
+  W.rparts = reinterpret_cast<float*>(b + P.off[16]);
+  // the array keeps the previous call's bytes: the dynamic value columns
+  // beyond T must read as zero (the attention multiplies them by p = 0)
+  const hipError_t e = launch_zero(W.vdt, P.off[11] - P.off[10], ctx->stream);
+  if (e != hipSuccess) return hip_fail(e);
+  return enqueue_chunk_dispatch(ctx, W, state, noise, num_steps, taus, actions_out, false, REFLEX_MODE_REFLEX,
+                                nullptr);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1042,6 +1110,14 @@ int reflex_pipeline_denoise_chunk(reflex_ctx* ctx, const float* state, const flo
   if (!ctx->cfg.spare_slot || n_frames < -1) return REFLEX_EINVAL;
   return denoise_entry(ctx, REFLEX_MODE_REFLEX, nullptr, state, noise, num_steps, tau_schedule, actions_out,
                        n_frames, n_frames_out);
+}
+
+int reflex_denoise_chunk_static(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                                const float* tau_schedule, float* actions_out) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  if (static_scratch_bytes(ctx->plan) > kScratchBytes) return REFLEX_ESCRATCH;
+  return denoise_entry(ctx, REFLEX_MODE_REFLEX, nullptr, state, noise, num_steps, tau_schedule, actions_out,
+                       kAllFrames, nullptr, true);
 }
 
 int reflex_check_status(reflex_ctx* ctx) {
@@ -1077,6 +1153,7 @@ const char* reflex_strerror(int status) {
     case REFLEX_EHIP: return g_hip_err[0] ? g_hip_err : "HIP error";
     case REFLEX_ESTATE: return "context not initialised or destroyed";
     case REFLEX_ENONFINITE: return "a denoise produced a non-finite action since the last status check";
+    case REFLEX_ESCRATCH: return "the call needs more scratch than the library's static device array holds";
     default: return "unknown status";
   }
 }

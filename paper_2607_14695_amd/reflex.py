@@ -27,6 +27,7 @@ REFLEX_EDTYPE = -2
 REFLEX_EHIP = -3
 REFLEX_ESTATE = -4
 REFLEX_ENONFINITE = -5
+REFLEX_ESCRATCH = -6
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
 MOD_FULL = 0
@@ -105,6 +106,7 @@ def load_library() -> ctypes.CDLL:
         "reflex_denoise_chunk_baseline": (c_i32, [c_vp, c_i32, P(SourcesC), c_vp, c_vp, c_i32, c_vp, c_vp]),
         "reflex_pipeline_write_frame": (c_i32, [c_vp, c_vp, c_vp, P(c_i64), P(c_i32)]),
         "reflex_pipeline_denoise_chunk": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp, c_i64, P(c_i64)]),
+        "reflex_denoise_chunk_static": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp]),
         "reflex_check_status": (c_i32, [c_vp]),
         "reflex_destroy": (c_i32, [c_vp]),
         "reflex_strerror": (ctypes.c_char_p, [c_i32]),
@@ -298,7 +300,7 @@ class ReflexEngine:
         return buf
 
     def denoise(self, state, noise, num_steps: Optional[int] = None, taus: Optional[Sequence[float]] = None,
-                out=None, mode: str = "reflex", n_frames: Optional[int] = None):
+                out=None, mode: str = "reflex", n_frames: Optional[int] = None, static_scratch: bool = False):
         """Denoise one chunk per env; returns the fp32 action tensor (device).
 
         Without ``out`` the result lands in a buffer owned by the engine that
@@ -314,8 +316,10 @@ class ReflexEngine:
         window: the first n_frames frames, or -1 for the newest frame whose
         write has completed; the value used is left in ``last_n_frames``.
 
-        ``taus`` may be a device tensor: the library copies it to the host on
-        the engine stream."""
+        ``static_scratch`` runs the chunk through the allocation-free entry
+        point (the library's static device array holds the transient buffers,
+        no graph).  ``taus`` may be a device tensor: the library copies it to
+        the host on the engine stream."""
         torch = self.torch
         if mode not in MODES:
             raise ValueError(f"unknown mode {mode!r}")
@@ -345,7 +349,12 @@ class ReflexEngine:
                     raise ValueError("tau schedule needs num_steps + 1 entries")
                 self._keep_taus = tau_np
                 tau_arr = tau_np.ctypes.data
-            if n_frames is not None:
+            if static_scratch:
+                if mode != "reflex" or n_frames is not None:
+                    raise ValueError("the allocation-free entry point computes the method over all frames")
+                _check(self.lib.reflex_denoise_chunk_static(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr,
+                                                            out.data_ptr()), "reflex_denoise_chunk_static")
+            elif n_frames is not None:
                 used = c_i64(0)
                 _check(self.lib.reflex_pipeline_denoise_chunk(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr,
                                                               out.data_ptr(), n_frames, ctypes.byref(used)),
