@@ -122,16 +122,15 @@ def _norm_bytes(cfg):
 def _ring_bytes(cfg, prof_w):
     """(bytes, flops) of the ring writer's launches for one frame of all envs.
     Direct path: pre-RoPE K/V in, RoPE'd K and V^T out.  Embedding path: the
-    frame projection GEMM (frame + per-layer Wk/Wv in, fp32 K/V scratch out)
-    and the ring kernel (scratch in, cache out)."""
+    frame projection GEMM, whose epilogue writes RoPE'd K and V^T into the
+    cache (frame + per-layer Wk/Wv in, bf16 K/V out)."""
     eb = 2 if cfg.bf16 else 4
     kv = cfg.batch * cfg.n_layers * 2 * cfg.frame_tokens * cfg.head_dim  # K and V elements
     if cfg.frame_dim == 0:
         return {"ring_write": (2 * kv * eb, 0.0)}
     n = cfg.n_layers * 2 * cfg.head_dim
     m = cfg.batch * cfg.frame_tokens
-    return {"frame_proj": (m * cfg.frame_dim * eb + n * cfg.frame_dim * eb + m * n * 4, 2.0 * m * n * cfg.frame_dim),
-            "ring_write": (kv * 4 + kv * eb, 0.0)}
+    return {"frame_proj": (m * cfg.frame_dim * eb + n * cfg.frame_dim * eb + m * n * eb, 2.0 * m * n * cfg.frame_dim)}
 
 
 def _stream_ticks(eng, frames, state, noise, ticks, warmup, torch, period_s=0.020):
@@ -648,10 +647,8 @@ def main():
         proj_ms = sum(p32[k][0] for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"))
         b32["projections_us_per_step"] = round(proj_ms / c32.num_steps * 1e3, 1)
         fp_ms, fp_n = pw32["frame_proj"]
-        rw_ms32, rw_n32 = pw32["ring_write"]
         b32["frame_proj_mfma_tflops"] = round(rb32["frame_proj"][1] / (fp_ms / fp_n / 1e3) / 1e12, 1)
         b32["roofline"]["frame_proj"] = _roofline("frame_proj", "mfma", *rb32["frame_proj"], fp_ms / fp_n / 1e3)
-        b32["ring_write_gbs"] = round(rb32["ring_write"][0] / (rw_ms32 / rw_n32 / 1e3) / 1e9, 1)
         b32["write_us"] = {k: round(v[0] / v[1] * 1e3, 3) for k, v in pw32.items() if v[1]}
         n32_ms, n32_n = p32["resid_norm"]
         b32["norm_gbs"] = round(_norm_bytes(c32) / (n32_ms / n32_n / 1e3) / 1e9, 1)

@@ -37,7 +37,8 @@ enum Pair : int { PAIR_NONE = 0, PAIR_N = 1, PAIR_HEAD = 2 };
 
 template <int EPI>
 struct EpiPair {
-  static constexpr int value = EPI == EPI_GELU ? PAIR_N : (EPI == EPI_ROPE ? PAIR_HEAD : PAIR_NONE);
+  static constexpr int value =
+      EPI == EPI_GELU ? PAIR_N : ((EPI == EPI_ROPE || EPI == EPI_KV) ? PAIR_HEAD : PAIR_NONE);
 };
 
 // Store one output (plain epilogues) or one column pair (paired epilogues).
@@ -56,6 +57,23 @@ RFX_DEV void epilogue_store(const GemmArgs& p, int z, int split, int row, int co
   } else if constexpr (EPI == EPI_GELU) {
     T* o = reinterpret_cast<T*>(p.out) + (int64_t)z * p.o_bstride + (int64_t)row * p.ldo + col;
     *o = from_f<T>(gelu_tanh(v) * u);
+  } else if constexpr (EPI == EPI_KV) {
+    const KvOut& q = p.kv;
+    const int dh = p.qkv.head_dim, half = dh >> 1;
+    const int blk = col / dh, d = col - blk * dh;  // d < half
+    const int l = blk >> 1;
+    const int b = row / q.F, j = row - b * q.F;
+    const int64_t bl = (int64_t)b * q.L + l;
+    if ((blk & 1) == 0) {
+      const float2 cs = q.rope[j * half + d];
+      T* dst = reinterpret_cast<T*>(q.cache_k) + (bl * q.R + q.row0 + j) * dh;
+      dst[d] = from_f<T>(v * cs.x - u * cs.y);
+      dst[d + half] = from_f<T>(u * cs.x + v * cs.y);
+    } else {
+      T* dst = reinterpret_cast<T*>(q.cache_vt) + bl * dh * q.R + q.row0 + j;
+      dst[(int64_t)d * q.R] = from_f<T>(v);
+      dst[(int64_t)(d + half) * q.R] = from_f<T>(u);
+    }
   } else {  // EPI_ROPE
     const QkvOut& q = p.qkv;
     const int dh = q.head_dim, half = dh >> 1;
@@ -102,6 +120,36 @@ RFX_DEV void epilogue_store4(const GemmArgs& p, int z, int split, int row, int c
     T* o = reinterpret_cast<T*>(p.out) + (int64_t)z * p.o_bstride + (int64_t)row * p.ldo + col;
     *reinterpret_cast<uint2*>(o) = make_uint2((uint32_t)f2bf(w[0]) | ((uint32_t)f2bf(w[1]) << 16),
                                               (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16));
+  } else if constexpr (EPI == EPI_KV) {
+    const KvOut& q = p.kv;
+    const int dh = p.qkv.head_dim, half = dh >> 1;
+    const int blk = col / dh, d = col - blk * dh;  // d .. d+3 < half
+    const int l = blk >> 1;
+    const int b = row / q.F, j = row - b * q.F;
+    const int64_t bl = (int64_t)b * q.L + l;
+    if ((blk & 1) == 0) {
+      const float4 c01 = *reinterpret_cast<const float4*>(q.rope + j * half + d);      // (cos, sin) of d, d+1
+      const float4 c23 = *reinterpret_cast<const float4*>(q.rope + j * half + d + 2);  // of d+2, d+3
+      const float cs[4] = {c01.x, c01.z, c23.x, c23.z}, sn[4] = {c01.y, c01.w, c23.y, c23.w};
+      float lo[4], hi[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo[e] = v[e] * cs[e] - u[e] * sn[e];
+        hi[e] = u[e] * cs[e] + v[e] * sn[e];
+      }
+      T* dst = reinterpret_cast<T*>(q.cache_k) + (bl * q.R + q.row0 + j) * dh;
+      *reinterpret_cast<uint2*>(dst + d) = make_uint2((uint32_t)f2bf(lo[0]) | ((uint32_t)f2bf(lo[1]) << 16),
+                                                      (uint32_t)f2bf(lo[2]) | ((uint32_t)f2bf(lo[3]) << 16));
+      *reinterpret_cast<uint2*>(dst + d + half) = make_uint2((uint32_t)f2bf(hi[0]) | ((uint32_t)f2bf(hi[1]) << 16),
+                                                             (uint32_t)f2bf(hi[2]) | ((uint32_t)f2bf(hi[3]) << 16));
+    } else {
+      T* dst = reinterpret_cast<T*>(q.cache_vt) + bl * dh * q.R + q.row0 + j;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dst[(int64_t)(d + e) * q.R] = f2bf(v[e]);
+        dst[(int64_t)(d + e + half) * q.R] = f2bf(u[e]);
+      }
+    }
   } else {  // EPI_ROPE
     const QkvOut& q = p.qkv;
     const int dh = q.head_dim, half = dh >> 1;
@@ -1324,7 +1372,7 @@ template <typename T, int EPI>
 static void launch_pick(const GemmArgs& a, hipStream_t s) {
   bool skinny = a.M <= 64;
   // paired tiles of the tiled kernel hold 64 first-half columns of one head
-  if (EPI == EPI_ROPE && a.qkv.head_dim < 128) skinny = true;
+  if ((EPI == EPI_ROPE || EPI == EPI_KV) && a.qkv.head_dim < 128) skinny = true;
   if (skinny)
     launch_skinny<T, EPI>(a, s);
   else
@@ -1335,7 +1383,9 @@ template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.K <= 0) return hipErrorInvalidValue;
   if (epi == EPI_GELU && a.N % 64) return hipErrorInvalidValue;
-  if (epi == EPI_ROPE && (a.qkv.head_dim % 64 || a.N % a.qkv.head_dim)) return hipErrorInvalidValue;
+  if ((epi == EPI_ROPE || epi == EPI_KV) && (a.qkv.head_dim % 64 || a.N % a.qkv.head_dim))
+    return hipErrorInvalidValue;
+  if (epi == EPI_KV && (a.N % (2 * a.qkv.head_dim) || a.M % a.kv.F)) return hipErrorInvalidValue;
   if (epi != EPI_F32 && a.splits != 1) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_F32: launch_pick<T, EPI_F32>(a, s); break;
@@ -1343,6 +1393,7 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s) {
     case EPI_SILU: launch_pick<T, EPI_SILU>(a, s); break;
     case EPI_GELU: launch_pick<T, EPI_GELU>(a, s); break;
     case EPI_ROPE: launch_pick<T, EPI_ROPE>(a, s); break;
+    case EPI_KV: launch_pick<T, EPI_KV>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -29,6 +29,9 @@ enum Epi : int {
                  // columns are replaced by 0/1 (scale-only modulation)
   EPI_ROPE = 4,  // packed QKV, paired columns d and d + head_dim/2 of a head:
                  // RoPE on q and k heads, scattered to the attention layouts
+  EPI_KV = 5,    // frame K/V projection, paired columns d and d + head_dim/2 of
+                 // each layer's K or V block: RoPE on K, written straight into
+                 // the cache (K rows, V^T columns) of the frame's ring slot
 };
 
 // Destinations of the EPI_ROPE epilogue (row m = b*T + i of the GEMM).
@@ -38,6 +41,15 @@ struct QkvOut {
   void* k;             // [B][T][head_dim]                       (RoPE applied)
   void* vt;            // [B][head_dim][tpad], column i          (V transposed)
   int T, Hq, head_dim, rows_pad, tpad;
+};
+
+// Destinations of the EPI_KV epilogue (row m = b*F + j of the GEMM, column
+// n = (2l + kv)*head_dim + d): K rows and V^T columns of ring rows row0 + j.
+struct KvOut {
+  const float2* rope;  // [F][head_dim/2] (cos, sin) at the frame's positions
+  void* cache_k;       // [B][L][R][head_dim]
+  void* cache_vt;      // [B][L][head_dim][R]
+  int R, row0, F, L;
 };
 
 // C[M][N] = A[M][K] * B[N][K]^T (+ epilogue).
@@ -53,7 +65,8 @@ struct GemmArgs {
   int k_per_split;   // multiple of the k-step
   int mod_width;     // EPI_MOD: width D, 0 = full modulation
   int batch;         // blockIdx.z extent
-  QkvOut qkv;        // EPI_ROPE only
+  QkvOut qkv;        // EPI_ROPE; EPI_KV uses qkv.head_dim only
+  KvOut kv;          // EPI_KV only
 };
 
 template <typename T> hipError_t launch_gemm(const GemmArgs& a, int epi, hipStream_t s);

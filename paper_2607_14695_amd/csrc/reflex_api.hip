@@ -73,7 +73,6 @@ struct Workspace {
   float* part_ml;
   void* z;
   float* rparts;
-  float* frame_scratch;
   void* naive_k;   // [L][B][T][dh] dynamic K of the first Euler step (Naive mode)
   void* naive_vt;  // [L][B][dh][tpad] dynamic V^T of the first Euler step (Naive mode)
   float* uf_wide;  // [M][max(Nqkv, 2*mlp)] fp32 projection outputs (unfused schedule)
@@ -182,7 +181,7 @@ Plan make_plan(const reflex_config* c) {
   sz[14] = B * p.attn_splits * (size_t)p.rows_pad * 2 * sizeof(float);    // part_ml
   sz[15] = (size_t)p.M * c->mlp_dim * eb;                                 // z
   sz[16] = (size_t)p.max_parts * p.M * D * sizeof(float);                 // rparts
-  sz[17] = c->frame_dim > 0 ? B * c->frame_tokens * L * 2 * dh * sizeof(float) : 0;  // frame scratch
+  sz[17] = 0;  // (unused: the frame projection writes the cache from its epilogue)
   p.naive_k_stride = align256(sz[9]);
   p.naive_vt_stride = align256(sz[10]);
   sz[18] = L * p.naive_k_stride;                                          // naive_k
@@ -629,20 +628,21 @@ int write_frame(reflex_ctx* ctx, const void* frame, const reflex_ring_step& stp,
   a.dyn_pos0 = stp.dyn_pos0;
   a.hole_row = hole_row(ctx, stp.frame_index + 1);
   if (c.frame_dim > 0) {
+    // the frame K/V projection of every layer, RoPE on K and the transposed V
+    // written by its epilogue straight into the slot's cache rows
     const int N = c.n_layers * 2 * dh;
     GemmArgs g{};
     g.A = frame; g.lda = c.frame_dim;
     g.B = ctx->w.w_kv; g.ldb = c.frame_dim;
-    g.out = ctx->ws.frame_scratch; g.ldo = N;
     g.M = c.batch * c.frame_tokens; g.N = N; g.K = c.frame_dim;
     g.splits = 1; g.k_per_split = c.frame_dim + 128; g.batch = 1;
-    RFX_TRY(L.run(PC_FRAME_PROJ, [&] { return launch_gemm<T>(g, EPI_F32, st); }));
-    a.src_k = ctx->ws.frame_scratch;
-    a.src_v = ctx->ws.frame_scratch + dh;
-    a.sb = (int64_t)c.frame_tokens * N;
-    a.sl = 2 * dh;
-    a.sj = N;
-    RFX_TRY(L.run(PC_RING, [&] { return launch_ring_write<T, float>(a, dh, st); }));
+    g.qkv.head_dim = dh;
+    g.kv = KvOut{ctx->ws.rope_frame, ctx->cache_k, ctx->cache_vt, P.R, a.row0, c.frame_tokens, c.n_layers};
+    RFX_TRY(L.run(PC_FRAME_PROJ, [&] { return launch_gemm<T>(g, EPI_KV, st); }));
+    if (publish)
+      RFX_TRY(L.run(PC_RING, [&] {
+        return launch_tick_set(ctx->ws.tick, a.frames_written, a.n_valid, a.dyn_pos0, a.hole_row, st);
+      }));
   } else {
     a.src_k = frame;
     a.src_v = (const char*)frame + (size_t)c.frame_tokens * dh * sizeof(T);
@@ -689,7 +689,7 @@ int write_entry(reflex_ctx* ctx, const void* frame, hipStream_t st, int64_t* fra
   const bool spare = c.spare_slot != 0;
   if (spare) {
     hipError_t e = hipSuccess;
-    // the previous write shares the frame scratch and must finish first
+    // the previous write shares the frame RoPE table and must finish first
     if (!ctx->write_recs.empty() && ctx->write_recs.back().stream != st)
       e = hipStreamWaitEvent(st, ctx->write_recs.back().ev, 0);
     // slot f mod (W+1) holds frame f-W-1, which the windows of chunks over
@@ -810,7 +810,6 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
   W.part_ml = reinterpret_cast<float*>(base + P.off[14]);
   W.z = base + P.off[15];
   W.rparts = reinterpret_cast<float*>(base + P.off[16]);
-  W.frame_scratch = reinterpret_cast<float*>(base + P.off[17]);
   W.naive_k = base + P.off[18];
   W.naive_vt = base + P.off[19];
   W.uf_wide = reinterpret_cast<float*>(base + P.off[20]);
