@@ -463,6 +463,29 @@ def soak(torch, log, ticks):
     return out
 
 
+def profile_run(torch, log, name, ticks):
+    """A short run of one workload for the profiler: the ring filled, then
+    `ticks` ticks of frame write + chunk through the captured graphs (the
+    launch configuration of the timed benchmark), each tick synchronized."""
+    from paper_2607_14695_amd import workloads as WL
+    from paper_2607_14695_amd.reflex import ReflexEngine
+
+    cfg = WL.CONFIGS[name]
+    w, sk, sv, frames, state, noise = _device_inputs(cfg, torch)
+    eng = ReflexEngine(cfg, w, sk, sv)
+    for i in range(cfg.window_frames):
+        eng.write_frame(frames[i % len(frames)])
+    for i in range(ticks):
+        eng.write_frame(frames[i % len(frames)])
+        out = eng.denoise(state, noise)
+        eng.synchronize()
+        if not bool(torch.isfinite(out).all()):
+            raise RuntimeError(f"non-finite actions in the profiled {name} run")
+        log(f"profile run {name}: tick {i + 1}/{ticks}")
+    eng.close()
+    return {"metric": "profile_run", "workload": name, "ticks": ticks, "batch": cfg.batch}
+
+
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
     10 Euler steps, one frame in the window), median of two runs."""
@@ -533,6 +556,8 @@ def main():
                     help="instead of the benchmark line, print one JSON line of the norm-precision soak")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
+    ap.add_argument("--profile-workload", metavar="NAME",
+                    help="instead of the benchmark line, run a few ticks of one workload (for rocprofv3)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -571,6 +596,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         log("calibration copy: 3 x 256 MiB")
+
+    if args.profile_workload:
+        print(json.dumps(profile_run(torch, log, args.profile_workload, max(1, args.steps))), flush=True)
+        return
 
     cfg = WL.CONFIGS["pi0_chunk_bf16"]
     w, sk, sv, frames, state, noise = _device_inputs(cfg, torch)

@@ -868,18 +868,29 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
 constexpr int GBM = 256, GBN = 256;
 constexpr int GSTAGE = (GBM + GBN) * DROWB;  // 64 KB
 
+// Tiles of one XCD (a contiguous range of the tile sequence) in groups of up
+// to 8 M tiles by every N tile, M fastest within a group: the 32 tiles an XCD
+// runs at once then cover 8 M x 4 N tiles, whose A and B panels they read in
+// step, instead of 32 M tiles of one N panel, which re-read A for every tile
+// (the frame projection at 32 envs: 96 x 36 tiles with a 1 MB A panel each).
 template <int PAIR>
 RFX_DEV bool big_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
+  constexpr int GM = 8;
   const int nx = PAIR == PAIR_NONE ? (p.N + GBN - 1) / GBN : (PAIR == PAIR_N ? p.N / 128 : p.N / 256);
   const int ny = (p.M + GBM - 1) / GBM;
   const int total = nx * ny * p.batch * p.splits;
   const int per = (total + 7) / 8;
   const int t = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
   if (t >= total) return false;
-  by = t % ny;
-  const int rest = t / ny;
-  bx = rest % nx;
-  bz = rest / nx;
+  const int tz = nx * ny;
+  bz = t / tz;
+  const int tt = t - bz * tz;
+  const int grp = tt / (GM * nx);
+  const int m0 = grp * GM;
+  const int gm = min(GM, ny - m0);
+  const int r = tt - grp * GM * nx;
+  by = m0 + r % gm;
+  bx = r / gm;
   return true;
 }
 

@@ -52,6 +52,9 @@ KERNEL_SOURCES: Dict[str, Tuple[str, ...]] = {
     "resid_norm": ("norm_ring.hip", "common.h", "kernels.h"),
     "embed_norm": ("norm_ring.hip", "common.h", "kernels.h"),
     "final_euler": ("norm_ring.hip", "common.h", "kernels.h"),
+    "frame_proj": ("gemm.hip", "common.h", "kernels.h"),
+    "ring_write": ("norm_ring.hip", "common.h", "kernels.h"),
+    "modulation": ("gemm.hip", "norm_ring.hip", "common.h", "kernels.h"),
     "all": ("attention.hip", "gemm.hip", "norm_ring.hip", "reflex_api.hip", "common.h", "kernels.h"),
 }
 
@@ -239,10 +242,230 @@ def load_traffic(path: str, kernel_class: str) -> Optional[int]:
     except (OSError, ValueError):
         return None
     rec = doc.get("records", {}).get(kernel_class)
-    if rec is None or rec.get("digest") != source_digest(kernel_class):
+    if rec is None:
+        return None
+    cls = rec.get("digest_class", kernel_class)
+    if cls not in KERNEL_SOURCES or rec.get("digest") != source_digest(cls):
         return None
     return int(rec["hbm_bytes_per_launch"])
 
 
+
+
+
+# ---------------------------------------------------------------------------
+# per-workload summary: every kernel of one workload's run, by class
+# ---------------------------------------------------------------------------
+SIMDS = 1024          # 256 CUs x 4 SIMDs
+CLOCK_GHZ = 2.4       # MI355X peak engine clock
+MFMA_PEAK_TFLOPS = 2500.0
+
+_EPI_CLASS = {"4": "gemm_qkv", "2": "gemm_gate_up", "5": "frame_proj", "1": "modulation", "3": "modulation"}
+
+
+def _epi(name: str) -> Optional[str]:
+    """Epilogue template argument of a GEMM kernel name (its first argument,
+    or the third for the skinny kernels)."""
+    m = re.search(r"gemm_(\w+)<([^>]*)>", name)
+    if not m:
+        return None
+    args = [a.strip() for a in m.group(2).split(",")]
+    if m.group(1) in ("skinny_lds",):
+        return args[2] if len(args) > 2 else None
+    if m.group(1) in ("skinny", "tiled"):
+        return args[3] if m.group(1) == "skinny" and len(args) > 3 else (args[1] if len(args) > 1 else None)
+    return args[0]
+
+
+def classify(names: List[str]) -> List[str]:
+    """Kernel class of each dispatch of one run, in dispatch order.  The fp32
+    GEMM after the attention (or its merge) is the output projection, the one
+    after the gate|up GEMM the down projection."""
+    out, prev = [], ""
+    for n in names:
+        if "reflex::" not in n:
+            c = "other"
+        elif re.search(r"attn(16p|16|_pair)?_kernel", n):
+            c = "attention"
+        elif "attn_merge" in n:
+            c = "attn_merge"
+        elif "resid_norm" in n:
+            c = "resid_norm"
+        elif "final_euler" in n:
+            c = "final_euler"
+        elif "embed_norm" in n:
+            c = "embed_norm"
+        elif "ring_write" in n:
+            c = "ring_write"
+        elif "cond_kernel" in n:
+            c = "modulation"
+        elif "gemm_" in n:
+            e = _epi(n)
+            if e == "0":
+                c = "gemm_o" if prev in ("attention", "attn_merge") else ("gemm_down" if prev == "gemm_gate_up"
+                                                                          else "gemm_f32")
+            else:
+                c = _EPI_CLASS.get(e, "gemm")
+        else:
+            c = re.sub(r".*reflex::(\w+).*", r"\1", n)
+        out.append(c)
+        if c != "other":
+            prev = c
+    return out
+
+
+def _dispatches(path: str) -> List[dict]:
+    """Counter CSV -> one record per dispatch: name, grid, duration, counters."""
+    recs: Dict[str, dict] = {}
+    order: List[str] = []
+    for r in _rows(path):
+        k = r["Dispatch_Id"]
+        if k not in recs:
+            recs[k] = {"name": r["Kernel_Name"], "grid": int(r["Grid_Size"]),
+                       "dur_ns": float(r["End_Timestamp"]) - float(r["Start_Timestamp"]), "c": {}}
+            order.append(k)
+        c = recs[k]["c"]
+        c[r["Counter_Name"]] = c.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return [recs[k] for k in sorted(order, key=lambda x: int(x))]
+
+
+def _trace_dispatches(path: str) -> List[dict]:
+    out = []
+    for r in _rows(path):
+        if r.get("Kind", "KERNEL_DISPATCH") != "KERNEL_DISPATCH":
+            continue
+        out.append({"name": r["Kernel_Name"], "grid": int(r["Grid_Size_X"]) * int(r.get("Grid_Size_Y", 1) or 1)
+                    * int(r.get("Grid_Size_Z", 1) or 1),
+                    "dur_ns": float(r["End_Timestamp"]) - float(r["Start_Timestamp"]),
+                    "start": float(r["Start_Timestamp"])})
+    out.sort(key=lambda d: d["start"])
+    return out
+
+
+def _copy_value(disp: List[dict], counter: str) -> float:
+    vals = [d["c"][counter] for d in disp if COPY_PATTERN.search(d["name"]) and d["grid"] == COPY_GRID
+            and counter in d["c"]]
+    if not vals:
+        raise ValueError(f"no calibration copy dispatch with {counter}")
+    return sorted(vals)[len(vals) // 2]
+
+
+def summarize(workload: str, trace: str, fetch: str, write: str, mfma: str, commands: Dict[str, str],
+              out_md: str, out_json: Optional[str]) -> dict:
+    """Per (class, kernel, grid): dispatches, average duration (kernel trace),
+    calibrated HBM bytes per dispatch (FETCH_SIZE and WRITE_SIZE runs), MFMA
+    busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over duration x clock x SIMDs) and
+    MFMA TFLOP/s (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 flops)."""
+    tr = _trace_dispatches(trace)
+    tcls = classify([d["name"] for d in tr])
+    groups: Dict[Tuple[str, str, int], dict] = {}
+
+    def grp(c, d):
+        key = (c, _short(d["name"]), d["grid"])
+        return groups.setdefault(key, {"n": 0, "dur": 0.0, "fetch": [], "write": [], "busy": [], "mops": [],
+                                       "cdur": []})
+
+    for c, d in zip(tcls, tr):
+        if c == "other":
+            continue
+        g = grp(c, d)
+        g["n"] += 1
+        g["dur"] += d["dur_ns"]
+    fd, wd, md = _dispatches(fetch), _dispatches(write), _dispatches(mfma)
+    f_fac = COPY_BYTES / (_copy_value(fd, "FETCH_SIZE") * 1024.0)
+    w_fac = COPY_BYTES / (_copy_value(wd, "WRITE_SIZE") * 1024.0)
+    for disp, field in ((fd, "fetch"), (wd, "write"), (md, "mfma")):
+        for c, d in zip(classify([x["name"] for x in disp]), disp):
+            if c == "other":
+                continue
+            g = grp(c, d)
+            if field == "fetch":
+                g["fetch"].append(d["c"]["FETCH_SIZE"] * 1024.0 * f_fac)
+            elif field == "write":
+                g["write"].append(d["c"]["WRITE_SIZE"] * 1024.0 * w_fac)
+            else:
+                g["busy"].append(d["c"].get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0))
+                g["mops"].append(d["c"].get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0))
+                g["cdur"].append(d["dur_ns"])
+    avg = lambda xs: sum(xs) / len(xs) if xs else None  # noqa: E731
+    rows = []
+    for (c, name, grid), g in groups.items():
+        if g["n"] == 0:
+            continue
+        dur = g["dur"] / g["n"]
+        hbm = (avg(g["fetch"]) or 0.0) + (avg(g["write"]) or 0.0) if g["fetch"] and g["write"] else None
+        busy = avg(g["busy"])
+        cdur = avg(g["cdur"])
+        rows.append({"class": c, "kernel": name, "grid": grid, "dispatches": g["n"], "avg_us": dur / 1e3,
+                     "total_us": g["dur"] / 1e3, "hbm_bytes": hbm,
+                     "hbm_gbs": hbm / dur if hbm is not None else None,
+                     "mfma_busy": busy / (cdur * CLOCK_GHZ * SIMDS) if busy is not None and cdur else None,
+                     "mfma_tflops": (avg(g["mops"]) * 512) / (cdur * 1e3) if g["mops"] and cdur else None})
+    rows.sort(key=lambda r: -r["total_us"])
+    lines = [f"# rocprofv3 summary: {workload}\n",
+             "Every kernel of a profiled run of the workload (ring filled, then ticks of frame write + chunk "
+             "through the captured graphs), grouped by kernel class, kernel and grid.  Durations from the "
+             "kernel trace.  HBM bytes per dispatch: FETCH_SIZE and WRITE_SIZE (KiB) of their own runs, each "
+             f"scaled by what it reads for a plain 256 MiB copy in the same process (factors {f_fac:.4f} and "
+             f"{w_fac:.4f}).  MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES / (duration x {CLOCK_GHZ} GHz x {SIMDS} "
+             "SIMDs), from the counter run's own durations; MFMA TFLOP/s: SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 "
+             "flops / duration.\n",
+             "Commands:\n", "```"] + [f"{k}: {v}" for k, v in commands.items()] + ["```\n",
+             "| class | kernel | grid (threads) | dispatches | avg us | total us | HBM MB / dispatch | HBM GB/s | "
+             "MFMA busy | MFMA TFLOP/s |", "|---|---|---|---|---|---|---|---|---|---|"]
+    fmt = lambda v, f: (f % v) if v is not None else "-"  # noqa: E731
+    for r in rows:
+        lines.append(f"| {r['class']} | `{r['kernel']}` | {r['grid']} | {r['dispatches']} | {r['avg_us']:.2f} | "
+                     f"{r['total_us']:.1f} | {fmt(r['hbm_bytes'] and r['hbm_bytes'] / 1e6, '%.3f')} | "
+                     f"{fmt(r['hbm_gbs'], '%.1f')} | {fmt(r['mfma_busy'] and 100 * r['mfma_busy'], '%.1f %%')} | "
+                     f"{fmt(r['mfma_tflops'], '%.1f')} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    if out_json:
+        # one traffic record per class: its most time-consuming kernel; the
+        # attention record covers the kernel and its split merge (one unit per layer)
+        best: Dict[str, dict] = {}
+        for r in rows:
+            if r["class"] not in best and r["hbm_bytes"] is not None:
+                best[r["class"]] = r
+        records = {}
+        for c, r in best.items():
+            cls = c if c in KERNEL_SOURCES else "all"
+            hbm = r["hbm_bytes"]
+            dur = r["avg_us"]
+            if c == "attention" and "attn_merge" in best:
+                hbm += best["attn_merge"]["hbm_bytes"]
+                dur += best["attn_merge"]["avg_us"]
+            records[c] = {"workload": workload, "kernel_class": c, "kernel": r["kernel"], "grid": r["grid"],
+                          "digest": source_digest(cls), "digest_class": cls,
+                          "hbm_bytes_per_launch": round(hbm), "avg_duration_us": round(dur, 3),
+                          "mfma_busy": r["mfma_busy"], "fetch_factor": round(f_fac, 4),
+                          "write_factor": round(w_fac, 4), "commands": commands}
+        with open(out_json, "w") as f:
+            json.dump({"workload": workload, "records": records}, f, indent=1)
+            f.write("\n")
+    return {"rows": rows}
+
+
+def main_summarize(argv: Optional[List[str]] = None) -> None:
+    ap = argparse.ArgumentParser(description="per-workload kernel summary from a kernel trace and counter runs")
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--mfma", required=True)
+    ap.add_argument("--command", action="append", default=[], help="NAME=COMMAND, repeated")
+    ap.add_argument("--out-md", required=True)
+    ap.add_argument("--out-json")
+    a = ap.parse_args(argv)
+    cmds = dict(c.split("=", 1) for c in a.command)
+    summarize(a.workload, a.trace, a.fetch, a.write, a.mfma, cmds, a.out_md, a.out_json)
+
+
 if __name__ == "__main__":
-    main()
+    import sys
+
+    if len(sys.argv) > 1 and sys.argv[1] == "summarize":
+        main_summarize(sys.argv[2:])
+    else:
+        main()
