@@ -26,6 +26,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+from paper_2607_14695_amd.profiling import load_traffic  # noqa: E402
+
 METRIC = "denoise-step latency (us) + action chunks/s at batch 1/32; attn HBM GB/s"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
@@ -628,8 +630,6 @@ def main():
     ct = _class_times(prof)
     dominant = max((k for k in ct if k in bf), key=lambda k: ct[k][0])
     ms, n = ct[dominant]
-    from paper_2607_14695_amd.profiling import load_traffic
-
     traffic = load_traffic(os.path.join(ROOT, "profiles", f"traffic_{cfg.name}.json"), dominant)
     roofline = _roofline(dominant, "hbm", bf[dominant][0], bf[dominant][1], ms / n / 1e3, traffic)
     roofline["share_of_chunk"] = round(ms / sum(v[0] for v in ct.values()), 4)
@@ -668,16 +668,19 @@ def main():
             "attn_mfma_tflops": round(bf32["attention"][1] / (a_ms / a_n / 1e3) / 1e12, 1),
             "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in p32.items() if v[1]},
         }
-        b32["roofline"] = {"attention": _roofline("attention", "hbm", *bf32["attention"], a_ms / a_n / 1e3)}
+        tf32 = os.path.join(ROOT, "profiles", f"traffic_{c32.name}.json")
+        b32["roofline"] = {"attention": _roofline("attention", "hbm", *bf32["attention"], a_ms / a_n / 1e3,
+                                                  load_traffic(tf32, "attention"))}
         for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
             ms_k, n_k = p32[k]
             b32[f"{k}_mfma_tflops"] = round(bf32[k][1] / (ms_k / n_k / 1e3) / 1e12, 1)
-            b32["roofline"][k] = _roofline(k, "mfma", *bf32[k], ms_k / n_k / 1e3)
+            b32["roofline"][k] = _roofline(k, "mfma", *bf32[k], ms_k / n_k / 1e3, load_traffic(tf32, k))
         proj_ms = sum(p32[k][0] for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"))
         b32["projections_us_per_step"] = round(proj_ms / c32.num_steps * 1e3, 1)
         fp_ms, fp_n = pw32["frame_proj"]
         b32["frame_proj_mfma_tflops"] = round(rb32["frame_proj"][1] / (fp_ms / fp_n / 1e3) / 1e12, 1)
-        b32["roofline"]["frame_proj"] = _roofline("frame_proj", "mfma", *rb32["frame_proj"], fp_ms / fp_n / 1e3)
+        b32["roofline"]["frame_proj"] = _roofline("frame_proj", "mfma", *rb32["frame_proj"], fp_ms / fp_n / 1e3,
+                                                  load_traffic(tf32, "frame_proj"))
         b32["write_us"] = {k: round(v[0] / v[1] * 1e3, 3) for k, v in pw32.items() if v[1]}
         n32_ms, n32_n = p32["resid_norm"]
         b32["norm_gbs"] = round(_norm_bytes(c32) / (n32_ms / n32_n / 1e3) / 1e9, 1)
@@ -719,9 +722,11 @@ def main():
             "attn_mfma_tflops": round(bfl["attention"][1] / (al_ms / al_n / 1e3) / 1e12, 1),
             "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in pl.items() if v[1]},
         }
-        long_ctx["roofline"] = {"attention": _roofline("attention", "hbm", *bfl["attention"], al_ms / al_n / 1e3)}
+        tfl = os.path.join(ROOT, "profiles", f"traffic_{cl.name}.json")
+        long_ctx["roofline"] = {"attention": _roofline("attention", "hbm", *bfl["attention"], al_ms / al_n / 1e3,
+                                                       load_traffic(tfl, "attention"))}
         for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
-            long_ctx["roofline"][k] = _roofline(k, "mfma", *bfl[k], pl[k][0] / pl[k][1] / 1e3)
+            long_ctx["roofline"][k] = _roofline(k, "mfma", *bfl[k], pl[k][0] / pl[k][1] / 1e3, load_traffic(tfl, k))
         el.close()
         del el, wl
         log(f"long context: {long_ctx}")

@@ -439,10 +439,10 @@ def summarize(workload: str, trace: str, fetch: str, write: str, mfma: str, comm
             records[c] = {"workload": workload, "kernel_class": c, "kernel": r["kernel"], "grid": r["grid"],
                           "digest": source_digest(cls), "digest_class": cls,
                           "hbm_bytes_per_launch": round(hbm), "avg_duration_us": round(dur, 3),
-                          "mfma_busy": r["mfma_busy"], "fetch_factor": round(f_fac, 4),
-                          "write_factor": round(w_fac, 4), "commands": commands}
+                          "mfma_busy": r["mfma_busy"] and round(r["mfma_busy"], 4)}
         with open(out_json, "w") as f:
-            json.dump({"workload": workload, "records": records}, f, indent=1)
+            json.dump({"workload": workload, "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4),
+                       "commands": commands, "records": records}, f, indent=1)
             f.write("\n")
     return {"rows": rows}
 
