@@ -135,12 +135,32 @@ def _ring_bytes(cfg, prof_w):
     return {"frame_proj": (m * cfg.frame_dim * eb + n * cfg.frame_dim * eb + m * n * eb, 2.0 * m * n * cfg.frame_dim)}
 
 
+def release_grid(tick, ticks, period_s, now=time.perf_counter, sleep=time.sleep):
+    """Latencies (s) of `ticks` calls of tick() released on a grid of period_s:
+    a tick's latency runs from its release to tick()'s return.  A tick that
+    would start after its release starts at once, and no queue builds up behind
+    a slow tick: the next release is the first grid point not already passed.
+    A latency above period_s is a missed deadline."""
+    lat = []
+    t0 = now()
+    k = 0
+    for _ in range(ticks):
+        release = t0 + k * period_s
+        cur = now()
+        if cur < release:
+            sleep(max(0.0, release - cur - 0.0005))
+            while now() < release:
+                pass
+        tick()
+        done = now()
+        lat.append(done - release)
+        k = int((done - t0) / period_s) + 1
+    return lat
+
+
 def _stream_ticks(eng, frames, state, noise, ticks, warmup, torch, period_s=0.020):
-    """Tick latency on a release grid: a tick is released every period_s; its
-    latency runs from the release to the action chunk synced on the device
-    (frame write + denoise).  A tick that would start after its release is
-    started at once (no queue builds up behind a slow tick: the next release
-    is the first grid point not already passed)."""
+    """Tick latency on the 20 ms release grid (release_grid): frame write +
+    denoise, synced on the device."""
     import numpy as np
 
     for i in range(warmup):
@@ -148,24 +168,16 @@ def _stream_ticks(eng, frames, state, noise, ticks, warmup, torch, period_s=0.02
         eng.denoise(state, noise)
     eng.synchronize()
     torch.cuda.synchronize()
-    lat = []
-    t0 = time.perf_counter()
-    k = 0
-    for i in range(ticks):
-        release = t0 + k * period_s
-        now = time.perf_counter()
-        if now < release:
-            time.sleep(max(0.0, release - now - 0.0005))
-            while time.perf_counter() < release:
-                pass
-        eng.write_frame(frames[i % len(frames)])
+    it = [0]
+
+    def tick():
+        eng.write_frame(frames[it[0] % len(frames)])
         eng.denoise(state, noise)
         eng.synchronize()
         torch.cuda.synchronize()
-        done = time.perf_counter()
-        lat.append(done - release)
-        k = int((done - t0) / period_s) + 1
-    a = np.array(lat) * 1e3
+        it[0] += 1
+
+    a = np.array(release_grid(tick, ticks, period_s)) * 1e3
     return {"period_ms": period_s * 1e3, "ticks": ticks, "p50_ms": round(float(np.percentile(a, 50)), 3),
             "p99_ms": round(float(np.percentile(a, 99)), 3), "mean_ms": round(float(a.mean()), 3),
             "misses": int((a > period_s * 1e3).sum())}

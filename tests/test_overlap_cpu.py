@@ -119,3 +119,69 @@ def test_k_adapts_to_a_latency_change():
 def test_unknown_strategy_rejected():
     with pytest.raises(ValueError):
         OV.OverlapScheduler(None, 10, P, strategy="eager")
+
+
+class _SlowOncePolicy(OV.SimPolicy):
+    """A fixed inference latency, except that launch number `slow_index` is
+    held up by `extra_s` more (a host stall inside one tick)."""
+
+    def __init__(self, clock, latency_s, chunk_fn, slow_index, extra_s):
+        super().__init__(clock, latency_s, chunk_fn)
+        self.n, self.slow, self.extra = 0, slow_index, extra_s
+
+    def launch(self, state):
+        t, acts, fr = super().launch(state)
+        lat = self.lat + (self.extra if self.n == self.slow else 0.0)
+        self.n += 1
+        return (t, acts, fr, lat)
+
+    def ready(self, h):
+        return self.clock.now() >= h[0] + h[3] - 1e-12
+
+    def latency(self, h):
+        return h[3]
+
+
+@pytest.mark.parametrize("extra_periods", [0.5, 1.5, 3.5])
+def test_forced_overrun_is_counted_as_stalls(extra_periods):
+    """One chunk held up by a host stall: the overlapped schedule launched it
+    with K actions left, the queue runs dry K + 1 periods after the launch and
+    every further period until the chunk lands is a stall; the latency average
+    then raises K, so the steady chunks after it do not stall."""
+    chunk, lat = 10, 2.5 * P
+    clk = OV.SimClock()
+    fn = lambda s: [s[:4] + 0.01 * i for i in range(1, chunk + 1)]  # noqa: E731
+    pol = _SlowOncePolicy(clk, lat, fn, slow_index=4, extra_s=extra_periods * P)
+    sch = OV.OverlapScheduler(pol, chunk, P, strategy="reflex", clock=clk)
+    st = sch.run(OV.FirstOrderRobot(np.zeros(4)), 300)
+    k = math.ceil(lat / P - 1e-9)
+    expect = max(0, math.ceil((lat + extra_periods * P) / P - 1e-9) - k - 1)
+    assert st.stalls == expect, (st.stalls, expect)
+    assert max(st.latency_s) == pytest.approx(lat + extra_periods * P)
+
+
+def test_release_grid_counts_a_slow_tick_as_one_miss():
+    """The benchmark's 20 ms release grid on a fake clock: a tick that takes
+    2.5 periods is one missed deadline, and the next tick is released at the
+    next grid point after it (no queue of late ticks)."""
+    import bench
+
+    t = {"now": 0.0}
+    durations = iter([0.005, 0.005, 0.050, 0.005, 0.005])
+
+    def tick():
+        t["now"] += next(durations)
+
+    def sleep(dt):
+        t["now"] += dt
+
+    def now():
+        t["now"] += 1e-6  # a spin iteration costs a microsecond
+        return t["now"]
+
+    lat = bench.release_grid(tick, 5, 0.020, now=now, sleep=sleep)
+    misses = [x > 0.020 for x in lat]
+    assert misses == [False, False, True, False, False]
+    assert lat[2] == pytest.approx(0.050, abs=1e-3)
+    # the slow tick, released at 40 ms, ended at 90 ms: the next one waits for the 100 ms grid point
+    assert lat[3] == pytest.approx(0.005, abs=1e-3)
