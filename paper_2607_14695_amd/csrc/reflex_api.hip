@@ -662,14 +662,21 @@ int collect_profile(reflex_ctx* ctx, hipStream_t st) {
     ctx->prof_ms[i] = 0.0;
     ctx->prof_launches[i] = 0;
   }
+  int rc = REFLEX_OK;
   for (auto& pe : ctx->ev_pending) {
     float ms = 0.f;
-    (void)hipEventElapsedTime(&ms, pe.second.first, pe.second.second);
+    const hipError_t t = hipEventElapsedTime(&ms, pe.second.first, pe.second.second);
+    if (t != hipSuccess) {
+      // report the failure and leave no pending error behind for the caller's next HIP call
+      rc = hip_fail(t);
+      (void)hipGetLastError();
+      break;
+    }
     ctx->prof_ms[pe.first] += ms;
     ctx->prof_launches[pe.first] += 1;
   }
   ctx->ev_pending.clear();
-  return REFLEX_OK;
+  return rc;
 }
 
 // One frame write on stream st.  A write on the context's stream also
