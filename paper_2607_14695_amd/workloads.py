@@ -278,13 +278,3 @@ def make_noise(cfg: ReflexConfig, tick: int, envs: Optional[Sequence[int]] = Non
         out.append(x)
     return np.stack(out)
 
-
-def micro_config(**kw) -> ReflexConfig:
-    """A very small float32 shape for brute-force checks of the oracle."""
-    base = dict(name="micro", n_layers=1, width=8, mlp_dim=16, n_q_heads=2,
-                n_kv_heads=1, head_dim=4, state_dim=3, action_dim=3,
-                action_horizon=2, cond_hidden=8, static_len=3, frame_tokens=2,
-                window_frames=2, frame_dim=5, batch=1, dtype=DTYPE_F32,
-                num_steps=2, ticks=3)
-    base.update(kw)
-    return ReflexConfig(**base)

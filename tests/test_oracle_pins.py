@@ -13,6 +13,17 @@ from oracle import reflex_oracle as O
 from paper_2607_14695_amd import workloads as WL
 from tests import brute_force
 
+
+def micro_config(**kw):
+    """A very small float32 shape for brute-force checks of the oracle."""
+    base = dict(name="micro", n_layers=1, width=8, mlp_dim=16, n_q_heads=2,
+                n_kv_heads=1, head_dim=4, state_dim=3, action_dim=3,
+                action_horizon=2, cond_hidden=8, static_len=3, frame_tokens=2,
+                window_frames=2, frame_dim=5, batch=1, dtype=WL.DTYPE_F32,
+                num_steps=2, ticks=3)
+    base.update(kw)
+    return WL.ReflexConfig(**base)
+
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
@@ -255,7 +266,7 @@ def test_chunk_matches_scalar_brute_force(frame_dim, mod_mode, hkv):
     """The oracle's whole chunk (its own window, positions, context K/V and
     Euler loop) against scalar loops that rebuild the context from the raw
     static K/V, frames and w_kv rows, with hand-enumerated positions."""
-    cfg = WL.micro_config(frame_dim=frame_dim, mod_mode=mod_mode, n_kv_heads=hkv,
+    cfg = micro_config(frame_dim=frame_dim, mod_mode=mod_mode, n_kv_heads=hkv,
                           embed_scale=1.5 if hkv == 2 else 1.0)
     w, sk, sv, frames = _inputs(cfg, 3)
     fw = 3  # the ring has wrapped once
@@ -273,7 +284,7 @@ def test_chunk_matches_scalar_brute_force(frame_dim, mod_mode, hkv):
 def test_velocity_matches_scalar_brute_force_empty_ring():
     """No frame written: the context is the static prefix alone and the
     dynamic tokens start right after it (positions 3, 4, 5)."""
-    cfg = WL.micro_config(frame_dim=5)
+    cfg = micro_config(frame_dim=5)
     w, sk, sv, frames = _inputs(cfg, 1)
     state = WL.make_state(cfg, 0)
     noise = WL.make_noise(cfg, 0)
@@ -473,7 +484,7 @@ def test_prop_a1_partitioned_equals_full_batch_tiny():
 
 
 def test_prop_a1_with_empty_ring_and_direct_path():
-    cfg = WL.micro_config(frame_dim=0, window_frames=3)
+    cfg = micro_config(frame_dim=0, window_frames=3)
     w, sk, sv, frames = _inputs(cfg, 6)
     cache = O.PartitionedCache(cfg, w, sk, sv, env=0)
     taus = [1.0, 0.6, 0.1, 0.0]
