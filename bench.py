@@ -61,8 +61,11 @@ def _class_bytes_flops(cfg):
     Attention (with its split merge, one unit per layer): the visible cached K
     and V rows + q and the dynamic k, v in + o out, all in the operand type.
     Residual/norm: h and the projection in, h and y out, the modulation rows.
-    Final kernel: h, the projection and the action head in, actions in and out.
-    Token embedding + first norm: the embedding weights, state, x in, h and y
+    Final kernel: h, the projection and the action head in, actions in and out;
+    at every step but the last it also embeds the new actions for the next
+    step (the embedding weights, state, h and y out, the modulation rows), so
+    its figures are the average over a chunk's K launches.  Token embedding +
+    first norm (once per chunk): the embedding weights, state, x in, h and y
     out.  Modulation (three launches per chunk): the conditioning weights."""
     B, T = cfg.batch, cfg.action_horizon + 1
     M = B * T
@@ -81,8 +84,11 @@ def _class_bytes_flops(cfg):
                         B * 4.0 * Hq * dh * vis)
     out["resid_norm"] = (_norm_bytes(cfg), 0.0)
     da, ds = cfg.action_dim, cfg.state_dim
-    out["final_euler"] = (M * D * 4 * 2 + da * D * eb + 2 * B * (T - 1) * da * 4 + B * 6 * D * 4,
-                          2.0 * B * (T - 1) * da * D)
+    K = cfg.num_steps
+    nxt = (K - 1) / K  # share of the final launches that embed the next step
+    out["final_euler"] = (M * D * 4 * 2 + da * D * eb + 2 * B * (T - 1) * da * 4 + B * 6 * D * 4
+                          + nxt * (D * (ds + da) * eb + B * ds * 4 + M * D * (4 + eb) + B * 3 * D * 4),
+                          2.0 * B * (T - 1) * da * D + nxt * 2.0 * B * (ds + (T - 1) * da) * D)
     out["embed_norm"] = (D * (ds + da) * eb + B * ds * 4 + B * (T - 1) * da * 4 + M * D * (4 + eb) + B * 3 * D * 4,
                          2.0 * B * (ds + (T - 1) * da) * D)
     S = 2 * cfg.n_layers + 1
@@ -200,11 +206,14 @@ def _time_ticks(eng, frames, state, noise, steps, warmup, torch, denoise_only=Fa
     return (time.perf_counter() - t0) / steps
 
 
-def _chunk_latencies(eng, state, noise, n, torch):
+def _chunk_latencies(eng, state, noise, n, torch, warmup=20):
     """Device time of n back-to-back single chunks, each bracketed by events on
-    the engine's stream (ms): mean and percentiles."""
+    the engine's stream (ms): mean and percentiles, after `warmup` untimed
+    chunks."""
     import numpy as np
 
+    for _ in range(warmup):
+        eng.denoise(state, noise)
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
     for a, b in evs:
         a.record(eng.stream)
@@ -477,16 +486,34 @@ def soak(torch, log, ticks):
     return out
 
 
+def _warm_clocks(torch, seconds=0.3):
+    """Keep the GPU busy for `seconds` with library GEMMs before a profiled
+    region.  After an idle spell the clocks take tens of milliseconds to come
+    back up: in a kernel trace the first batch-32 chunk after idle averaged
+    42 us per attention launch (46 us in its first step) against 39 us for
+    every later chunk, with or without a frame write before it.  The warm-up
+    kernels are not the library's and stay out of the profile tables."""
+    a = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            torch.matmul(a, a)
+        torch.cuda.synchronize()
+    del a
+
+
 def profile_run(torch, log, name, ticks):
-    """A short run of one workload for the profiler: the ring filled, then
-    `ticks` ticks of frame write + chunk through the captured graphs (the
-    launch configuration of the timed benchmark), each tick synchronized."""
+    """A short run of one workload for the profiler: the GPU warmed up, the
+    ring filled, then `ticks` ticks of frame write + chunk through the
+    captured graphs (the launch configuration of the timed benchmark), each
+    tick synchronized."""
     from paper_2607_14695_amd import workloads as WL
     from paper_2607_14695_amd.reflex import ReflexEngine
 
     cfg = WL.CONFIGS[name]
     w, sk, sv, frames, state, noise = _device_inputs(cfg, torch)
     eng = ReflexEngine(cfg, w, sk, sv)
+    _warm_clocks(torch)
     for i in range(cfg.window_frames):
         eng.write_frame(frames[i % len(frames)])
     for i in range(ticks):
@@ -629,7 +656,7 @@ def main():
     ring_gbs = rb["ring_write"][0] / (rw_ms / rw_n / 1e3) / 1e9
     lat = None
     if not args.no_latency:
-        lat = _chunk_latencies(eng, state, noise, max(20, args.steps), torch)
+        lat = _chunk_latencies(eng, state, noise, max(100, args.steps), torch)
         log(f"chunk latency p50 {lat['p50']:.3f} ms, p99 {lat['p99']:.3f} ms")
     finite = bool(torch.isfinite(eng.denoise(state, noise)).all())
     if not finite:

@@ -162,8 +162,16 @@ struct FinalArgs {
   float dt, eps;
   int norm_mode;          // NormMode
   int32_t* status;        // bit 0 set when an action leaves the kernel non-finite
+  // fuse_next: also the next Euler step's token embedding and first norm
+  // (`next` as for launch_embed_norm; its x is this kernel's x_out, taken from
+  // LDS), one extra block per env for the state row.  next.h must be h; only
+  // where final_fuses_embed holds.
+  int fuse_next;
+  EmbedArgs next;
 };
 template <typename T> hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s);
+// whether launch_final_euler takes fuse_next for B envs of T tokens, width D
+bool final_fuses_embed(int B, int T, int D);
 
 // RoPE (cos, sin) table for positions pos0 + i, i < n; pos0 from *pos0_dev
 // when non-null.  Angles formed in double.

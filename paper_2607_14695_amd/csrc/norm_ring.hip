@@ -93,49 +93,55 @@ RFX_DEV float4 ada4(float4 v, float r, float4 sc, float4 sh) {
 // ---------------------------------------------------------------------------
 // embedding + first norm: row m = b*T + t; t = 0 is the state token
 // ---------------------------------------------------------------------------
-// GROUPED: per group of 8 inputs, the weight loads of a thread's four
-// columns are issued before any is used (one L2 round trip per group, not
-// per column and group); each column still sums its inputs in order.  Taken
-// for a few rows; with many rows the per-column form keeps more rows
-// resident (batch 32: 13.6 against 17.8 us).
+// h = embed_scale * W in and y = ada(h) for token row m = b*T + t (t = 0:
+// the state through W_s, else an action through W_ain), its n_in inputs
+// already in LDS (`in`, visible to every thread).  hs: D floats of LDS; red:
+// 4 floats of LDS for the norm's block reduction.  Shared by the embedding
+// kernel and the final kernel's next-step epilogue.
+// GROUPED: a thread issues the weight loads of up to 32 inputs (16 in fp32)
+// of its four columns before it uses any (one L2 round trip per round, not
+// per column and group of inputs).  Taken for a few rows; with many rows the
+// per-column form keeps more rows resident (batch 32: 13.6 against 17.8 us
+// for an earlier grouped form).  Each column sums its inputs in order, one
+// group of four at a time (for a multiple of 8 inputs, the same arithmetic
+// either way).
 template <typename T, bool GROUPED>
-__global__ __launch_bounds__(256) void embed_norm_kernel(EmbedArgs p) {
-  __shared__ float red[4];
-  __shared__ float in[64];
-  __shared__ float hs[16 * 256];
-  const int m = blockIdx.x, b = m / p.T, t = m % p.T;
+RFX_DEV void embed_row(const EmbedArgs& p, int64_t m, int b, int t, const float* in, float* hs, float* red) {
   const int n_in = (t == 0) ? p.ds : p.da;
-  const float* src = (t == 0) ? p.state + (int64_t)b * p.ds : p.x + ((int64_t)b * (p.T - 1) + (t - 1)) * p.da;
   const T* W = reinterpret_cast<const T*>(t == 0 ? p.w_state : p.w_ain);
-  if (threadIdx.x < n_in) in[threadIdx.x] = src[threadIdx.x];
-  __syncthreads();
   float ss = 0.f;
   if constexpr (GROUPED) {
+    constexpr int CH = 64 / (int)sizeof(T);  // inputs per round of loads: 32 bf16 / 16 fp32
     for (int cb = 0; cb < p.D; cb += 1024) {
       float acc[4] = {0.f, 0.f, 0.f, 0.f};
       const T* w[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u)  // clamped column: a valid address, result unused
         w[u] = W + (int64_t)min(cb + (int)threadIdx.x + 256 * u, p.D - 1) * n_in;
-      int e = 0;
       if ((n_in & 3) == 0) {
-        for (; e + 8 <= n_in; e += 8) {
-          float4 w0[4], w1[4];
+        // every load of a round is issued before any is used; the sum adds
+        // one group of four inputs at a time, in input order
+        for (int e0 = 0; e0 < n_in; e0 += CH) {
+          float4 wv[4][CH / 4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            w0[u] = ld4f(w[u] + e);
-            w1[u] = ld4f(w[u] + e + 4);
-          }
+          for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            acc[u] += w0[u].x * in[e] + w0[u].y * in[e + 1] + w0[u].z * in[e + 2] + w0[u].w * in[e + 3];
-            acc[u] += w1[u].x * in[e + 4] + w1[u].y * in[e + 5] + w1[u].z * in[e + 6] + w1[u].w * in[e + 7];
+            for (int j = 0; j < CH / 4; ++j) wv[u][j] = ld4f(w[u] + min(e0 + 4 * j, n_in - 4));  // clamped: unused
+#pragma unroll
+          for (int j = 0; j < CH / 4; ++j) {
+            const int e = e0 + 4 * j;
+            if (e < n_in) {
+#pragma unroll
+              for (int u = 0; u < 4; ++u)
+                acc[u] += wv[u][j].x * in[e] + wv[u][j].y * in[e + 1] + wv[u][j].z * in[e + 2] + wv[u][j].w * in[e + 3];
+            }
           }
         }
-      }
-      for (; e < n_in; ++e)
+      } else {
+        for (int e = 0; e < n_in; ++e)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) acc[u] += to_f(w[u][e]) * in[e];
+          for (int u = 0; u < 4; ++u) acc[u] += to_f(w[u][e]) * in[e];
+      }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = cb + threadIdx.x + 256 * u;
@@ -174,6 +180,19 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(EmbedArgs p) {
     const float y = xr * (1.f + mod[c]) + mod[p.D + c];
     reinterpret_cast<T*>(p.y)[(int64_t)m * p.D + c] = from_f<T>(y);
   }
+}
+
+template <typename T, bool GROUPED>
+__global__ __launch_bounds__(256) void embed_norm_kernel(EmbedArgs p) {
+  __shared__ float red[4];
+  __shared__ float in[64];
+  __shared__ float hs[16 * 256];
+  const int m = blockIdx.x, b = m / p.T, t = m % p.T;
+  const int n_in = (t == 0) ? p.ds : p.da;
+  const float* src = (t == 0) ? p.state + (int64_t)b * p.ds : p.x + ((int64_t)b * (p.T - 1) + (t - 1)) * p.da;
+  if (threadIdx.x < n_in) in[threadIdx.x] = src[threadIdx.x];
+  __syncthreads();
+  embed_row<T, GROUPED>(p, m, b, t, in, hs, red);
 }
 
 template <typename T>
@@ -244,15 +263,33 @@ hipError_t launch_resid_norm(const ResidArgs& a, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// last residual + final norm + action head + Euler: one block per action row
+// last residual + final norm + action head + Euler: one block per action row.
+// With fuse_next the kernel also starts the next Euler step: each action
+// row's block embeds its new x and applies the next step's first norm (the
+// embedding kernel's work for that row, in its grouped form), and one more
+// block per env, after the action rows, does the same for the state token.
+// The action rows read only their own h row, so writing it afterwards races
+// with no other block.  Taken for a few rows only (final_fuses_embed: the
+// launch-bound regime); at 32 envs the separate embedding kernel measured
+// faster, and the other variants stay without the embedding's registers.
 // ---------------------------------------------------------------------------
-// GU: action-head weight loads a thread issues before using any
-template <typename T, int MAXC, int GU>  // MAXC 4-column chunks per thread: D <= 1024 * MAXC
+// GU: action-head weight loads a thread issues before using any; FUSE: the
+// variant with the next step's embedding (p.fuse_next decides per launch)
+template <typename T, int MAXC, int GU, bool FUSE>  // MAXC 4-column chunks per thread: D <= 1024 * MAXC
 __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   __shared__ float red[4];
+  __shared__ float red2[4];
+  __shared__ float xin[64];
   __shared__ float4 ys[4 * 256];
   __shared__ float vpart[4][64];
   const int H = p.T - 1;
+  if (FUSE && blockIdx.x >= p.B * H) {  // the next step's state row of env b
+    const int b = blockIdx.x - p.B * H;
+    if (threadIdx.x < p.next.ds) xin[threadIdx.x] = p.next.state[(int64_t)b * p.next.ds + threadIdx.x];
+    __syncthreads();
+    embed_row<T, true>(p.next, (int64_t)b * p.T, b, 0, xin, reinterpret_cast<float*>(ys), red2);
+    return;
+  }
   const int b = blockIdx.x / H, i = blockIdx.x % H;
   const int64_t m = (int64_t)b * p.T + 1 + i;
   const float* gmod = p.gate_mod + (int64_t)b * 3 * p.D + 2 * p.D;
@@ -324,24 +361,35 @@ __global__ __launch_bounds__(256) void final_euler_kernel(FinalArgs p) {
   for (int a = threadIdx.x; a < p.da; a += 256) {
     const float x = p.x_in[xo + a] + p.dt * vpart[0][a];
     p.x_out[xo + a] = x;
+    xin[a] = x;
     if (!__builtin_isfinite(x)) atomicOr(p.status, 1);
   }
+  if (!FUSE || !p.fuse_next) return;
+  __syncthreads();  // xin complete; every read of ys is done
+  embed_row<T, true>(p.next, m, b, 1 + i, xin, reinterpret_cast<float*>(ys), red2);
 }
+
+bool final_fuses_embed(int B, int T, int D) { return B * T <= 256 && D <= 1024; }
 
 template <typename T>
 hipError_t launch_final_euler(const FinalArgs& a, hipStream_t s) {
   if (a.D > 16 * 256 || (a.D & 3) || a.da > 64) return hipErrorInvalidValue;
-  const dim3 grid(a.B * (a.T - 1));
+  if (a.fuse_next && (!final_fuses_embed(a.B, a.T, a.D) || a.next.D != a.D || a.next.B != a.B ||
+                      a.next.T != a.T || a.next.da != a.da || a.next.ds > 64 || a.next.h != a.h))
+    return hipErrorInvalidValue;
   // a few rows: every weight load of a thread in flight at once (32 for
   // D = 1024); many rows: groups of 8, fewer registers, more rows resident
-  if (a.D <= 1024 && grid.x <= 256)
-    RFX_LAUNCH((final_euler_kernel<T, 1, 32>), grid, dim3(256), 0, s, a);
+  const dim3 grid(a.B * (a.T - 1));
+  if (a.fuse_next)
+    RFX_LAUNCH((final_euler_kernel<T, 1, 32, true>), dim3(a.B * a.T), dim3(256), 0, s, a);
+  else if (a.D <= 1024 && grid.x <= 256)
+    RFX_LAUNCH((final_euler_kernel<T, 1, 32, false>), grid, dim3(256), 0, s, a);
   else if (a.D <= 1024)
-    RFX_LAUNCH((final_euler_kernel<T, 1, 8>), grid, dim3(256), 0, s, a);
+    RFX_LAUNCH((final_euler_kernel<T, 1, 8, false>), grid, dim3(256), 0, s, a);
   else if (a.D <= 2048)
-    RFX_LAUNCH((final_euler_kernel<T, 2, 8>), grid, dim3(256), 0, s, a);
+    RFX_LAUNCH((final_euler_kernel<T, 2, 8, false>), grid, dim3(256), 0, s, a);
   else
-    RFX_LAUNCH((final_euler_kernel<T, 4, 8>), grid, dim3(256), 0, s, a);
+    RFX_LAUNCH((final_euler_kernel<T, 4, 8, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -368,12 +368,20 @@ int enqueue_chunk(reflex_ctx* ctx, const Workspace& W, const float* state, const
   const char* wdown = (const char*)ctx->w.w_down;
   const int64_t rpart_stride = (int64_t)M * D;
 
+  // token embedding + first norm of step k (x_k, site 0 of step k).  With a
+  // few rows (launch-bound) the final kernel of step k - 1 does it for k > 0.
+  auto embed_args = [&](int k, const float* x) {
+    return EmbedArgs{x, state, ctx->w.w_state, ctx->w.w_ain, mod_at(0, k), W.h, W.y,
+                     B, Tn, D, c.state_dim, c.action_dim, c.embed_scale, c.rms_eps, c.norm_precision};
+  };
+  const bool fuse_embed = final_fuses_embed(B, Tn, D);
   for (int k = 0; k < steps; ++k) {
     const float* x_in = (k == 0) ? noise : out;
     if (mode == REFLEX_MODE_STANDARD) RFX_TRY(reencode_history<T>(ctx, src, L));
-    EmbedArgs ea{x_in, state, ctx->w.w_state, ctx->w.w_ain, mod_at(0, k), W.h, W.y,
-                 B, Tn, D, c.state_dim, c.action_dim, c.embed_scale, c.rms_eps, c.norm_precision};
-    RFX_TRY(L.run(PC_EMBED, [&] { return launch_embed_norm<T>(ea, st); }));
+    if (k == 0 || !fuse_embed) {
+      const EmbedArgs ea = embed_args(k, x_in);
+      RFX_TRY(L.run(PC_EMBED, [&] { return launch_embed_norm<T>(ea, st); }));
+    }
     for (int l = 0; l < c.n_layers; ++l) {
       GemmArgs q{};
       q.A = W.y; q.lda = D;
@@ -439,7 +447,8 @@ int enqueue_chunk(reflex_ctx* ctx, const Workspace& W, const float* state, const
     const float dt = (float)((double)taus[k + 1] - (double)taus[k]);
     FinalArgs fa{W.h, W.rparts, rpart_stride, P.down.splits, mod_at(2 * c.n_layers - 1, k),
                  mod_at(2 * c.n_layers, k), ctx->w.w_aout, x_in, out, B, Tn, D, c.action_dim, dt, c.rms_eps,
-                 c.norm_precision, W.status};
+                 c.norm_precision, W.status, fuse_embed && k + 1 < steps ? 1 : 0,
+                 embed_args(k + 1 < steps ? k + 1 : k, out)};
     RFX_TRY(L.run(PC_FINAL, [&] { return launch_final_euler<T>(fa, st); }));
   }
   return REFLEX_OK;
