@@ -109,13 +109,39 @@ def _roofline(kernel, bound, nbytes, flops, seconds, traffic=None):
             "frac": round(achieved / peak, 4), "traffic": traffic, "avg_us": round(seconds * 1e6, 3)}
 
 
+def _graph_profile(eng, state, noise, reps=3):
+    """{class: (ms per chunk, launches per chunk)}, each kernel class timed
+    inside the chunk's captured graph: its launches bracketed by wall-clock
+    stamp kernels, each bracket less the cost of a launch boundary measured at
+    the same point (reflex_profile_graph), so every kernel runs in the chunk's
+    own order and cache state.  Launch counts from one eager profiled chunk.
+    "attention_unit" is the attention kernel and its split merge (one unit
+    per layer)."""
+    eager = eng.profile(state, noise)
+    out = {}
+    for cls, (_, n) in eager.items():
+        if n and cls not in ("frame_proj", "ring_write"):
+            out[cls] = eng.profile_graph(state, noise, [cls], reps=reps)
+    if out.get("attn_merge", (0, 0))[1]:
+        ms, _ = eng.profile_graph(state, noise, ["attention", "attn_merge"], reps=reps)
+        out["attention_unit"] = (ms, out["attention"][1])
+    return out
+
+
 def _class_times(prof):
     """{class: (total ms, launches)} with the attention merge folded into the
     attention (one attention unit per layer: the kernel and its merge)."""
-    out = {k: v for k, v in prof.items() if v[1] and k != "attn_merge"}
-    if "attention" in out and prof.get("attn_merge", (0, 0))[1]:
+    out = {k: v for k, v in prof.items() if v[1] and k not in ("attn_merge", "attention_unit")}
+    if "attention_unit" in prof:
+        out["attention"] = prof["attention_unit"]
+    elif "attention" in out and prof.get("attn_merge", (0, 0))[1]:
         out["attention"] = (out["attention"][0] + prof["attn_merge"][0], out["attention"][1])
     return out
+
+
+def _avg_us(prof):
+    """Average device microseconds per launch of every timed class."""
+    return {k: round(v[0] / v[1] * 1e3, 3) for k, v in prof.items() if v[1] and k != "attention_unit"}
 
 
 def _norm_bytes(cfg):
@@ -382,9 +408,10 @@ def sweep_window(torch, log, windows=(1, 2, 5, 10, 20, 50)):
         r["reflex_chunk_ms"] = _event_ms(eng, torch, lambda: eng.denoise(state, noise), 10)
         r["standard_chunk_ms"] = _event_ms(eng, torch, lambda: eng.denoise(state, noise, mode="standard"), 3)
         r["standard_over_reflex"] = round(r["standard_chunk_ms"] / r["reflex_chunk_ms"], 3)
-        prof = eng.profile(state, noise)
-        r["attention_us"] = round(prof["attention"][0] / prof["attention"][1] * 1e3, 3)
-        r["attn_merge_us"] = round(prof["attn_merge"][0] / max(1, prof["attn_merge"][1]) * 1e3, 3)
+        a_ms, a_n = eng.profile_graph(state, noise, ["attention"])
+        m_ms, m_n = eng.profile_graph(state, noise, ["attn_merge"])  # (0, 0) with one key split
+        r["attention_us"] = round(a_ms / a_n * 1e3, 3)
+        r["attn_merge_us"] = round(m_ms / m_n * 1e3, 3) if m_n else 0.0
         k = [0]
 
         def tick():
@@ -502,11 +529,14 @@ def _warm_clocks(torch, seconds=0.3):
     del a
 
 
-def profile_run(torch, log, name, ticks):
+def profile_run(torch, log, name, ticks, stamps=False):
     """A short run of one workload for the profiler: the GPU warmed up, the
     ring filled, then `ticks` ticks of frame write + chunk through the
     captured graphs (the launch configuration of the timed benchmark), each
-    tick synchronized."""
+    tick synchronized.  With `stamps`, then the in-graph class timing the
+    benchmark reports (_graph_profile), its per-launch microseconds in the
+    returned record, so that a kernel trace of this run holds the very
+    dispatches those figures measure."""
     from paper_2607_14695_amd import workloads as WL
     from paper_2607_14695_amd.reflex import ReflexEngine
 
@@ -523,8 +553,13 @@ def profile_run(torch, log, name, ticks):
         if not bool(torch.isfinite(out).all()):
             raise RuntimeError(f"non-finite actions in the profiled {name} run")
         log(f"profile run {name}: tick {i + 1}/{ticks}")
+    rec = {"metric": "profile_run", "workload": name, "ticks": ticks, "batch": cfg.batch}
+    if stamps:
+        gp = _graph_profile(eng, state, noise)
+        rec["stamp_us"] = {k: round(v[0] / v[1] * 1e3, 3) for k, v in gp.items() if v[1]}
+        log(f"profile run {name}: in-graph class timing done")
     eng.close()
-    return {"metric": "profile_run", "workload": name, "ticks": ticks, "batch": cfg.batch}
+    return rec
 
 
 def cpu_baseline(cfg, log):
@@ -599,6 +634,8 @@ def main():
                     help="also run a plain 256 MiB elementwise copy (reference for HBM byte counters)")
     ap.add_argument("--profile-workload", metavar="NAME",
                     help="instead of the benchmark line, run a few ticks of one workload (for rocprofv3)")
+    ap.add_argument("--stamps", action="store_true",
+                    help="with --profile-workload: also the benchmark's in-graph class timing")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -639,7 +676,8 @@ def main():
         log("calibration copy: 3 x 256 MiB")
 
     if args.profile_workload:
-        print(json.dumps(profile_run(torch, log, args.profile_workload, max(1, args.steps))), flush=True)
+        print(json.dumps(profile_run(torch, log, args.profile_workload, max(1, args.steps), args.stamps)),
+              flush=True)
         return
 
     cfg = WL.CONFIGS["pi0_chunk_bf16"]
@@ -661,7 +699,7 @@ def main():
     finite = bool(torch.isfinite(eng.denoise(state, noise)).all())
     if not finite:
         raise RuntimeError("non-finite actions from the timed batch-1 configuration")
-    prof = eng.profile(state, noise)
+    prof = _graph_profile(eng, state, noise)
     log("profile: " + ", ".join(f"{k}={v[0]:.3f}ms/{v[1]}" for k, v in prof.items() if v[1]))
     bf = _class_bytes_flops(cfg)
     # the dominant kernel class: the largest share of the chunk's device time,
@@ -674,7 +712,7 @@ def main():
     roofline["share_of_chunk"] = round(ms / sum(v[0] for v in ct.values()), 4)
     attn_ms, attn_n = ct["attention"]
     attn_gbs = bf["attention"][0] / (attn_ms / attn_n / 1e3) / 1e9
-    kernel_avg_us = {k: round(v[0] / v[1] * 1e3, 3) for k, v in prof.items() if v[1]}
+    kernel_avg_us = _avg_us(prof)
     n_ms, n_n = prof["resid_norm"]
     norm_gbs = _norm_bytes(cfg) / (n_ms / n_n / 1e3) / 1e9
     eng.close()
@@ -690,7 +728,7 @@ def main():
         c32s = _time_ticks(e32, fr32, st32, nz32, steps32, 1, torch, denoise_only=True)
         if not bool(torch.isfinite(e32.denoise(st32, nz32)).all()):
             raise RuntimeError("non-finite actions from the timed batch-32 configuration")
-        p32 = e32.profile(st32, nz32)
+        p32 = _graph_profile(e32, st32, nz32)
         pw32 = e32.profile_write(fr32[0])
         rb32 = _ring_bytes(c32, pw32)
         bf32 = _class_bytes_flops(c32)
@@ -705,7 +743,7 @@ def main():
             "denoise_step_us": round(c32s / c32.num_steps * 1e6, 1),
             "attn_hbm_gbs": round(bf32["attention"][0] / (a_ms / a_n / 1e3) / 1e9, 1),
             "attn_mfma_tflops": round(bf32["attention"][1] / (a_ms / a_n / 1e3) / 1e12, 1),
-            "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in p32.items() if v[1]},
+            "kernel_avg_us": _avg_us(p32),
         }
         tf32 = os.path.join(ROOT, "profiles", f"traffic_{c32.name}.json")
         b32["roofline"] = {"attention": _roofline("attention", "hbm", *bf32["attention"], a_ms / a_n / 1e3,
@@ -748,7 +786,7 @@ def main():
         cls_ = _time_ticks(el, frl, stl, nzl, max(3, args.steps // 3), 1, torch, denoise_only=True)
         if not bool(torch.isfinite(el.denoise(stl, nzl)).all()):
             raise RuntimeError("non-finite actions from the timed long-context configuration")
-        pl = el.profile(stl, nzl)
+        pl = _graph_profile(el, stl, nzl)
         bfl = _class_bytes_flops(cl)
         al_ms, al_n = _class_times(pl)["attention"]
         long_ctx = {
@@ -759,7 +797,7 @@ def main():
             "attn_us": round(al_ms / al_n * 1e3, 2),
             "attn_hbm_gbs": round(bfl["attention"][0] / (al_ms / al_n / 1e3) / 1e9, 1),
             "attn_mfma_tflops": round(bfl["attention"][1] / (al_ms / al_n / 1e3) / 1e12, 1),
-            "kernel_avg_us": {k: round(v[0] / v[1] * 1e3, 3) for k, v in pl.items() if v[1]},
+            "kernel_avg_us": _avg_us(pl),
         }
         tfl = os.path.join(ROOT, "profiles", f"traffic_{cl.name}.json")
         long_ctx["roofline"] = {"attention": _roofline("attention", "hbm", *bfl["attention"], al_ms / al_n / 1e3,

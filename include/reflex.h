@@ -420,6 +420,28 @@ int reflex_profile_enable(reflex_ctx* ctx, int enable);
 int reflex_profile_read(reflex_ctx* ctx, const char** names, double* ms, int32_t* launches,
                         int32_t* n_classes);
 
+/*
+ * Device time of some kernel classes inside the chunk's graph (diagnostics;
+ * the launch-level timing of Appendix D's measurement).  One
+ * reflex_denoise_chunk call (same arguments and rules; it computes and writes
+ * actions_out) is captured into a HIP graph in which every launch of a class
+ * whose bit is set in class_mask (bit i: class i in reflex_profile_read's
+ * order) is bracketed by one-thread kernels that write the GPU's wall clock:
+ * two back to back before it, one after.  Per launch the time is (t2 - t1) -
+ * (t1 - t0), the bracket minus the cost of a launch boundary measured at the
+ * same point of the graph, so every kernel runs in the chunk's own order and
+ * cache state.  The graph is replayed once untimed and then reps times, the
+ * stamps read back after each.  Out: the summed milliseconds of the selected
+ * classes per chunk (mean over the replays) and their launches per chunk (0
+ * and 0 when they launch nothing).  Allocates and frees a stamp buffer;
+ * synchronizes the stream.  Errors: REFLEX_ESTATE, REFLEX_EINVAL (null
+ * pointers, num_steps out of range, reps < 1, no known class selected),
+ * REFLEX_EHIP.
+ */
+int reflex_profile_graph(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                         const float* tau_schedule, float* actions_out, uint32_t class_mask, int32_t reps,
+                         double* ms_per_replay, int32_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

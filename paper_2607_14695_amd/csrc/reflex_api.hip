@@ -216,6 +216,11 @@ struct reflex_ctx {
   int32_t prof_launches[PC_N];
   std::vector<hipEvent_t> ev_pool;
   std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> ev_pending;
+  // in-graph timing: launches of the classes in stamp_mask (bit i: class i)
+  // are bracketed by wall-clock stamps written to stamps[3 j .. 3 j + 2]
+  uint32_t stamp_mask = 0;
+  unsigned long long* stamps = nullptr;
+  int32_t stamp_next = 0, stamp_cap = 0;
   // pipelined streaming (spare slot): completion events of the last two frame
   // writes (n = frame index) and of recent chunks (n = frames they read, one
   // record per distinct n, increasing), with a pool of free events
@@ -265,6 +270,12 @@ hipEvent_t pipe_event(reflex_ctx* ctx) {
   return e;
 }
 
+// One thread writes the GPU's constant-rate wall clock: in a graph it runs
+// after the previous launch has completed and before the next one starts.
+__global__ __launch_bounds__(64) void stamp_kernel(unsigned long long* slot) {
+  if (threadIdx.x == 0) *slot = (unsigned long long)wall_clock64();
+}
+
 struct Launcher {
   reflex_ctx* ctx;
   bool prof;
@@ -277,8 +288,21 @@ struct Launcher {
     }
     return ctx->ev_pool[ev_next++];
   }
+  hipError_t stamp(int k) {
+    hipLaunchKernelGGL(stamp_kernel, dim3(1), dim3(64), 0, ctx->stream, ctx->stamps + ctx->stamp_next + k);
+    return hipGetLastError();
+  }
   template <typename F>
   int run(int cls, F&& f) {
+    // in-graph timing: two adjacent stamps (their difference is the cost of a
+    // launch boundary at this point of the graph), the launch, a third stamp
+    const bool stamped = (ctx->stamp_mask >> cls) & 1u;
+    if (stamped) {
+      if (ctx->stamp_next + 3 > ctx->stamp_cap) return REFLEX_EINVAL;
+      hipError_t e = stamp(0);
+      if (e == hipSuccess) e = stamp(1);
+      if (e != hipSuccess) return hip_fail(e);
+    }
     hipEvent_t a = nullptr, b = nullptr;
     if (prof) {
       a = take();
@@ -291,6 +315,11 @@ struct Launcher {
     g_launch_events = LaunchEvents{};
     if (e != hipSuccess) return hip_fail(e);
     if (prof) ctx->ev_pending.push_back({cls, {a, b}});
+    if (stamped) {
+      e = stamp(2);
+      if (e != hipSuccess) return hip_fail(e);
+      ctx->stamp_next += 3;
+    }
     return REFLEX_OK;
   }
 };
@@ -1194,6 +1223,80 @@ int reflex_profile_read(reflex_ctx* ctx, const char** names, double* ms, int32_t
     launches[i] = ctx->prof_launches[i];
   }
   *n_classes = n;
+  return REFLEX_OK;
+}
+
+int reflex_profile_graph(reflex_ctx* ctx, const float* state, const float* noise, int32_t num_steps,
+                         const float* tau_schedule, float* actions_out, uint32_t class_mask, int32_t reps,
+                         double* ms_per_replay, int32_t* launches) {
+  if (!ctx || !ctx->alive) return REFLEX_ESTATE;
+  if (!state || !noise || !actions_out || !ms_per_replay || !launches) return REFLEX_EINVAL;
+  if (num_steps < 1 || num_steps > ctx->cfg.max_steps || reps < 1 || (class_mask & ((1u << PC_N) - 1)) == 0)
+    return REFLEX_EINVAL;
+  float taus[REFLEX_MAX_STEPS + 1];
+  RFX_TRY(read_taus(ctx, tau_schedule, num_steps, taus));
+  int dev = 0, khz = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (khz <= 0) return hip_fail(hipErrorInvalidValue);
+
+  // room for three stamps per launch of the chunk (a bound on its launches:
+  // at most 12 per layer and step plus the per-chunk ones)
+  const reflex_config& c = ctx->cfg;
+  const int cap = 3 * (num_steps * (12 * c.n_layers + 8) + 16);
+  unsigned long long* stamps = nullptr;
+  e = hipMalloc(&stamps, sizeof(unsigned long long) * cap);
+  if (e != hipSuccess) return hip_fail(e);
+  std::vector<unsigned long long> host(cap);
+
+  // the whole chunk, the selected classes' launches stamped
+  hipGraph_t graph;
+  hipGraphExec_t exec = nullptr;
+  int rc = REFLEX_OK;
+  e = hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal);
+  if (e == hipSuccess) {
+    ctx->stamp_mask = class_mask;
+    ctx->stamps = stamps;
+    ctx->stamp_next = 0;
+    ctx->stamp_cap = cap;
+    rc = enqueue_chunk_dispatch(ctx, ctx->ws, state, noise, num_steps, taus, actions_out, false,
+                                REFLEX_MODE_REFLEX, nullptr);
+    ctx->stamp_mask = 0;
+    ctx->stamps = nullptr;
+    e = hipStreamEndCapture(ctx->stream, &graph);
+    if (e == hipSuccess && rc != REFLEX_OK) (void)hipGraphDestroy(graph);
+    if (e == hipSuccess && rc == REFLEX_OK) {
+      e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+    }
+  }
+  const int n = ctx->stamp_next / 3;
+  double ticks = 0.0;
+  // one untimed replay, then reps replays, the stamps read back after each
+  if (rc == REFLEX_OK && e == hipSuccess) e = hipGraphLaunch(exec, ctx->stream);
+  for (int r = 0; rc == REFLEX_OK && e == hipSuccess && r < reps; ++r) {
+    e = hipGraphLaunch(exec, ctx->stream);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(host.data(), stamps, sizeof(unsigned long long) * 3 * n, hipMemcpyDeviceToHost,
+                         ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    for (int j = 0; e == hipSuccess && j < n; ++j) {
+      const double t0 = (double)host[3 * j], t1 = (double)host[3 * j + 1], t2 = (double)host[3 * j + 2];
+      ticks += (t2 - t1) - (t1 - t0);
+    }
+  }
+  if (exec) (void)hipGraphExecDestroy(exec);
+  const hipError_t f = hipFree(stamps);
+  if (rc != REFLEX_OK) return rc;
+  if (e == hipSuccess) e = f;
+  if (e != hipSuccess) {
+    const int r = hip_fail(e);
+    (void)hipGetLastError();  // leave no pending error for the caller's next call
+    return r;
+  }
+  *ms_per_replay = ticks / reps / (double)khz;  // kHz: ticks per millisecond
+  *launches = n;
   return REFLEX_OK;
 }
 

@@ -350,8 +350,33 @@ def _copy_value(disp: List[dict], counter: str) -> float:
     return sorted(vals)[len(vals) // 2]
 
 
+STAMP_PATTERN = re.compile(r"stamp_kernel")
+
+
+def stamp_validation(trace: str, stamp_us: Dict[str, float]) -> List[dict]:
+    """Per kernel class: the kernel-trace durations of the dispatches that the
+    in-graph class timing stamped (a library dispatch right after two stamp
+    kernels) against the stamp figure the same run reported."""
+    tr = _trace_dispatches(trace)
+    tcls = classify([d["name"] for d in tr])
+    acc: Dict[str, List[float]] = {}
+    for i in range(2, len(tr)):
+        if tcls[i] != "other" and STAMP_PATTERN.search(tr[i - 1]["name"]) and \
+                STAMP_PATTERN.search(tr[i - 2]["name"]):
+            acc.setdefault(tcls[i], []).append(tr[i]["dur_ns"] / 1e3)
+    rows = []
+    for c, durs in acc.items():
+        if c in stamp_us:
+            t = sum(durs) / len(durs)
+            rows.append({"class": c, "stamped": len(durs), "trace_us": t, "stamp_us": stamp_us[c],
+                         "ratio": stamp_us[c] / t})
+    rows.sort(key=lambda r: r["class"])
+    return rows
+
+
 def summarize(workload: str, trace: str, fetch: str, write: str, mfma: str, commands: Dict[str, str],
-              out_md: str, out_json: Optional[str]) -> dict:
+              out_md: str, out_json: Optional[str], stamp_trace: Optional[str] = None,
+              stamp_us: Optional[Dict[str, float]] = None) -> dict:
     """Per (class, kernel, grid): dispatches, average duration (kernel trace),
     calibrated HBM bytes per dispatch (FETCH_SIZE and WRITE_SIZE runs), MFMA
     busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over duration x clock x SIMDs) and
@@ -419,6 +444,17 @@ def summarize(workload: str, trace: str, fetch: str, write: str, mfma: str, comm
                      f"{r['total_us']:.1f} | {fmt(r['hbm_bytes'] and r['hbm_bytes'] / 1e6, '%.3f')} | "
                      f"{fmt(r['hbm_gbs'], '%.1f')} | {fmt(r['mfma_busy'] and 100 * r['mfma_busy'], '%.1f %%')} | "
                      f"{fmt(r['mfma_tflops'], '%.1f')} |")
+    if stamp_trace and stamp_us:
+        lines += ["", "In-graph class timing against the trace of the same dispatches: the benchmark's per-class "
+                  "durations come from wall-clock stamp kernels around each launch inside the chunk's graph "
+                  "(reflex_profile_graph).  The stamp run (command `stamps`) makes that measurement under the "
+                  "kernel tracer; per class, the stamp figure it reported against the traced durations of the "
+                  "stamped dispatches themselves.", "",
+                  "| class | stamped dispatches | trace avg us | stamp avg us | stamp / trace |",
+                  "|---|---|---|---|---|"]
+        for r in stamp_validation(stamp_trace, stamp_us):
+            lines.append(f"| {r['class']} | {r['stamped']} | {r['trace_us']:.2f} | {r['stamp_us']:.2f} | "
+                         f"{r['ratio']:.3f} |")
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
     if out_json:
@@ -457,9 +493,17 @@ def main_summarize(argv: Optional[List[str]] = None) -> None:
     ap.add_argument("--command", action="append", default=[], help="NAME=COMMAND, repeated")
     ap.add_argument("--out-md", required=True)
     ap.add_argument("--out-json")
+    ap.add_argument("--stamp-trace", help="kernel trace of a `bench.py --profile-workload W --stamps` run")
+    ap.add_argument("--stamp-log", help="that run's output: its JSON line holds stamp_us")
     a = ap.parse_args(argv)
     cmds = dict(c.split("=", 1) for c in a.command)
-    summarize(a.workload, a.trace, a.fetch, a.write, a.mfma, cmds, a.out_md, a.out_json)
+    stamp_us = None
+    if a.stamp_log:
+        with open(a.stamp_log) as f:
+            for line in f:
+                if line.startswith("{") and "stamp_us" in line:
+                    stamp_us = json.loads(line)["stamp_us"]
+    summarize(a.workload, a.trace, a.fetch, a.write, a.mfma, cmds, a.out_md, a.out_json, a.stamp_trace, stamp_us)
 
 
 if __name__ == "__main__":

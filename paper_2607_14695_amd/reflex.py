@@ -11,7 +11,7 @@ import collections
 import ctypes
 import os
 import re
-from typing import Dict, Optional, Sequence, Tuple
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -114,6 +114,8 @@ def load_library() -> ctypes.CDLL:
         "reflex_frames_written": (c_i64, [c_vp]),
         "reflex_profile_enable": (c_i32, [c_vp, c_i32]),
         "reflex_profile_read": (c_i32, [c_vp, P(ctypes.c_char_p), P(c_f64), P(c_i32), P(c_i32)]),
+        "reflex_profile_graph": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp, ctypes.c_uint32, c_i32, P(c_f64),
+                                         P(c_i32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -442,6 +444,42 @@ class ReflexEngine:
                 mode: str = "reflex") -> Dict[str, Tuple[float, int]]:
         """Run one denoise eagerly with per-launch events; {class: (ms, launches)}."""
         return self._profiled(lambda: self.denoise(state, noise, num_steps, mode=mode))
+
+    def class_names(self) -> List[str]:
+        """The library's kernel classes, in the bit order of class masks."""
+        n = 32
+        names = (ctypes.c_char_p * n)()
+        ms = (c_f64 * n)()
+        cnt = (c_i32 * n)()
+        nc = c_i32(n)
+        _check(self.lib.reflex_profile_read(self.ctx, names, ms, cnt, ctypes.byref(nc)), "reflex_profile_read")
+        return [names[i].decode() for i in range(nc.value)]
+
+    def profile_graph(self, state, noise, classes: Sequence[str], reps: int = 5,
+                      num_steps: Optional[int] = None) -> Tuple[float, int]:
+        """Device time of the given kernel classes inside the chunk's graph:
+        one full denoise first, then a captured graph of the same chunk in
+        which each launch of those classes is bracketed by wall-clock stamps
+        (reflex_profile_graph), replayed reps times.  Returns (ms per chunk
+        summed over those classes' launches, launches per chunk)."""
+        names = self.class_names()
+        unknown = [c for c in classes if c not in names]
+        if unknown:
+            raise ValueError(f"unknown kernel classes {unknown}")
+        mask = 0
+        for c in classes:
+            mask |= 1 << names.index(c)
+        k = num_steps if num_steps is not None else self.cfg.num_steps
+        out = self.denoise(state, noise, k)
+        s, n, _ = self._keep_io
+        taus = self._keep_taus if (self.cfg.tau_schedule is not None and k == self.cfg.num_steps) else None
+        tau_arr = taus.ctypes.data if isinstance(taus, np.ndarray) else None
+        ms = c_f64(0.0)
+        cnt = c_i32(0)
+        _check(self.lib.reflex_profile_graph(self.ctx, s.data_ptr(), n.data_ptr(), k, tau_arr, out.data_ptr(),
+                                             mask, reps, ctypes.byref(ms), ctypes.byref(cnt)),
+               "reflex_profile_graph")
+        return ms.value, cnt.value
 
     def profile_write(self, frame) -> Dict[str, Tuple[float, int]]:
         """Write one frame eagerly with per-launch events; {class: (ms, launches)}."""

@@ -107,3 +107,32 @@ def test_summarize_calibrates_bytes_and_mfma_busy(tmp_path):
     doc = json.loads((tmp_path / "t.json").read_text())
     assert doc["records"]["gemm_qkv"]["hbm_bytes_per_launch"] == round(row["hbm_bytes"])
     assert P.load_traffic(str(tmp_path / "t.json"), "gemm_qkv") == round(row["hbm_bytes"])
+
+
+def test_stamp_validation_takes_only_the_stamped_dispatches(tmp_path):
+    stamp = "(anonymous namespace)::stamp_kernel(unsigned long long*)"
+    attn = "reflex::attn_pair_kernel<256>(reflex::AttnArgs)"
+    merge = "reflex::attn_merge_kernel<unsigned short, 256, 2>(reflex::AttnArgs)"
+    seq, t = [], 0
+
+    def add(name, dur):
+        nonlocal t
+        seq.append((name, 64, t, t + dur, None))
+        t += dur + 100
+
+    add(attn, 9000)           # unstamped: ignored
+    add(merge, 4000)
+    for _ in range(3):        # stamped attention launches of 8 and 10 us
+        add(stamp, 500)
+        add(stamp, 500)
+        add(attn, 8000 if _ % 2 == 0 else 10000)
+        add(stamp, 500)
+    add(merge, 3000)          # after the last launch's trailing stamp only: not stamped
+    path = tmp_path / "kt.csv"
+    _trace_csv(path, seq)
+    rows = P.stamp_validation(str(path), {"attention": 8.5, "attn_merge": 3.0})
+    assert [r["class"] for r in rows] == ["attention"]
+    r = rows[0]
+    assert r["stamped"] == 3
+    assert abs(r["trace_us"] - (8.0 + 10.0 + 8.0) / 3) < 1e-9
+    assert abs(r["ratio"] - 8.5 / r["trace_us"]) < 1e-12
