@@ -661,10 +661,11 @@ RFX_DEV bool dma_tile(const GemmArgs& p, int& bx, int& by, int& bz) {
 // maxima (no wait)
 constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-// BM (128, 96 or 64) rows per tile: two waves along M hold BM/2 rows each
-// (MB = BM/32 blocks of 16).  96-row tiles serve grids whose 128-row count
-// just exceeds one wave of workgroups (two tiles on a few CUs would set the
-// kernel time): 340 tiles of 96 at two per CU cost 3/4 of that.
+// BM (160, 128, 96 or 64) rows per tile: two waves along M hold BM/2 rows
+// each (MB = BM/32 blocks of 16).  160- and 96-row tiles serve grids whose
+// 128-row count just exceeds one wave of workgroups (two tiles on a few CUs
+// would set the kernel time): 160-row tiles one per CU where they fit one
+// wave, else 96-row tiles two per CU (340 of them cost 3/4 of that).
 template <int EPI, int NS, int NSTC, int BM = TBM>
 __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   using T = bf16_t;
@@ -672,13 +673,14 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   // BM / 32: 16-row blocks per wave, and A copies (8 rows each) per wave per
   // stage
   static_assert(NS == 2 || NS == 4, "two or four stages");
-  static_assert(BM == 128 || BM == 96 || BM == 64, "128-, 96- or 64-row tiles");
+  static_assert(BM == 160 || BM == 128 || BM == 96 || BM == 64, "160-, 128-, 96- or 64-row tiles");
   constexpr int CPS = BM / 32 + 4;  // copy instructions per wave per stage
-  // stages sized for 128 rows (a 96-row tile uses 28 of the 32 KB)
-  __shared__ __attribute__((aligned(16))) unsigned char st0[DSTAGE];
-  __shared__ __attribute__((aligned(16))) unsigned char st1[DSTAGE];
-  __shared__ __attribute__((aligned(16))) unsigned char st2[NS == 4 ? DSTAGE : 16];
-  __shared__ __attribute__((aligned(16))) unsigned char st3[NS == 4 ? DSTAGE : 16];
+  // stages sized for at least 128 rows (a 96-row tile uses 28 of the 32 KB)
+  constexpr int STB = ((BM > TBM ? BM : TBM) + TBN) * DROWB;
+  __shared__ __attribute__((aligned(16))) unsigned char st0[STB];
+  __shared__ __attribute__((aligned(16))) unsigned char st1[STB];
+  __shared__ __attribute__((aligned(16))) unsigned char st2[NS == 4 ? STB : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char st3[NS == 4 ? STB : 16];
 
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
@@ -715,7 +717,7 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   // 8*(NA*w + j) + (lane >> 3) of A (j < NA) or 8*(4w + j - NA) + (lane >> 3)
   // of B (j >= NA); physical chunk lane & 7 holds logical chunk
   // (lane & 7) ^ swizzle(row)
-  const T* gsrc[8];  // the first BM/32 + 4 are used (a bound that depends on BM breaks the lambda capture)
+  const T* gsrc[9];  // the first BM/32 + 4 are used (a bound that depends on BM breaks the lambda capture)
   {
     const int rr = lane >> 3, pc = lane & 7;
 #pragma unroll
@@ -1345,6 +1347,15 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
     // given a range past K: its range is then K).
     const int kr1 = a.splits == 1 ? a.K : (a.K == a.k_per_split * a.splits ? a.k_per_split : 0);
     const int nst = kr1 % DST == 0 ? kr1 / DST : 0;
+    // just over one wave of 128-row tiles with a 16-stage K range: 160-row
+    // tiles on the four-stage pipeline when they fit one wave, one per CU
+    // (QKV at 32 envs: 220 workgroups instead of 340 96-row ones two per CU,
+    // 23.5 -> 21.2 us; the two-stage 160-row kernel took 26.6 us)
+    const int total160 = nx * ((a.M + 159) / 160) * a.batch * a.splits;
+    if (total > 256 && total160 <= 256 && nst == 16) {
+      RFX_LAUNCH((gemm_dma<EPI, 4, 16, 160>), dim3((total160 + 7) / 8 * 8), dim3(256), 0, s, a);
+      return;
+    }
     if (total > 256) {
       // just over one wave of 128-row tiles: 96-row tiles, two per CU, when
       // they fit in two waves' worth (the busiest CU then holds 2 x 96 rows

@@ -382,3 +382,27 @@ def test_engine_waits_for_inputs_made_on_the_callers_stream():
     np.testing.assert_allclose(K[0, 0, :cfg.static_len], ks[:, 0], rtol=1e-5, atol=1e-5)
     np.testing.assert_allclose(Vt[0, 0, :, :cfg.static_len], vs[:, 0].T, rtol=0, atol=0)
     eng.close()
+
+
+def test_gemm_160_row_tiles_bf16():
+    """32 envs of 51 rows (M = 1632) at width 1024 with eight 256-wide heads:
+    the packed QKV GEMM (N = 2560, K = 1024, RoPE epilogue) has 260 128-row
+    tiles, just over one wave, and takes 220 160-row tiles on the four-stage
+    pipeline.  Envs 0, 17 and 31 (the last, partial tile) against the oracle."""
+    cfg = RAGGED.replace(name="tile160_bf16", dtype="bf16", batch=32, action_horizon=50, width=1024,
+                         mlp_dim=512, n_q_heads=8, head_dim=256, state_dim=8, action_dim=5, cond_hidden=64,
+                         frame_dim=0, n_layers=1, num_steps=1, window_frames=1, static_len=40, frame_tokens=24)
+    w, sk, sv, frames = _setup(cfg, 1)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    eng.write_frame(frames[0])
+    envs = [0, 17, 31]
+    state, noise = WL.make_state(cfg, 1), WL.make_noise(cfg, 1)
+    got = eng.denoise(state, noise).cpu().numpy()[envs]
+    eng.synchronize()
+    ref = O.denoise_chunk(cfg, w, sk, sv, {0: frames[0]}, 1, state, noise, cfg.taus(), envs=envs)
+    for i, e in enumerate(envs):
+        rel = float(np.linalg.norm(got[i] - ref[i]) / np.linalg.norm(ref[i]))
+        mx = float(np.max(np.abs(got[i] - ref[i])))
+        print(f"160-row tiles env {e}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+        assert rel <= BF16_REL and mx <= BF16_ABS, (e, rel, mx)
+    eng.close()
