@@ -1224,7 +1224,10 @@ __global__ __launch_bounds__(128) void attn_pair_kernel(AttnArgs p) {
 // The partial O_s are fp32 on the fp32 path and bf16 on the bf16 path.
 constexpr int kMaxSplits = 16;
 
-template <typename T, int DH, int VEC>
+// MAXS: the split count it is compiled for (at least p.nsplit): the partials
+// of every split are held in registers at once, so a bound of 16 for two
+// splits would cost the occupancy a memory-bound kernel needs.
+template <typename T, int DH, int VEC, int MAXS>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   static_assert(VEC * sizeof(T) == 16 || VEC * sizeof(T) == 8 || VEC * sizeof(T) == 4, "4-, 8- or 16-byte accesses");
   using Raw = typename std::conditional<VEC * sizeof(T) == 16, uint4,
@@ -1239,10 +1242,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   const int64_t base = (int64_t)b * p.nsplit * p.rows_pad + rq;
   // all loads of this thread are independent: one memory round trip
   // (the raw partials are converted only after every load is issued)
-  float2 ml[kMaxSplits];
-  Raw raw[kMaxSplits];
+  float2 ml[MAXS];
+  Raw raw[MAXS];
 #pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s) {
+  for (int s = 0; s < MAXS; ++s) {
     if (s < p.nsplit) {
       const int64_t prow = base + (int64_t)s * p.rows_pad;
       ml[s] = *reinterpret_cast<const float2*>(p.part_ml + prow * 2);
@@ -1251,7 +1254,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
   }
   float M = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s)
+  for (int s = 0; s < MAXS; ++s)
     if (s < p.nsplit) M = fmaxf(M, ml[s].x);
   const float Mu = (M == -INFINITY) ? 0.f : M;
   float L = 0.f;
@@ -1259,7 +1262,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs p) {
 #pragma unroll
   for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
 #pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s)
+  for (int s = 0; s < MAXS; ++s)
     if (s < p.nsplit) {
       const float w = exp2f(ml[s].x - Mu);
       L += w * ml[s].y;
@@ -1341,6 +1344,18 @@ static void launch_attn_dh(const AttnArgs& a, hipStream_t s) {
   }
 }
 
+template <typename T, int DH, int VEC>
+static void launch_merge_vec(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  if (a.nsplit <= 2)
+    RFX_LAUNCH((attn_merge_kernel<T, DH, VEC, 2>), grid, dim3(256), 0, s, a);
+  else if (a.nsplit <= 4)
+    RFX_LAUNCH((attn_merge_kernel<T, DH, VEC, 4>), grid, dim3(256), 0, s, a);
+  else if (a.nsplit <= 8)
+    RFX_LAUNCH((attn_merge_kernel<T, DH, VEC, 8>), grid, dim3(256), 0, s, a);
+  else
+    RFX_LAUNCH((attn_merge_kernel<T, DH, VEC, kMaxSplits>), grid, dim3(256), 0, s, a);
+}
+
 template <typename T, int DH>
 static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
   constexpr int V16 = 16 / (int)sizeof(T);
@@ -1348,10 +1363,10 @@ static void launch_merge_dh(const AttnArgs& a, hipStream_t s) {
   const int rows = a.T * a.Hq;
   const int blocks16 = (rows + RPB16 - 1) / RPB16 * a.B;
   if (sizeof(T) == 4 || blocks16 >= 256) {
-    RFX_LAUNCH((attn_merge_kernel<T, DH, V16>), dim3((rows + RPB16 - 1) / RPB16, a.B), dim3(256), 0, s, a);
+    launch_merge_vec<T, DH, V16>(a, dim3((rows + RPB16 - 1) / RPB16, a.B), s);
   } else {
     constexpr int RPB4 = 256 / (DH / 2);
-    RFX_LAUNCH((attn_merge_kernel<T, DH, 2>), dim3((rows + RPB4 - 1) / RPB4, a.B), dim3(256), 0, s, a);
+    launch_merge_vec<T, DH, 2>(a, dim3((rows + RPB4 - 1) / RPB4, a.B), s);
   }
 }
 
