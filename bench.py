@@ -564,7 +564,7 @@ def profile_run(torch, log, name, ticks, stamps=False):
 
 def cpu_baseline(cfg, log):
     """The float64 oracle timed on this host's cores: one full chunk (1 env,
-    10 Euler steps, one frame in the window), median of two runs."""
+    10 Euler steps, one frame in the window), median of four runs (about 12 s)."""
     import numpy as np
 
     from oracle import reflex_oracle as O
@@ -596,7 +596,7 @@ def cpu_baseline(cfg, log):
     state = rng.standard_normal(size=(1, cfg.state_dim))
     noise = rng.standard_normal(size=(1, cfg.action_horizon, cfg.action_dim))
     times = []
-    for _ in range(2):
+    for _ in range(4):
         t0 = time.perf_counter()
         O.denoise_chunk(cfg, w, sk, sv, frames, 1, state, noise, cfg.taus())
         times.append(time.perf_counter() - t0)
@@ -606,7 +606,7 @@ def cpu_baseline(cfg, log):
         limiter.unregister()
     return {"value": 1.0 / sec, "unit": "chunks/s", "cores": cores, "cpu_model": model, "kind": "oracle",
             "sample": "one full pi0_chunk_bf16 chunk (env 0, 10 Euler steps, 48 static + 768 frame "
-                      f"+ 51 dynamic tokens), float64 numpy, median of 2 runs = {sec:.2f} s/chunk"}
+                      f"+ 51 dynamic tokens), float64 numpy, median of 4 runs = {sec:.2f} s/chunk"}
 
 
 def main():
