@@ -406,3 +406,26 @@ def test_gemm_160_row_tiles_bf16():
         print(f"160-row tiles env {e}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
         assert rel <= BF16_REL and mx <= BF16_ABS, (e, rel, mx)
     eng.close()
+
+
+@pytest.mark.parametrize("shape", ["rows320", "width1152"])
+def test_embedding_kernel_every_step_fp32(shape):
+    """Chunks outside the final kernel's fused-embedding range launch the
+    embedding kernel at every Euler step: 5 envs x 64 tokens (320 rows) and
+    one env at width 1152.  fp32 against the oracle."""
+    if shape == "rows320":
+        cfg = RAGGED.replace(name="embed_rows320", batch=5, action_horizon=63, num_steps=3)
+    else:
+        cfg = RAGGED.replace(name="embed_w1152", batch=1, width=1152, mlp_dim=256, num_steps=3)
+    w, sk, sv, frames = _setup(cfg, 2)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    for t in range(2):
+        eng.write_frame(frames[t])
+    state, noise = WL.make_state(cfg, 1), WL.make_noise(cfg, 1)
+    prof = eng.profile(state, noise)
+    assert prof["embed_norm"][1] == cfg.num_steps
+    got = eng.denoise(state, noise).cpu().numpy()
+    eng.synchronize()
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 2, state, noise, cfg.taus())
+    assert np.max(np.abs(got - ref)) <= FP32_TOL, np.max(np.abs(got - ref))
+    eng.close()
