@@ -121,7 +121,9 @@ def _graph_profile(eng, state, noise, reps=3):
     out = {}
     for cls, (_, n) in eager.items():
         if n and cls not in ("frame_proj", "ring_write"):
-            out[cls] = eng.profile_graph(state, noise, [cls], reps=reps)
+            # at least 30 stamped launches per class: a class launched once
+            # per chunk has one boundary calibration per replay
+            out[cls] = eng.profile_graph(state, noise, [cls], reps=max(reps, -(-30 // n)))
     if out.get("attn_merge", (0, 0))[1]:
         ms, _ = eng.profile_graph(state, noise, ["attention", "attn_merge"], reps=reps)
         out["attention_unit"] = (ms, out["attention"][1])

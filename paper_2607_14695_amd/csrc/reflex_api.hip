@@ -1242,11 +1242,12 @@ int reflex_profile_graph(reflex_ctx* ctx, const float* state, const float* noise
   if (khz <= 0) return hip_fail(hipErrorInvalidValue);
 
   // room for three stamps per launch of the chunk (a bound on its launches:
-  // at most 12 per layer and step plus the per-chunk ones)
+  // at most 12 per layer and step plus the per-chunk ones), and one slot for
+  // the two stamps that open the graph
   const reflex_config& c = ctx->cfg;
   const int cap = 3 * (num_steps * (12 * c.n_layers + 8) + 16);
   unsigned long long* stamps = nullptr;
-  e = hipMalloc(&stamps, sizeof(unsigned long long) * cap);
+  e = hipMalloc(&stamps, sizeof(unsigned long long) * (cap + 1));
   if (e != hipSuccess) return hip_fail(e);
   std::vector<unsigned long long> host(cap);
 
@@ -1256,20 +1257,31 @@ int reflex_profile_graph(reflex_ctx* ctx, const float* state, const float* noise
   int rc = REFLEX_OK;
   e = hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal);
   if (e == hipSuccess) {
-    ctx->stamp_mask = class_mask;
-    ctx->stamps = stamps;
-    ctx->stamp_next = 0;
-    ctx->stamp_cap = cap;
-    rc = enqueue_chunk_dispatch(ctx, ctx->ws, state, noise, num_steps, taus, actions_out, false,
-                                REFLEX_MODE_REFLEX, nullptr);
-    ctx->stamp_mask = 0;
-    ctx->stamps = nullptr;
+    // two uncounted stamps open the graph: a measured bracket never starts
+    // at a replay's first node, whose boundary is not the chunk's
+    hipError_t le = hipSuccess;
+    for (int i = 0; le == hipSuccess && i < 2; ++i) {
+      hipLaunchKernelGGL(stamp_kernel, dim3(1), dim3(64), 0, ctx->stream, stamps + cap);
+      le = hipGetLastError();
+    }
+    if (le == hipSuccess) {
+      ctx->stamp_mask = class_mask;
+      ctx->stamps = stamps;
+      ctx->stamp_next = 0;
+      ctx->stamp_cap = cap;
+      rc = enqueue_chunk_dispatch(ctx, ctx->ws, state, noise, num_steps, taus, actions_out, false,
+                                  REFLEX_MODE_REFLEX, nullptr);
+      ctx->stamp_mask = 0;
+      ctx->stamps = nullptr;
+    }
+    // the capture is always ended, whatever failed inside it
     e = hipStreamEndCapture(ctx->stream, &graph);
-    if (e == hipSuccess && rc != REFLEX_OK) (void)hipGraphDestroy(graph);
-    if (e == hipSuccess && rc == REFLEX_OK) {
+    if (e == hipSuccess && (rc != REFLEX_OK || le != hipSuccess)) (void)hipGraphDestroy(graph);
+    if (e == hipSuccess && rc == REFLEX_OK && le == hipSuccess) {
       e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
       (void)hipGraphDestroy(graph);
     }
+    if (e == hipSuccess) e = le;
   }
   const int n = ctx->stamp_next / 3;
   double ticks = 0.0;
