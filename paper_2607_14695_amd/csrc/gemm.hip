@@ -625,7 +625,12 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs p) {
 // stage's copy latency); NS = 4: a ring of four stages, three in flight, one
 // workgroup per CU.  Two stages measured faster at the batch-32 shapes.
 // 16-byte chunks are XOR-swizzled (RFX_GSWZ).  K and the split length must be
-// multiples of 64 (no partial stage to zero-fill).
+// multiples of 64 (no partial stage to zero-fill).  M32: each wave's 64x64
+// block as 2x2 32x32x16 MFMAs (four accumulators) instead of 4x4 16x16x32
+// ones (sixteen): the same LDS fragment bytes and matrix-core cycles in half
+// the instructions, which one wave per SIMD issues closer to the unit's rate
+// (gate|up on the long context 12.9 -> 12.3 us; the 32-stage down projection
+// at 32 envs measured slower, 22.4 -> 22.8 us, and keeps 16x16x32).
 // --------------------------------------------------------------------------
 constexpr int DST = 64;                  // K elements per stage
 constexpr int DROWB = DST * 2;           // bytes per stage row (128)
@@ -666,7 +671,7 @@ constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
 // 128-row count just exceeds one wave of workgroups (two tiles on a few CUs
 // would set the kernel time): 160-row tiles one per CU where they fit one
 // wave, else 96-row tiles two per CU (340 of them cost 3/4 of that).
-template <int EPI, int NS, int NSTC, int BM = TBM>
+template <int EPI, int NS, int NSTC, int BM = TBM, bool M32 = false>
 __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   using T = bf16_t;
   constexpr int PAIR = EpiPair<EPI>::value;
@@ -748,11 +753,31 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
     }
   };
 
-  f32x4_v acc[(BM / 32)][4];
+  static_assert(!M32 || BM % 64 == 0, "32x32 blocks need 32-row wave halves");
+  constexpr int MB2 = M32 ? BM / 64 : 1;  // 32-row blocks per wave
+  f32x4_v acc[(BM / 32)][4];              // 16x16x32: C^T blocks [16-row block][16-column block]
+  f32x16_v acc2[MB2][2];                  // 32x32x16: C^T blocks [32-row block][32-column block]
+  if constexpr (M32) {
 #pragma unroll
-  for (int a = 0; a < (BM / 32); ++a)
+    for (int a = 0; a < MB2; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+      for (int b = 0; b < 2; ++b) acc2[a][b] = f32x16_v{};
+  } else {
+#pragma unroll
+    for (int a = 0; a < (BM / 32); ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+  }
+  // 32x32x16: lane l reads row l & 31 of a 32-row block (32-aligned, so the
+  // swizzle is that of l & 31), chunk 2kk + (l >> 5) of k-step kk; column
+  // block 1 of a pair holds the paired columns of block 0
+  const int r32 = lane & 31, h32 = lane >> 5;
+  int foff2[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) foff2[kk] = r32 * DROWB + ((2 * kk + h32) ^ RFX_GSWZ(r32)) * 16;
+  int brow2[2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) brow2[nb] = PAIR != PAIR_NONE ? nb * 64 + wn * 32 : wn * 64 + nb * 32;
 
   // fragment offsets: row r (r & 7 == r16 & 7), k-step kk of the stage,
   // chunk 4kk + g at (4kk + g) ^ (r16 & 7)
@@ -782,6 +807,23 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
     // stage st-1, whose buffer the next copy overwrites
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (st + NS - 1 < nst) issue(st + NS - 1, nxt);
+    if constexpr (M32) {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        uint4 af[MB2], bf[2];
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          bf[nb] = *reinterpret_cast<const uint4*>(cur + (BM + brow2[nb]) * DROWB + foff2[kk]);
+#pragma unroll
+        for (int mb = 0; mb < MB2; ++mb)
+          af[mb] = *reinterpret_cast<const uint4*>(cur + (wm * (BM / 2) + mb * 32) * DROWB + foff2[kk]);
+#pragma unroll
+        for (int mb = 0; mb < MB2; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb) mfma32_step(acc2[mb][nb], bf[nb], af[mb]);  // C^T blocks
+      }
+      return;
+    }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       uint4 af[(BM / 32)], bf[4];
@@ -824,6 +866,42 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
     }
   }
 
+  if constexpr (M32) {
+    // acc2[mb][nb] holds the transposed 32x32 block: lane l has output row
+    // m0 + wm*BM/2 + mb*32 + (l & 31) and, for q4 < 4, the four consecutive
+    // columns 8*q4 + 4*(l >> 5) .. +3 of column block nb
+#pragma unroll
+    for (int mb = 0; mb < MB2; ++mb) {
+      const int grow = m0 + wm * (BM / 2) + mb * 32 + r32;
+      if (grow >= p.M) continue;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        if (PAIR != PAIR_NONE) {
+          const int gcol = n0 + wn * 32 + 8 * q4 + 4 * h32;
+          const float v[4] = {acc2[mb][0][4 * q4], acc2[mb][0][4 * q4 + 1], acc2[mb][0][4 * q4 + 2],
+                              acc2[mb][0][4 * q4 + 3]};
+          const float u[4] = {acc2[mb][1][4 * q4], acc2[mb][1][4 * q4 + 1], acc2[mb][1][4 * q4 + 2],
+                              acc2[mb][1][4 * q4 + 3]};
+          epilogue_store4<EPI>(p, z, split, grow, gcol, v, u);
+        } else {
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb) {
+            const int gcol = n0 + wn * 64 + nb * 32 + 8 * q4 + 4 * h32;
+            const float v[4] = {acc2[mb][nb][4 * q4], acc2[mb][nb][4 * q4 + 1], acc2[mb][nb][4 * q4 + 2],
+                                acc2[mb][nb][4 * q4 + 3]};
+            if (gcol + 3 < p.N) {
+              epilogue_store4<EPI>(p, z, split, grow, gcol, v, v);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (gcol + e < p.N) epilogue_store<EPI, T>(p, z, split, grow, gcol + e, v[e], 0.f);
+            }
+          }
+        }
+      }
+    }
+    return;
+  }
   // acc[mb][nb] holds the transposed 16x16 block: lane (r16, g) has output
   // row m0 + wm*64 + mb*16 + r16, columns 4g .. 4g+3 of column block nb
 #pragma unroll
@@ -1374,10 +1452,10 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
       const bool t64 = total64 <= 256;
       if (nst == 8) {
         if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 8, 64>), g64, dim3(256), 0, s, a);
-        else RFX_LAUNCH((gemm_dma<EPI, 4, 8>), g128, dim3(256), 0, s, a);
+        else RFX_LAUNCH((gemm_dma<EPI, 4, 8, 128, true>), g128, dim3(256), 0, s, a);
       } else if (nst == 16) {
         if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 16, 64>), g64, dim3(256), 0, s, a);
-        else RFX_LAUNCH((gemm_dma<EPI, 4, 16>), g128, dim3(256), 0, s, a);
+        else RFX_LAUNCH((gemm_dma<EPI, 4, 16, 128, true>), g128, dim3(256), 0, s, a);
       } else {
         if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 32, 64>), g64, dim3(256), 0, s, a);
         else RFX_LAUNCH((gemm_dma<EPI, 4, 32>), g128, dim3(256), 0, s, a);

@@ -408,6 +408,31 @@ def test_gemm_160_row_tiles_bf16():
     eng.close()
 
 
+def test_gemm_32x32_blocks_bf16():
+    """41 envs of 51 rows (M = 2091) at width 512 with six 128-wide heads: the
+    packed QKV (N = 1024, RoPE epilogue) and gate|up (gated GELU) GEMMs have
+    8 column tiles of 17 128-row tiles, one wave, but 264 64-row ones, so they
+    take 128-row tiles on the four-stage pipeline with 32x32x16 MFMAs (8
+    stages).  Envs 0, 20 and 40 (the last, partial tile) against the oracle."""
+    cfg = RAGGED.replace(name="mfma32_bf16", dtype="bf16", batch=41, action_horizon=50, width=512,
+                         mlp_dim=512, n_q_heads=6, head_dim=128, state_dim=8, action_dim=5, cond_hidden=64,
+                         frame_dim=0, n_layers=1, num_steps=2, window_frames=1, static_len=40, frame_tokens=24)
+    w, sk, sv, frames = _setup(cfg, 1)
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    eng.write_frame(frames[0])
+    envs = [0, 20, 40]
+    state, noise = WL.make_state(cfg, 1), WL.make_noise(cfg, 1)
+    got = eng.denoise(state, noise).cpu().numpy()[envs]
+    eng.synchronize()
+    ref = O.denoise_chunk(cfg, w, sk, sv, {0: frames[0]}, 1, state, noise, cfg.taus(), envs=envs)
+    for i, e in enumerate(envs):
+        rel = float(np.linalg.norm(got[i] - ref[i]) / np.linalg.norm(ref[i]))
+        mx = float(np.max(np.abs(got[i] - ref[i])))
+        print(f"32x32 blocks env {e}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+        assert rel <= BF16_REL and mx <= BF16_ABS, (e, rel, mx)
+    eng.close()
+
+
 @pytest.mark.parametrize("shape", ["rows320", "width1152"])
 def test_embedding_kernel_every_step_fp32(shape):
     """Chunks outside the final kernel's fused-embedding range launch the
