@@ -192,6 +192,22 @@ def release_grid(tick, ticks, period_s, now=time.perf_counter, sleep=time.sleep)
     return lat
 
 
+
+def _on(eng, torch):
+    """Make the engine's stream the current stream for the measurements that
+    follow (ReflexEngine.current: the calls then leave no wait for the
+    engine's work pending in another hardware queue while it runs); returns
+    the stream that was current."""
+    prev = torch.cuda.current_stream()
+    torch.cuda.set_stream(eng.stream)
+    return prev
+
+
+def _off(eng, prev, torch):
+    eng.synchronize()
+    torch.cuda.set_stream(prev)
+
+
 def _stream_ticks(eng, frames, state, noise, ticks, warmup, torch, period_s=0.020):
     """Tick latency on the 20 ms release grid (release_grid): frame write +
     denoise, synced on the device."""
@@ -288,15 +304,16 @@ def _pipeline(cfg, w, sk, sv, frames, state, noise, torch, rounds, warmup):
     "pipelined" = the write on the engine's second stream while the chunk, on
     the engine stream, reads the frames written before this tick's frame
     (asynchronous pipeline, Section 3.3).  Each tick is bracketed by events on
-    the caller's stream, which waits for both engine streams at the end (device
-    time), and by the host clock (tick latency including launch).  The window a
-    chunk read is checked on every tick; the write and the chunk alone are
-    timed the same way."""
+    the engine stream, made current, which waits for the writer stream at the
+    end (device time), and by the host clock (tick latency including launch).
+    The window a chunk read is checked on every tick; the write and the chunk
+    alone are timed the same way."""
     import numpy as np
 
     from paper_2607_14695_amd.reflex import ReflexEngine
 
     eng = ReflexEngine(cfg.replace(spare_slot=1), w, sk, sv)
+    prev = _on(eng, torch)
     cur = torch.cuda.current_stream()
     for i in range(cfg.window_frames):
         eng.write_frame(frames[i % len(frames)])
@@ -350,6 +367,7 @@ def _pipeline(cfg, w, sk, sv, frames, state, noise, torch, rounds, warmup):
     else:
         res["write_hidden_fraction"] = None
     res["rounds"] = rounds
+    _off(eng, prev, torch)
     eng.close()
     return res
 
@@ -365,13 +383,14 @@ def _scheduler(cfg, w, sk, sv, frames, noise, torch, chunks):
     from paper_2607_14695_amd.reflex import ReflexEngine
 
     eng = ReflexEngine(cfg.replace(spare_slot=1), w, sk, sv)
+    prev = _on(eng, torch)
     out = {}
     for strategy in OV.STRATEGIES:
         pol = OV.EnginePolicy(eng, frames, lambda i: noise)
         sch = OV.OverlapScheduler(pol, cfg.action_horizon, 0.020, strategy=strategy, frame_period_s=0.020)
         st = sch.run(OV.FirstOrderRobot(np.zeros(cfg.state_dim), alpha=0.5), chunks * cfg.action_horizon)
         out[strategy] = st.summary()
-    eng.synchronize()
+    _off(eng, prev, torch)
     eng.close()
     return out
 
@@ -404,6 +423,7 @@ def sweep_window(torch, log, windows=(1, 2, 5, 10, 20, 50)):
     for W in windows:
         cfg = base.replace(window_frames=W)
         eng = ReflexEngine(cfg, w, sk, sv)
+        prev = _on(eng, torch)
         for i in range(W):
             eng.write_frame(frames[i % len(frames)])
         r = {"window_frames": W, "cached_tokens": cfg.static_len + W * cfg.frame_tokens}
@@ -422,6 +442,7 @@ def sweep_window(torch, log, windows=(1, 2, 5, 10, 20, 50)):
             eng.denoise(state, noise)
 
         r["tick_ms"] = _event_ms(eng, torch, tick, 10)
+        _off(eng, prev, torch)
         eng.close()
         log(f"window {r}")
         rows.append(r)
@@ -442,9 +463,11 @@ def sweep_chunk(torch, log, horizons=(25, 50, 75, 100)):
             cfg = base.replace(action_horizon=H)
             noise = torch.randn((cfg.batch, H, cfg.action_dim), device="cuda")
             eng = ReflexEngine(cfg, w, sk, sv)
+            prev = _on(eng, torch)
             for i in range(cfg.window_frames):
                 eng.write_frame(frames[i])
             ms = _event_ms(eng, torch, lambda: eng.denoise(state, noise), 5)
+            _off(eng, prev, torch)
             r = {"workload": name, "batch": cfg.batch, "action_horizon": H, "dynamic_tokens": H + 1,
                  "chunk_ms": ms, "denoise_step_us": round(ms / cfg.num_steps * 1e3, 1),
                  "actions_per_s": round(cfg.batch * H / (ms / 1e3), 1)}
@@ -546,6 +569,7 @@ def profile_run(torch, log, name, ticks, stamps=False):
     w, sk, sv, frames, state, noise = _device_inputs(cfg, torch)
     eng = ReflexEngine(cfg, w, sk, sv)
     _warm_clocks(torch)
+    prev = _on(eng, torch)
     for i in range(cfg.window_frames):
         eng.write_frame(frames[i % len(frames)])
     for i in range(ticks):
@@ -560,6 +584,7 @@ def profile_run(torch, log, name, ticks, stamps=False):
         gp = _graph_profile(eng, state, noise)
         rec["stamp_us"] = {k: round(v[0] / v[1] * 1e3, 3) for k, v in gp.items() if v[1]}
         log(f"profile run {name}: in-graph class timing done")
+    _off(eng, prev, torch)
     eng.close()
     return rec
 
@@ -685,6 +710,7 @@ def main():
     cfg = WL.CONFIGS["pi0_chunk_bf16"]
     w, sk, sv, frames, state, noise = _device_inputs(cfg, torch)
     eng = ReflexEngine(cfg, w, sk, sv)
+    prev = _on(eng, torch)
     log("engine ready (pi0_chunk_bf16)")
     tick_s = _time_ticks(eng, frames, state, noise, args.steps, args.warmup, torch)
     log(f"tick {tick_s * 1e3:.3f} ms")
@@ -717,6 +743,7 @@ def main():
     kernel_avg_us = _avg_us(prof)
     n_ms, n_n = prof["resid_norm"]
     norm_gbs = _norm_bytes(cfg) / (n_ms / n_n / 1e3) / 1e9
+    _off(eng, prev, torch)
     eng.close()
     del eng, w
 
@@ -725,6 +752,7 @@ def main():
         c32 = WL.CONFIGS["pi0_batch32_bf16"]
         w32, sk32, sv32, fr32, st32, nz32 = _device_inputs(c32, torch, seed=1)
         e32 = ReflexEngine(c32, w32, sk32, sv32)
+        prev = _on(e32, torch)
         steps32 = max(3, args.steps // 3)
         t32 = _time_ticks(e32, fr32, st32, nz32, steps32, 2, torch)
         c32s = _time_ticks(e32, fr32, st32, nz32, steps32, 1, torch, denoise_only=True)
@@ -770,6 +798,7 @@ def main():
         if not args.no_baselines:
             b32["strategies"] = _mode_chunks(e32, st32, nz32, torch, 3)
             log(f"b32 strategies: {b32['strategies']}")
+        _off(e32, prev, torch)
         e32.close()
         if not args.no_pipeline:
             b32["pipeline"] = _pipeline(c32, w32, sk32, sv32, fr32, st32, nz32, torch, 10, 2)
@@ -783,6 +812,7 @@ def main():
         cl = WL.CONFIGS["pi0_long_bf16"]
         wl, skl, svl, frl, stl, nzl = _device_inputs(cl, torch, seed=3)
         el = ReflexEngine(cl, wl, skl, svl)
+        prev = _on(el, torch)
         for f in range(cl.window_frames):
             el.write_frame(frl[f % len(frl)])
         cls_ = _time_ticks(el, frl, stl, nzl, max(3, args.steps // 3), 1, torch, denoise_only=True)
@@ -806,6 +836,7 @@ def main():
                                                        load_traffic(tfl, "attention"))}
         for k in ("gemm_qkv", "gemm_gate_up", "gemm_o", "gemm_down"):
             long_ctx["roofline"][k] = _roofline(k, "mfma", *bfl[k], pl[k][0] / pl[k][1] / 1e3, load_traffic(tfl, k))
+        _off(el, prev, torch)
         el.close()
         del el, wl
         log(f"long context: {long_ctx}")
@@ -815,6 +846,7 @@ def main():
         cs = WL.CONFIGS["pi0_stream_bf16"]
         ws_, sks, svs, frs, sts, nzs = _device_inputs(cs, torch, seed=2)
         es = ReflexEngine(cs, ws_, sks, svs)
+        prev = _on(es, torch)
         if not args.no_latency:
             stream = _stream_ticks(es, frs, sts, nzs, cs.ticks, 5, torch)
             stream["workload"] = ("pi0_stream_bf16: 1 env, 768-token frames of width 2048 through the per-layer "
@@ -831,6 +863,7 @@ def main():
             pst = es.profile(sts, nzs, mode="standard")
             strategies["standard_class_ms"] = {k: round(v[0], 4) for k, v in pst.items() if v[1]}
             log(f"strategies: {strategies}")
+        _off(es, prev, torch)
         es.close()
         if not args.no_pipeline:
             pipeline = _pipeline(cs, ws_, sks, svs, frs, sts, nzs, torch, 30, 3)

@@ -244,6 +244,20 @@ class ReflexEngine:
         return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(self.device)
 
     # -- API -----------------------------------------------------------------
+    def current(self):
+        """Context manager making the engine's stream the caller's current
+        stream.
+
+        Every call orders the engine's stream after the caller's current stream
+        and the caller's stream after the engine's work.  With a caller stream
+        of its own, the second ordering leaves a wait for the engine's event in
+        another hardware queue for as long as that work runs, and the chunk's
+        kernels then run with longer gaps between them: a batch-1 chunk took
+        9.78 ms against 8.73 ms with the orderings on the engine's own stream
+        (32 envs 28.8 against 28.4 ms, the long context 18.5 against 17.8 ms).
+        Inside this context both orderings stay on the one stream."""
+        return self.torch.cuda.stream(self.stream)
+
     def _enter(self):
         """Order the engine stream after the caller's current stream."""
         caller = self.torch.cuda.current_stream(self.device)

@@ -146,6 +146,32 @@ def test_tiny_graph_replay_is_deterministic(tiny):
     eng.close()
 
 
+def test_tiny_engine_stream_current(tiny):
+    """Calls made with the engine's own stream current (ReflexEngine.current)
+    return the same actions, bit for bit, as calls from the default stream, and
+    the oracle's within the fp32 bound; frame writes inside the context reach
+    the chunks outside it."""
+    cfg, w, sk, sv, frames = tiny
+    eng = R.ReflexEngine(cfg, w, sk, sv)
+    default = torch.cuda.current_stream()
+    eng.write_frame(frames[0])
+    state, noise = WL.make_state(cfg, 1), WL.make_noise(cfg, 1)
+    ref_gpu = eng.denoise(state, noise).cpu().numpy().copy()
+    with eng.current():
+        assert torch.cuda.current_stream() == eng.stream
+        got = eng.denoise(state, noise).clone()
+        eng.write_frame(frames[1])
+        got2 = eng.denoise(state, noise).clone()
+    assert torch.cuda.current_stream() == default
+    eng.synchronize()
+    assert np.array_equal(got.cpu().numpy(), ref_gpu)
+    after = eng.denoise(state, noise).cpu().numpy()
+    assert np.array_equal(after, got2.cpu().numpy())
+    ref = O.denoise_chunk(cfg, w, sk, sv, frames, 2, state, noise, cfg.taus())
+    assert np.max(np.abs(after - ref)) <= FP32_TOL
+    eng.close()
+
+
 def test_tiny_scale_only_and_custom_schedule():
     cfg = WL.CONFIGS["tiny_fp32"].replace(mod_mode="scale_only", num_steps=5,
                                           tau_schedule=(1.0, 0.97, 0.6, 0.3, 0.02, 0.0))
