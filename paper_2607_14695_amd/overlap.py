@@ -277,7 +277,10 @@ class EnginePolicy:
 
     def launch(self, state):
         torch = self.torch
-        st = torch.as_tensor(np.asarray(state, dtype=np.float32)[None], device=self.eng.device)
+        # a host array: the engine copies it into one persistent device buffer,
+        # so every chunk replays the same captured graph (a new device tensor
+        # per launch would be a new pointer, and a new capture)
+        st = np.ascontiguousarray(np.asarray(state, dtype=np.float32)[None])
         noise = self.noise_fn(self.launched)
         self.launched += 1
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
