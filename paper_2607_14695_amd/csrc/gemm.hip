@@ -671,15 +671,25 @@ constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
 // 128-row count just exceeds one wave of workgroups (two tiles on a few CUs
 // would set the kernel time): 160-row tiles one per CU where they fit one
 // wave, else 96-row tiles two per CU (340 of them cost 3/4 of that).
-template <int EPI, int NS, int NSTC, int BM = TBM, bool M32 = false>
-__global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
+//
+// KW = 2 (160-row tiles): eight waves, two per output block, each taking one
+// of the two 32-wide k-steps of every stage, so that each SIMD holds two
+// waves and one's MFMAs run while the other waits on LDS; the two partial
+// blocks are summed through LDS at the end.  QKV at 32 envs: 21.8 -> 18.3 us.
+// On the 128-row (16x16 or 32x32 blocks) and 64-row tiles it was not faster
+// (32 envs: output projection 15.1 -> 15.5, down 23.1 -> 23.1 us; long
+// context: output projection 7.5 -> 8.2, down 10.3 -> 10.7 us).
+template <int EPI, int NS, int NSTC, int BM = TBM, bool M32 = false, int KW = 1>
+__global__ __launch_bounds__(256 * KW) void gemm_dma(GemmArgs p) {
   using T = bf16_t;
   constexpr int PAIR = EpiPair<EPI>::value;
   // BM / 32: 16-row blocks per wave, and A copies (8 rows each) per wave per
   // stage
   static_assert(NS == 2 || NS == 4, "two or four stages");
   static_assert(BM == 160 || BM == 128 || BM == 96 || BM == 64, "160-, 128-, 96- or 64-row tiles");
-  constexpr int CPS = BM / 32 + 4;  // copy instructions per wave per stage
+  static_assert(KW == 1 || (KW == 2 && NS == 4 && NSTC > 0 && !M32), "K-split waves: unrolled pipeline, 16x16 blocks");
+  constexpr int CPS = BM / 32 + 4;          // copy instructions per output block per stage
+  constexpr int CPW = (CPS + KW - 1) / KW;  // copy instructions per wave per stage
   // stages sized for at least 128 rows (a 96-row tile uses 28 of the 32 KB)
   constexpr int STB = ((BM > TBM ? BM : TBM) + TBN) * DROWB;
   __shared__ __attribute__((aligned(16))) unsigned char st0[STB];
@@ -689,7 +699,10 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
 
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
-  const int wm = wave >> 1, wn = wave & 1;
+  // output block wq (2 x 2 over the tile); with KW = 2 two waves share it,
+  // wave wk taking k-step wk (elements 32wk .. 32wk + 31) of every stage
+  const int wq = wave & 3, wk = wave >> 2;
+  const int wm = wq >> 1, wn = wq & 1;
   int bx, by, bz;
   if (!dma_tile<PAIR, BM>(p, bx, by, bz)) return;
   const int z = bz / p.splits, split = bz % p.splits;
@@ -722,15 +735,24 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   // 8*(NA*w + j) + (lane >> 3) of A (j < NA) or 8*(4w + j - NA) + (lane >> 3)
   // of B (j >= NA); physical chunk lane & 7 holds logical chunk
   // (lane & 7) ^ swizzle(row)
-  const T* gsrc[9];  // the first BM/32 + 4 are used (a bound that depends on BM breaks the lambda capture)
+  // The copies of output block wq are split over its KW waves: wave wk issues
+  // instructions j = wk*CPW + i.  With KW = 2 and an odd count the second
+  // wave's last instruction repeats its previous one (same bytes to the same
+  // place), so every wave issues CPW copies per stage and waits on one count.
+  const T* gsrc[9];  // the first CPW are used (a bound that depends on BM breaks the lambda capture)
+  int lrow[9];       // LDS stage row of copy i (wave-uniform)
   {
     const int rr = lane >> 3, pc = lane & 7;
 #pragma unroll
-    for (int j = 0; j < (BM / 32) + 4; ++j) {
-      const int row = (j < (BM / 32) ? 8 * ((BM / 32) * wave + j) : 8 * (4 * wave + j - (BM / 32))) + rr;
+    for (int i = 0; i < CPW; ++i) {
+      const int j = KW == 1 ? i : min(wk * CPW + i, CPS - 1);
+      const bool isa = j < (BM / 32);
+      const int row0 = isa ? 8 * ((BM / 32) * wq + j) : 8 * (4 * wq + j - (BM / 32));
+      const int row = row0 + rr;
+      lrow[i] = isa ? row0 : BM + row0;
       const int lc = pc ^ RFX_GSWZ(row);
-      if (j < (BM / 32)) {
-        gsrc[j] = A + (int64_t)min(m0 + row, p.M - 1) * p.lda + kbeg + lc * 8;
+      if (isa) {
+        gsrc[i] = A + (int64_t)min(m0 + row, p.M - 1) * p.lda + kbeg + lc * 8;
       } else {
         int brw;
         if (PAIR != PAIR_NONE) {
@@ -739,7 +761,7 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
         } else {
           brw = min(n0 + row, p.N - 1);
         }
-        gsrc[j] = B + (int64_t)brw * p.ldb + kbeg + lc * 8;
+        gsrc[i] = B + (int64_t)brw * p.ldb + kbeg + lc * 8;
       }
     }
   }
@@ -747,10 +769,7 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   auto issue = [&](int st, unsigned char* buf) __attribute__((always_inline)) {
     const int k0 = st * DST;
 #pragma unroll
-    for (int j = 0; j < (BM / 32) + 4; ++j) {
-      const int row = j < (BM / 32) ? 8 * ((BM / 32) * wave + j) : BM + 8 * (4 * wave + j - (BM / 32));
-      __builtin_amdgcn_global_load_lds(gsrc[j] + k0, buf + row * DROWB, 16, 0, 0);
-    }
+    for (int i = 0; i < CPW; ++i) __builtin_amdgcn_global_load_lds(gsrc[i] + k0, buf + lrow[i] * DROWB, 16, 0, 0);
   };
 
   static_assert(!M32 || BM % 64 == 0, "32x32 blocks need 32-row wave halves");
@@ -781,9 +800,12 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
 
   // fragment offsets: row r (r & 7 == r16 & 7), k-step kk of the stage,
   // chunk 4kk + g at (4kk + g) ^ (r16 & 7)
-  int foff[2];
+  int foff[2 / KW];  // k-step kk = kh + wk*2/KW
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) foff[kk] = r16 * DROWB + ((4 * kk + g) ^ RFX_GSWZ(r16)) * 16;
+  for (int kh = 0; kh < 2 / KW; ++kh) {
+    const int kk = kh + wk * (2 / KW);
+    foff[kh] = r16 * DROWB + ((4 * kk + g) ^ RFX_GSWZ(r16)) * 16;
+  }
   int brow_l[4];
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb) {
@@ -798,9 +820,9 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
   auto step = [&](int st, const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt)
                   __attribute__((always_inline)) {
     if (NS == 4 && st + 2 < nst)
-      __builtin_amdgcn_s_waitcnt(vmcnt_enc(2 * CPS));
+      __builtin_amdgcn_s_waitcnt(vmcnt_enc(2 * CPW));
     else if (NS == 4 && st + 1 < nst)
-      __builtin_amdgcn_s_waitcnt(vmcnt_enc(CPS));
+      __builtin_amdgcn_s_waitcnt(vmcnt_enc(CPW));
     else
       __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
     // every wave's share of stage st is in LDS and every wave has finished
@@ -825,14 +847,14 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
       return;
     }
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int kh = 0; kh < 2 / KW; ++kh) {
       uint4 af[(BM / 32)], bf[4];
 #pragma unroll
       for (int mb = 0; mb < (BM / 32); ++mb)
-        af[mb] = *reinterpret_cast<const uint4*>(cur + (wm * (BM / 2) + mb * 16) * DROWB + foff[kk]);
+        af[mb] = *reinterpret_cast<const uint4*>(cur + (wm * (BM / 2) + mb * 16) * DROWB + foff[kh]);
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb)
-        bf[nb] = *reinterpret_cast<const uint4*>(cur + (BM + brow_l[nb]) * DROWB + foff[kk]);
+        bf[nb] = *reinterpret_cast<const uint4*>(cur + (BM + brow_l[nb]) * DROWB + foff[kh]);
 #pragma unroll
       for (int mb = 0; mb < (BM / 32); ++mb)
 #pragma unroll
@@ -866,6 +888,66 @@ __global__ __launch_bounds__(256) void gemm_dma(GemmArgs p) {
     }
   }
 
+  if constexpr (KW == 2) {
+    // The two waves of an output block hold partial sums over their halves of
+    // every stage.  Each finalizes half of the block's columns: it hands the
+    // other half to its partner through LDS (the stage buffer numbered like
+    // the block: after this barrier every copy has landed and every fragment
+    // read is done) and adds what the partner hands over.  a + b = b + a, so
+    // both orders give the same sum.
+    constexpr int NX = (BM / 32) * 2;  // float4s handed over per lane
+    static_assert(2 * NX * 64 * 16 <= STB, "hand-over fits one stage buffer");
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    unsigned char* const xb = wq == 0 ? st0 : (wq == 1 ? st1 : (wq == 2 ? st2 : st3));
+    float4* const sendp = reinterpret_cast<float4*>(xb) + wk * (NX * 64) + lane;
+    const float4* const recvp = reinterpret_cast<const float4*>(xb) + (1 - wk) * (NX * 64) + lane;
+    // wave wk finalizes two of the four column blocks, slot s being block
+    // nbA(s) for wave 0 and nbB(s) for wave 1 (with pairs: one block and its
+    // paired columns)
+#pragma unroll
+    for (int mb = 0; mb < (BM / 32); ++mb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int nbA = PAIR != PAIR_NONE ? 2 * s2 : s2, nbB = PAIR != PAIR_NONE ? 1 + 2 * s2 : 2 + s2;
+        const f32x4_v v = wk ? acc[mb][nbA] : acc[mb][nbB];
+        sendp[(mb * 2 + s2) * 64] = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    f32x4_v fin[(BM / 32)][2];
+#pragma unroll
+    for (int mb = 0; mb < (BM / 32); ++mb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int nbA = PAIR != PAIR_NONE ? 2 * s2 : s2, nbB = PAIR != PAIR_NONE ? 1 + 2 * s2 : 2 + s2;
+        const float4 r = recvp[(mb * 2 + s2) * 64];
+        fin[mb][s2] = (wk ? acc[mb][nbB] : acc[mb][nbA]) + f32x4_v{r.x, r.y, r.z, r.w};
+      }
+#pragma unroll
+    for (int mb = 0; mb < (BM / 32); ++mb) {
+      const int grow = m0 + wm * (BM / 2) + mb * 16 + r16;
+      if (grow >= p.M) continue;
+      if (PAIR != PAIR_NONE) {
+        const int gcol = n0 + wn * 32 + wk * 16 + 4 * g;
+        const float v[4] = {fin[mb][0][0], fin[mb][0][1], fin[mb][0][2], fin[mb][0][3]};
+        const float u[4] = {fin[mb][1][0], fin[mb][1][1], fin[mb][1][2], fin[mb][1][3]};
+        epilogue_store4<EPI>(p, z, split, grow, gcol, v, u);
+      } else {
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const int gcol = n0 + wn * 64 + (2 * wk + s2) * 16 + 4 * g;
+          const float v[4] = {fin[mb][s2][0], fin[mb][s2][1], fin[mb][s2][2], fin[mb][s2][3]};
+          if (gcol + 3 < p.N) {
+            epilogue_store4<EPI>(p, z, split, grow, gcol, v, v);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (gcol + e < p.N) epilogue_store<EPI, T>(p, z, split, grow, gcol + e, v[e], 0.f);
+          }
+        }
+      }
+    }
+    return;
+  }
   if constexpr (M32) {
     // acc2[mb][nb] holds the transposed 32x32 block: lane l has output row
     // m0 + wm*BM/2 + mb*32 + (l & 31) and, for q4 < 4, the four consecutive
@@ -1428,10 +1510,11 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
     // just over one wave of 128-row tiles with a 16-stage K range: 160-row
     // tiles on the four-stage pipeline when they fit one wave, one per CU
     // (QKV at 32 envs: 220 workgroups instead of 340 96-row ones two per CU,
-    // 23.5 -> 21.2 us; the two-stage 160-row kernel took 26.6 us)
+    // 23.5 -> 21.2 us; the two-stage 160-row kernel took 26.6 us), with two
+    // waves per output block (21.8 -> 18.3 us)
     const int total160 = nx * ((a.M + 159) / 160) * a.batch * a.splits;
     if (total > 256 && total160 <= 256 && nst == 16) {
-      RFX_LAUNCH((gemm_dma<EPI, 4, 16, 160>), dim3((total160 + 7) / 8 * 8), dim3(256), 0, s, a);
+      RFX_LAUNCH((gemm_dma<EPI, 4, 16, 160, false, 2>), dim3((total160 + 7) / 8 * 8), dim3(512), 0, s, a);
       return;
     }
     if (total > 256) {

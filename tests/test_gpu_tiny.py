@@ -410,13 +410,22 @@ def test_engine_waits_for_inputs_made_on_the_callers_stream():
     eng.close()
 
 
-def test_gemm_160_row_tiles_bf16():
-    """32 envs of 51 rows (M = 1632) at width 1024 with eight 256-wide heads:
-    the packed QKV GEMM (N = 2560, K = 1024, RoPE epilogue) has 260 128-row
-    tiles, just over one wave, and takes 220 160-row tiles on the four-stage
-    pipeline.  Envs 0, 17 and 31 (the last, partial tile) against the oracle."""
-    cfg = RAGGED.replace(name="tile160_bf16", dtype="bf16", batch=32, action_horizon=50, width=1024,
-                         mlp_dim=512, n_q_heads=8, head_dim=256, state_dim=8, action_dim=5, cond_hidden=64,
+@pytest.mark.parametrize("shape", ["qkv_gelu", "o_proj"])
+def test_gemm_160_row_tiles_bf16(shape):
+    """32 envs of 51 rows (M = 1632), so a GEMM with 20 column tiles has 260
+    128-row tiles, just over one wave, and takes 220 160-row tiles on the
+    four-stage pipeline with two waves per output block (K = 1024).
+    "qkv_gelu": width 1024, eight 256-wide heads: the packed QKV (N = 2560,
+    RoPE epilogue on head pairs) and gate|up (1280 gated-GELU pairs) take that
+    path.  "o_proj": width 2560, four heads: the output projection (N = 2560,
+    K = 1024, one split, fp32 epilogue) takes it.  Envs 0, 17 and 31 (the
+    last, partial tile) against the oracle."""
+    if shape == "qkv_gelu":
+        width, heads, mlp = 1024, 8, 1280
+    else:
+        width, heads, mlp = 2560, 4, 512
+    cfg = RAGGED.replace(name="tile160_" + shape, dtype="bf16", batch=32, action_horizon=50, width=width,
+                         mlp_dim=mlp, n_q_heads=heads, head_dim=256, state_dim=8, action_dim=5, cond_hidden=64,
                          frame_dim=0, n_layers=1, num_steps=1, window_frames=1, static_len=40, frame_tokens=24)
     w, sk, sv, frames = _setup(cfg, 1)
     eng = R.ReflexEngine(cfg, w, sk, sv)
@@ -429,7 +438,7 @@ def test_gemm_160_row_tiles_bf16():
     for i, e in enumerate(envs):
         rel = float(np.linalg.norm(got[i] - ref[i]) / np.linalg.norm(ref[i]))
         mx = float(np.max(np.abs(got[i] - ref[i])))
-        print(f"160-row tiles env {e}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+        print(f"160-row tiles ({shape}) env {e}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
         assert rel <= BF16_REL and mx <= BF16_ABS, (e, rel, mx)
     eng.close()
 
