@@ -672,12 +672,14 @@ constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) |
 // would set the kernel time): 160-row tiles one per CU where they fit one
 // wave, else 96-row tiles two per CU (340 of them cost 3/4 of that).
 //
-// KW = 2 (160-row tiles): eight waves, two per output block, each taking one
-// of the two 32-wide k-steps of every stage, so that each SIMD holds two
-// waves and one's MFMAs run while the other waits on LDS; the two partial
-// blocks are summed through LDS at the end.  QKV at 32 envs: 21.8 -> 18.3 us.
-// On the 128-row (16x16 or 32x32 blocks) and 64-row tiles it was not faster
-// (32 envs: output projection 15.1 -> 15.5, down 23.1 -> 23.1 us; long
+// KW = 2 (160-row tiles; 64-row tiles with a paired epilogue): eight waves,
+// two per output block, each taking one of the two 32-wide k-steps of every
+// stage, so that each SIMD holds two waves and one's MFMAs run while the
+// other waits on LDS; each wave then finalizes half of the block's columns,
+// so the epilogue work is shared too.  QKV at 32 envs: 21.8 -> 18.3 us; QKV
+// of the long context (64-row tiles): 11.7 -> 11.1 us.  With the fp32
+// epilogue on 128-row (16x16 or 32x32 blocks) and 64-row tiles it was not
+// faster (32 envs: output projection 15.1 -> 15.5, down 23.1 -> 23.1 us; long
 // context: output projection 7.5 -> 8.2, down 10.3 -> 10.7 us).
 template <int EPI, int NS, int NSTC, int BM = TBM, bool M32 = false, int KW = 1>
 __global__ __launch_bounds__(256 * KW) void gemm_dma(GemmArgs p) {
@@ -1533,14 +1535,19 @@ static void launch_tiled(const GemmArgs& a, hipStream_t s) {
       const int total64 = nx * ((a.M + 63) / 64) * a.batch * a.splits;
       const dim3 g64((total64 + 7) / 8 * 8), g128((total + 7) / 8 * 8);
       const bool t64 = total64 <= 256;
+      // 64-row tiles with a paired epilogue (RoPE, gated GELU, K/V scatter)
+      // run two waves per output block, as the 160-row tiles do: the QKV of
+      // the long context 11.7 -> 11.1 us; with the fp32 epilogue it was not
+      // faster
+      constexpr int KE = (EPI == EPI_ROPE || EPI == EPI_GELU || EPI == EPI_KV) ? 2 : 1;
       if (nst == 8) {
-        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 8, 64>), g64, dim3(256), 0, s, a);
+        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 8, 64, false, KE>), g64, dim3(256 * KE), 0, s, a);
         else RFX_LAUNCH((gemm_dma<EPI, 4, 8, 128, true>), g128, dim3(256), 0, s, a);
       } else if (nst == 16) {
-        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 16, 64>), g64, dim3(256), 0, s, a);
+        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 16, 64, false, KE>), g64, dim3(256 * KE), 0, s, a);
         else RFX_LAUNCH((gemm_dma<EPI, 4, 16, 128, true>), g128, dim3(256), 0, s, a);
       } else {
-        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 32, 64>), g64, dim3(256), 0, s, a);
+        if (t64) RFX_LAUNCH((gemm_dma<EPI, 4, 32, 64, false, KE>), g64, dim3(256 * KE), 0, s, a);
         else RFX_LAUNCH((gemm_dma<EPI, 4, 32>), g128, dim3(256), 0, s, a);
       }
     } else {

@@ -268,16 +268,17 @@ def test_multi_tile_splits_pipelined_equals_rows16(head_dim):
         e.close()
 
 
-@pytest.mark.parametrize("batch", [1, 8])
-def test_gemm_row_tilings_bf16(batch):
-    """51 dynamic rows per env at width 512 with 128-wide heads.  Eight envs
-    (M = 408 GEMM rows): the packed QKV (RoPE epilogue), gate|up (gated GELU)
-    and down (fp32 output) GEMMs take the tiled path with 64-row tiles on the
-    four-stage pipeline (8 stages of 64 over K = 512).  One env (M = 51): the
-    unsplit skinny GEMMs with few column strips (QKV, gate|up) take their rows
-    in two 32-row halves, and the split merge its 4-byte form.  Every env is
-    checked against the oracle within the bf16 tolerance."""
-    cfg = RAGGED.replace(name=f"rowtile_bf16_b{batch}", dtype="bf16", batch=batch, action_horizon=50, width=512,
+@pytest.mark.parametrize("batch,width", [(1, 512), (8, 512), (8, 2048)])
+def test_gemm_row_tilings_bf16(batch, width):
+    """51 dynamic rows per env with 128-wide heads.  Eight envs (M = 408 GEMM
+    rows): the packed QKV (RoPE epilogue), gate|up (gated GELU) and down (fp32
+    output) GEMMs take the tiled path with 64-row tiles on the four-stage
+    pipeline, 8 stages of 64 over K = 512 at width 512 and 32 stages at width
+    2048 (QKV and gate|up with two waves per output block).  One env (M = 51):
+    the unsplit skinny GEMMs with few column strips (QKV, gate|up) take their
+    rows in two 32-row halves, and the split merge its 4-byte form.  Every env
+    is checked against the oracle within the bf16 tolerance."""
+    cfg = RAGGED.replace(name=f"rowtile_bf16_b{batch}_w{width}", dtype="bf16", batch=batch, action_horizon=50, width=width,
                          mlp_dim=512, n_q_heads=2, head_dim=128, frame_dim=0, n_layers=1, num_steps=2,
                          window_frames=2)
     w, sk, sv, frames = _setup(cfg, 2)
@@ -290,7 +291,7 @@ def test_gemm_row_tilings_bf16(batch):
     ref = O.denoise_chunk(cfg, w, sk, sv, frames, 2, state, noise, cfg.taus())
     rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
     mx = float(np.max(np.abs(got - ref)))
-    print(f"row tilings B={batch}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+    print(f"row tilings B={batch} width {width}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
     assert rel <= BF16_REL and mx <= BF16_ABS, (rel, mx)
     eng.close()
 
