@@ -16,9 +16,10 @@
 // so the dynamic tile is staged exactly like a cached tile.
 //
 // Decomposition and placement.  A workgroup owns one query block of one env
-// (64 rows on the fp32 path; 128 rows as eight 16-row waves, or 32 rows as
-// one wave pair, on the bf16 path) and a contiguous range of 64-key tiles (a
-// key split); the dynamic tile comes last.  All query blocks of one (env,
+// (64 rows on the fp32 path; up to 128 rows as eight 16-row waves, the env's
+// row waves spread evenly over its blocks, or 32 rows as one wave pair, on
+// the bf16 path) and a contiguous range of 64-key tiles (a key split); the
+// dynamic tile comes last.  All query blocks of one (env,
 // split) group share the same K/V tiles, so the 1-D grid is laid out such
 // that a group's blocks are dispatched to the same XCD (workgroups go
 // round-robin over the 8 XCDs): the tiles then come from HBM once and from
@@ -353,8 +354,15 @@ __global__ __launch_bounds__(512) void attn16_kernel(AttnArgs p) {
   const int r16 = lane & 15, g = lane >> 4;
   const int T_ = p.T, Hq = p.Hq;
   const int nrows = T_ * Hq;
-  const int rq = rb * 128 + wave * 16 + r16;
-  const bool qvalid = rq < nrows;
+  // rows of the block as in attn16p_kernel (the row waves of an env spread
+  // evenly over its blocks), so both kernels group the same rows into a wave
+  // and take the same lazy-rescale decisions; waves past the block's count
+  // compute on row 0's data and store nothing
+  const int nrb = p.rows_pad / 128, nw16 = (nrows + 15) / 16;
+  const int wbase = nw16 / nrb, wextra = nw16 - wbase * nrb;
+  const int nwb = wbase + (rb < wextra ? 1 : 0);
+  const int rq = 16 * (rb * wbase + min(rb, wextra)) + wave * 16 + r16;
+  const bool qvalid = wave < nwb && rq < nrows;
   const int iq = qvalid ? rq / Hq : 0;
   const int jq = qvalid ? rq % Hq : 0;
 
@@ -646,8 +654,17 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
   const int r16 = lane & 15, g = lane >> 4;
   const int T_ = p.T, Hq = p.Hq;
   const int nrows = T_ * Hq;
-  const int rq = rb * 128 + wave * 16 + r16;
-  const bool qvalid = rq < nrows;
+  // The ceil(nrows/16) row waves of an env are spread evenly over its blocks
+  // (408 rows: 7, 7, 6 and 6 waves instead of 8, 8, 8 and 2), so no block has
+  // more computing waves than it must.  A wave past its block's count still
+  // issues its share of the tile copies and joins every barrier, but does no
+  // math: the per-tile LDS reads of the busiest block set the kernel's pace.
+  const int nrb = p.rows_pad / 128, nw16 = (nrows + 15) / 16;
+  const int wbase = nw16 / nrb, wextra = nw16 - wbase * nrb;
+  const int nwb = wbase + (rb < wextra ? 1 : 0);  // computing waves of this block
+  const bool active = wave < nwb;
+  const int rq = 16 * (rb * wbase + min(rb, wextra)) + wave * 16 + r16;
+  const bool qvalid = active && rq < nrows;
   const int iq = qvalid ? rq / Hq : 0;
   const int jq = qvalid ? rq % Hq : 0;
 
@@ -841,6 +858,7 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
     lds_barrier();
     if (i + 2 < n) issue_k(t_beg + i + 2, kf);
     issue_v(t_beg + i + 1, vn);
+    if (!active) return;
     f32x4_v s[4];
     scores(kn, s);
     const float m_use = m_run == -INFINITY ? 0.f : m_run;
@@ -858,11 +876,13 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
     lds_barrier();
     if (n > 1) issue_k(t_beg + 1, kbuf1);
     issue_v(t_beg, vbuf0);
-    f32x4_v s[4];
-    scores(kbuf0, s);
-    const float mt = mask_max(t_beg, s);
-    const float psum = expo(s, 0.f, pcur);
-    commit(mt, s, pcur, psum);
+    if (active) {
+      f32x4_v s[4];
+      scores(kbuf0, s);
+      const float mt = mask_max(t_beg, s);
+      const float psum = expo(s, 0.f, pcur);
+      commit(mt, s, pcur, psum);
+    }
     // tile i's K sits in kbuf[i & 1] and its V^T in vbuf[i & 1]
     int i = 0;
     for (; i + 2 < n; i += 2) {
@@ -876,7 +896,7 @@ __global__ __launch_bounds__(512) void attn16p_kernel(AttnArgs p) {
     // last tile: its P.V only
     __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
     lds_barrier();
-    pv((i & 1) ? vbuf1 : vbuf0, pcur);
+    if (active) pv((i & 1) ? vbuf1 : vbuf0, pcur);
   }
 
   if (!qvalid) return;
