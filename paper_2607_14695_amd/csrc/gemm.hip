@@ -903,9 +903,9 @@ __global__ __launch_bounds__(256 * KW) void gemm_dma(GemmArgs p) {
     unsigned char* const xb = wq == 0 ? st0 : (wq == 1 ? st1 : (wq == 2 ? st2 : st3));
     float4* const sendp = reinterpret_cast<float4*>(xb) + wk * (NX * 64) + lane;
     const float4* const recvp = reinterpret_cast<const float4*>(xb) + (1 - wk) * (NX * 64) + lane;
-    // wave wk finalizes two of the four column blocks, slot s being block
-    // nbA(s) for wave 0 and nbB(s) for wave 1 (with pairs: one block and its
-    // paired columns)
+    // wave wk finalizes two of the four column blocks, slot s2 being block
+    // nbA(s2) for wave 0 and nbB(s2) for wave 1 (with pairs: a first-half
+    // block and the block of its paired columns)
 #pragma unroll
     for (int mb = 0; mb < (BM / 32); ++mb)
 #pragma unroll
