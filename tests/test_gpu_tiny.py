@@ -235,19 +235,21 @@ def test_ragged_bf16(head_dim, frame_dim, attn):
     eng.close()
 
 
-@pytest.mark.parametrize("head_dim", [64, 256])
-def test_multi_tile_splits_pipelined_equals_rows16(head_dim):
+@pytest.mark.parametrize("head_dim,heads,horizon", [(64, 2, 7), (256, 2, 7), (64, 8, 50)])
+def test_multi_tile_splits_pipelined_equals_rows16(head_dim, heads, horizon):
     """Key splits of several tiles each: two envs and a 20-frame ring of
     200-token frames give 21 to 65 key tiles over 16 splits, so a split runs
     2, 3, 4 or 5 tiles (odd and even counts, the pipelined kernel's loop and
     its tail).  Frame keys are scaled by 1, 2 and 4 for frames 0-6, 7-13 and
     14-19 (exact in bf16), so tile maxima grow by more than the lazy-rescale
-    threshold inside a split.  The pipelined 16-row kernel must equal the
-    plain one bit for bit (same operations in the same order per row), and
-    both must match the oracle within the bf16 tolerance."""
-    cfg = RAGGED.replace(name=f"multi_tile_{head_dim}", dtype="bf16", batch=2, static_len=40, frame_tokens=200,
-                         window_frames=20, action_horizon=7, n_q_heads=2, head_dim=head_dim, frame_dim=0,
-                         num_steps=2)
+    threshold inside a split.  16 query rows per env fill one wave of one
+    block; 408 rows (51 tokens x 8 heads) spread 26 row waves over four blocks
+    as 7, 7, 6 and 6.  The pipelined 16-row kernel must equal the plain one
+    bit for bit (same rows per wave, same operations in the same order per
+    row), and both must match the oracle within the bf16 tolerance."""
+    cfg = RAGGED.replace(name=f"multi_tile_{head_dim}_{heads}x{horizon}", dtype="bf16", batch=2, static_len=40,
+                         frame_tokens=200, window_frames=20, action_horizon=horizon, n_q_heads=heads,
+                         head_dim=head_dim, frame_dim=0, num_steps=2)
     w, sk, sv, frames = _setup(cfg, 20)
     for f in frames:
         frames[f][:, :, 0] *= float(2 ** (f // 7))
@@ -262,7 +264,8 @@ def test_multi_tile_splits_pipelined_equals_rows16(head_dim):
             ref = O.denoise_chunk(cfg, w, sk, sv, frames, t + 1, state, noise, cfg.taus())
             rel = float(np.linalg.norm(got["rows16p"] - ref) / np.linalg.norm(ref))
             mx = float(np.max(np.abs(got["rows16p"] - ref)))
-            print(f"multi-tile dh={head_dim} frames {t + 1}: rel-L2 {rel:.2e} max-abs {mx:.2e}", flush=True)
+            print(f"multi-tile dh={head_dim} rows {heads * (horizon + 1)} frames {t + 1}: rel-L2 {rel:.2e} "
+                  f"max-abs {mx:.2e}", flush=True)
             assert rel <= BF16_REL and mx <= BF16_ABS, (t, rel, mx)
     for e in engs.values():
         e.close()
