@@ -67,7 +67,6 @@ struct Workspace {
   void* q;
   void* kd;
   void* vdt;
-  int32_t* counters;
   void* o;
   float* part_o;
   float* part_ml;
@@ -82,7 +81,7 @@ struct Workspace {
 constexpr int kWsParts = 22;
 
 struct Plan {
-  int T, M, S, Nqkv, C, R, slots, rows_pad, tpad, nrb, eb;
+  int T, M, S, Nqkv, C, R, slots, rows_pad, tpad, eb;
   SplitK o, down;
   int attn_splits, attn_kernel;
   int max_parts;
@@ -150,7 +149,6 @@ Plan make_plan(const reflex_config* c) {
   p.R = c->static_len + p.slots * c->frame_tokens;
   const int rows = p.T * c->n_q_heads;
   p.rows_pad = (rows + 127) / 128 * 128;
-  p.nrb = p.rows_pad / 64;
   p.tpad = (p.T + 63) / 64 * 64;
   p.o = make_split(p.M, c->n_q_heads * c->head_dim,
                    gemm_pick_splits(p.M, c->width, c->n_q_heads * c->head_dim, eb), eb);
@@ -175,7 +173,7 @@ Plan make_plan(const reflex_config* c) {
   sz[8] = B * (size_t)p.rows_pad * dh * eb;                               // q
   sz[9] = B * (size_t)p.T * dh * eb;                                      // kd
   sz[10] = B * dh * (size_t)p.tpad * eb;                                  // vdt
-  sz[11] = B * (size_t)p.nrb * sizeof(int32_t);                           // counters
+  sz[11] = 0;  // (unused)
   sz[12] = (size_t)p.M * c->n_q_heads * dh * eb;                          // o
   sz[13] = B * p.attn_splits * (size_t)p.rows_pad * dh * sizeof(float);   // part_o
   sz[14] = B * p.attn_splits * (size_t)p.rows_pad * 2 * sizeof(float);    // part_ml
@@ -849,7 +847,6 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
   W.q = base + P.off[8];
   W.kd = base + P.off[9];
   W.vdt = base + P.off[10];
-  W.counters = reinterpret_cast<int32_t*>(base + P.off[11]);
   W.o = base + P.off[12];
   W.part_o = reinterpret_cast<float*>(base + P.off[13]);
   W.part_ml = reinterpret_cast<float*>(base + P.off[14]);
@@ -864,8 +861,8 @@ int reflex_cache_init(const reflex_config* cfg, const reflex_weights* w, void* c
 
   // zeroed cache, as the paper's pre-allocated ring buffer (Appendix B.2)
   hipError_t e = hipMemsetAsync(cache_mem, 0, P.cache_bytes, ctx->stream);
-  // the workspace starts zeroed: tick state, split counters, the zero padding
-  // of the dynamic value columns beyond T
+  // the workspace starts zeroed: tick state and the zero padding of the
+  // dynamic value columns beyond T
   if (e == hipSuccess) e = hipMemsetAsync(workspace_mem, 0, P.ws_bytes, ctx->stream);
   if (e != hipSuccess) {
     delete ctx;
@@ -1117,7 +1114,6 @@ int denoise_launch_static(reflex_ctx* ctx, const float* state, const float* nois
   W.q = b + P.off[8];
   W.kd = b + P.off[9];
   W.vdt = b + P.off[10];
-  W.counters = reinterpret_cast<int32_t*>(b + P.off[11]);
   W.o = b + P.off[12];
   W.part_o = reinterpret_cast<float*>(b + P.off[13]);
   W.part_ml = reinterpret_cast<float*>(b + P.off[14]);
